@@ -1,0 +1,62 @@
+"""Dense element-wise-masked softmax attention in float64.
+
+Test infrastructure only (see the package docstring).
+
+For every batch b, head h and query position i, over all key positions j:
+
+  S_ij   = scale * <q_i, k_j>   if mask(i, j) else -inf
+  m_i    = max_j S_ij
+  l_i    = sum_j exp(S_ij - m_i)
+  out_i  = sum_j exp(S_ij - m_i) * v_j / l_i
+  lse_i  = m_i + ln(l_i)
+
+This is the result the block-sparse kernel must reproduce: masked entries add
+exp(-inf) = 0, empty tiles contribute nothing, and skipping them changes only
+the cost (Sec. 3.1 and Eq. 1). The paper checks its block-sparse outputs
+against a dense implementation of the same pattern in the same way (Sec. 4.2,
+HWT/HNT results). A row with no allowed key (not produced by the paper's
+patterns, where every query attends itself) is defined as out = 0,
+lse = -inf. The log-sum-exp is natural-log.
+
+Inputs are float arrays [B, heads, N, d] already in the order the pattern's
+positions refer to; they are upcast to float64 exactly. ``positions`` maps an
+index on the token axis to the pattern position of that token (default:
+identity); with positions = Hilbert rank this evaluates a Hilbert pattern on
+row-major tensors. ``rows`` restricts the output to those query indices.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import masks
+
+
+def attention(q, k, v, pattern, scale: float, rows=None, positions=None,
+              chunk: int = 256):
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    B, Hh, N, d = q.shape
+    if k.shape != (B, Hh, N, d) or v.shape[:3] != (B, Hh, N):
+        raise ValueError("q, k, v shapes disagree")
+    rows = np.arange(N, dtype=np.int64) if rows is None else np.asarray(rows, dtype=np.int64)
+    pos = np.arange(N, dtype=np.int64) if positions is None else np.asarray(positions, dtype=np.int64)
+    dv = v.shape[3]
+    out = np.zeros((B, Hh, rows.shape[0], dv), dtype=np.float64)
+    lse = np.full((B, Hh, rows.shape[0]), -np.inf, dtype=np.float64)
+    for c0 in range(0, rows.shape[0], chunk):
+        r = rows[c0:c0 + chunk]
+        allow = masks.allowed(pattern, pos[r][:, None], pos[None, :])   # [R, N]
+        any_allowed = allow.any(axis=1)
+        for b in range(B):
+            for h in range(Hh):
+                s = scale * (q[b, h, r] @ k[b, h].T)                      # [R, N]
+                s = np.where(allow, s, -np.inf)
+                m = s.max(axis=1)
+                m_safe = np.where(any_allowed, m, 0.0)
+                p = np.exp(s - m_safe[:, None])
+                l = p.sum(axis=1)
+                l_safe = np.where(any_allowed, l, 1.0)
+                out[b, h, c0:c0 + len(r)] = (p @ v[b, h]) / l_safe[:, None]
+                lse[b, h, c0:c0 + len(r)] = np.where(any_allowed, m + np.log(l_safe), -np.inf)
+    return out, lse

@@ -1,0 +1,441 @@
+"""Benchmark of the Hilbert-guided block-sparse attention hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--all]
+
+A step is one pass of the whole hot path over one batch of synthetic input
+already resident in HBM: Hilbert index and inverse, gather of q, k, v into
+Hilbert order, tile classification and lists, block-sparse attention forward,
+scatter of the output back to row-major (for the layer workload: gather of the
+features, QKV projection, attention, output projection, scatter). Input buffer
+sets are rotated from step to step so that the working set exceeds the 256 MB
+Infinity Cache and every step reads from HBM.
+
+Prints ONE JSON line on stdout. Timing uses HIP events on the stream every
+kernel is launched on (torch's current stream): one pair around the K timed
+steps, and one pair around every launch of each stage, which gives each
+kernel's average duration inside the timed region. The default workload is the
+128x128-token Hilbert window attention (B=4, heads=8, d=64, window 256), the
+same batch x heads x tokens x head_dim as the paper's headline window row
+(Table 1, I=128x128, W=16x16). The same kernel is then timed on the row-major
+16x16 window mask for the empty-tile comparison, and the CPU oracle is timed
+on a bounded sample of the same step on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import torch  # noqa: E402
+
+import workloads as W  # noqa: E402
+
+METRIC = "attn fwd ms/call + TFLOP/s on non-empty tiles (% bf16 MFMA peak); perm GB/s"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 (vector and matrix)
+MALL_BYTES = 256 << 20
+
+
+def esize(dtype: str) -> int:
+    return 2 if dtype == "bf16" else 4
+
+
+def tdtype(dtype: str):
+    return torch.bfloat16 if dtype == "bf16" else torch.float32
+
+
+class Timer:
+    """Per-stage event pairs on the current stream, averaged over the timed steps."""
+
+    def __init__(self):
+        self.pairs = {}
+        self.active = False
+
+    def stage(self, name):
+        timer = self
+
+        class _Ctx:
+            def __enter__(self_inner):
+                if timer.active:
+                    self_inner.a = torch.cuda.Event(enable_timing=True)
+                    self_inner.a.record()
+
+            def __exit__(self_inner, *exc):
+                if timer.active:
+                    b = torch.cuda.Event(enable_timing=True)
+                    b.record()
+                    timer.pairs.setdefault(name, []).append((self_inner.a, b))
+                return False
+        return _Ctx()
+
+    def mean_ms(self, name):
+        ps = self.pairs.get(name, [])
+        return sum(a.elapsed_time(b) for a, b in ps) / len(ps) if ps else float("nan")
+
+    def count(self, name):
+        return len(self.pairs.get(name, []))
+
+
+# ----------------------------------------------------------------------------
+# attention workloads
+
+
+class AttnPipeline:
+    def __init__(self, w: W.AttnWorkload, hla):
+        self.w, self.hla = w, hla
+        pat = w.pattern
+        self.hilbert = pat.hilbert
+        B, Hh, N, d = w.B, w.heads, w.N, w.d
+        tensor_bytes = B * Hh * N * d * esize(w.dtype)
+        set_bytes = tensor_bytes * (7 if self.hilbert else 4)
+        self.nsets = max(2, min(64, math.ceil(3 * MALL_BYTES / set_bytes)))
+        q, k, v = W.workload_inputs(w)
+        self.sets = []
+        for i in range(self.nsets):
+            s = {"q": q.cuda(), "k": k.cuda(), "v": v.cuda()}
+            if self.hilbert:
+                for n in ("qh", "kh", "vh", "oh"):
+                    s[n] = torch.empty_like(s["q"])
+            s["o"] = torch.empty_like(s["q"])
+            s["lse"] = torch.empty((B, Hh, N), dtype=torch.float32, device="cuda")
+            self.sets.append(s)
+        del q, k, v
+        self.order = torch.empty(N, dtype=torch.int32, device="cuda")
+        self.rank = torch.empty(N, dtype=torch.int32, device="cuda")
+        self.mask = hla.BlockMask(pat, w.tile_m, w.tile_n)
+        self.timer = Timer()
+
+    def step(self, i):
+        hla, w, s, T = self.hla, self.w, self.sets[i % self.nsets], self.timer
+        if self.hilbert:
+            with T.stage("hilbert"):
+                hla.hilbert_perm(w.pattern.H, w.pattern.W, out=(self.order, self.rank))
+            with T.stage("gather"):
+                for a, b in (("q", "qh"), ("k", "kh"), ("v", "vh")):
+                    hla.gather(s[a], self.order, out=s[b])
+            qn, kn, vn, on = "qh", "kh", "vh", "oh"
+        else:
+            qn, kn, vn, on = "q", "k", "v", "o"
+        with T.stage("mask"):
+            self.mask.build()
+        with T.stage("attn"):
+            hla.attn_fwd(s[qn], s[kn], s[vn], self.mask, w.scale, out=s[on], lse=s["lse"])
+        if self.hilbert:
+            with T.stage("scatter"):
+                hla.scatter(s["oh"], self.order, out=s["o"])
+
+    # algorithmic figures -------------------------------------------------
+    def tile_flops(self):
+        tf, tp = self.mask.host_totals()
+        w = self.w
+        return 4.0 * w.tile_m * w.tile_n * w.d * (tf + tp) * w.B * w.heads, tf, tp
+
+    def attn_bytes(self):
+        """q, k, v, out once each plus the fp32 log-sum-exp: 4 N d s + 4 N per (b, h)."""
+        w = self.w
+        return (4 * w.N * w.d * esize(w.dtype) + 4 * w.N) * w.B * w.heads
+
+    def perm_bytes_per_tensor(self):
+        """One gather or scatter of a [B, heads, N, d] tensor: read + write + int32 index."""
+        w = self.w
+        return 2 * w.B * w.heads * w.N * w.d * esize(w.dtype) + 4 * w.N
+
+
+# ----------------------------------------------------------------------------
+# layer workload
+
+
+class LayerPipeline:
+    def __init__(self, w: W.LayerWorkload, hla):
+        self.w, self.hla = w, hla
+        self.hilbert = True
+        B, N, C, Hh, d = w.B, w.N, w.C, w.heads, w.d
+        x, wq, wp = W.layer_inputs(w)
+        set_bytes = B * N * C * 2 * 7
+        self.nsets = max(2, min(64, math.ceil(3 * MALL_BYTES / set_bytes)))
+        self.wq, self.wp = wq.cuda(), wp.cuda()
+        self.sets = []
+        for i in range(self.nsets):
+            s = {"x": x.cuda()}
+            s["xh"] = torch.empty_like(s["x"])
+            for n in ("q", "k", "v", "o"):
+                s[n] = torch.empty((B, Hh, N, d), dtype=torch.bfloat16, device="cuda")
+            s["yh"] = torch.empty((B, N, C), dtype=torch.bfloat16, device="cuda")
+            s["y"] = torch.empty_like(s["yh"])
+            self.sets.append(s)
+        self.order = torch.empty(N, dtype=torch.int32, device="cuda")
+        self.rank = torch.empty(N, dtype=torch.int32, device="cuda")
+        self.mask = hla.BlockMask(w.pattern, w.tile_m, w.tile_n)
+        self.timer = Timer()
+
+    def step(self, i):
+        hla, w, s, T = self.hla, self.w, self.sets[i % self.nsets], self.timer
+        with T.stage("hilbert"):
+            hla.hilbert_perm(w.H, w.W, out=(self.order, self.rank))
+        with T.stage("gather"):
+            hla.gather(s["x"], self.order, out=s["xh"])
+        with T.stage("qkv"):
+            hla.qkv_proj(s["xh"], self.wq, w.heads, outs=(s["q"], s["k"], s["v"]))
+        with T.stage("mask"):
+            self.mask.build()
+        with T.stage("attn"):
+            hla.attn_fwd(s["q"], s["k"], s["v"], self.mask, w.scale, out=s["o"], with_lse=False)
+        with T.stage("proj"):
+            hla.out_proj(s["o"], self.wp, out=s["yh"])
+        with T.stage("scatter"):
+            hla.scatter(s["yh"], self.order, out=s["y"])
+
+    def tile_flops(self):
+        tf, tp = self.mask.host_totals()
+        w = self.w
+        return 4.0 * w.tile_m * w.tile_n * w.d * (tf + tp) * w.B * w.heads, tf, tp
+
+    def attn_bytes(self):
+        w = self.w
+        return 4 * w.N * w.d * 2 * w.B * w.heads
+
+    def perm_bytes_per_tensor(self):
+        w = self.w
+        return 2 * w.B * w.N * w.C * 2 + 4 * w.N
+
+
+def make_pipeline(w, hla):
+    return LayerPipeline(w, hla) if isinstance(w, W.LayerWorkload) else AttnPipeline(w, hla)
+
+
+def run_timed(pipe, steps, warmup):
+    for i in range(warmup):
+        pipe.step(i)
+    torch.cuda.synchronize()
+    pipe.timer.active = True
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        pipe.step(warmup + i)
+    end.record()
+    torch.cuda.synchronize()
+    pipe.timer.active = False
+    return start.elapsed_time(end) / steps
+
+
+def summarize(pipe, ms_step):
+    T = pipe.timer
+    flops, tf, tp = pipe.tile_flops()
+    w = pipe.w
+    attn_ms = T.mean_ms("attn")
+    attn_tflops = flops / (attn_ms * 1e-3) / 1e12
+    peak = BF16_PEAK_TFLOPS if getattr(w, "dtype", "bf16") == "bf16" else FP32_PEAK_TFLOPS
+    res = {
+        "workload": w.name,
+        "ms_per_step": ms_step,
+        "attn_ms": attn_ms,
+        "attn_tile_tflops": attn_tflops,
+        "attn_pct_peak": 100.0 * attn_tflops / peak,
+        "attn_hbm_gbs": pipe.attn_bytes() / (attn_ms * 1e-3) / 1e9,
+        "tiles_full": tf, "tiles_partial": tp,
+        "tile_flops": flops,
+        "stages_ms": {n: T.mean_ms(n) for n in T.pairs},
+    }
+    if "gather" in T.pairs:
+        per = 1 if isinstance(w, W.LayerWorkload) else 3
+        res["gather_gbs"] = per * pipe.perm_bytes_per_tensor() / (T.mean_ms("gather") * 1e-3) / 1e9
+    if "scatter" in T.pairs:
+        res["scatter_gbs"] = pipe.perm_bytes_per_tensor() / (T.mean_ms("scatter") * 1e-3) / 1e9
+    return res
+
+
+# ----------------------------------------------------------------------------
+# CPU baseline: the oracle on a bounded sample of the same step
+
+
+def blas_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        n = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+        return max(n) if n else 1
+    except Exception:
+        return 1
+
+
+def cpu_baseline(w: W.AttnWorkload, flops_per_step: float, budget_s: float = 12.0):
+    """Times the oracle's stages for one step of workload w: Hilbert order, gather of
+    q, k, v, brute-force tile lists, dense masked attention on a sample of query rows
+    (scaled to all rows), scatter. Returns the record for the JSON line."""
+    import numpy as np
+
+    from oracle import attention as o_attn
+    from oracle import blockmask as o_bm
+    from oracle import hilbert as o_hil
+    from oracle import permute as o_perm
+
+    q, k, v = (t.float().numpy().astype(np.float64) for t in W.workload_inputs(w))
+    pat = w.pattern
+    t0 = time.perf_counter()
+    order = o_hil.hilbert_order(pat.H, pat.W)
+    t_hil = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    qh, kh, vh = (o_perm.gather(a, order) for a in (q, k, v))
+    t_gather = time.perf_counter() - t0
+    # tile lists: brute force over a sample of query-tile rows, scaled to all rows
+    nq = w.N // w.tile_m
+    rows_t = list(range(0, nq, max(1, nq // 16)))
+    t0 = time.perf_counter()
+    o_bm.build(pat, w.tile_m, w.tile_n, rows_t)
+    t_mask = (time.perf_counter() - t0) * nq / len(rows_t)
+    # attention: calibrate the row sample on a pilot, then time the sample
+    pilot = np.arange(0, w.N, max(1, w.N // 16))[:16]
+    t0 = time.perf_counter()
+    o_attn.attention(qh, kh, vh, pat, w.scale, rows=pilot)
+    per_row = (time.perf_counter() - t0) / len(pilot)
+    n_rows = int(max(16, min(w.N, budget_s / max(per_row, 1e-9))))
+    rows = np.linspace(0, w.N - 1, n_rows).astype(np.int64)
+    t0 = time.perf_counter()
+    out, _ = o_attn.attention(qh, kh, vh, pat, w.scale, rows=rows)
+    t_attn = (time.perf_counter() - t0) * w.N / n_rows
+    t0 = time.perf_counter()
+    o_perm.scatter(qh, order)   # same-size scatter
+    t_scatter = time.perf_counter() - t0
+    total = t_hil + t_gather + t_mask + t_attn + t_scatter
+    return {
+        "value": flops_per_step / total / 1e12,
+        "unit": "TFLOP/s",
+        "cores": blas_threads(),
+        "kind": "oracle",
+        "sample": (f"float64 oracle on the host: full Hilbert order and gathers, brute-force tile "
+                   f"lists on {len(rows_t)}/{nq} query-tile rows, dense masked attention on "
+                   f"{n_rows}/{w.N} query rows of all {w.B * w.heads} (b,h); each sampled stage "
+                   f"scaled to the whole step; est. {total:.1f} s per step"),
+        "stage_s": {"hilbert": t_hil, "gather": t_gather, "mask": t_mask, "attn": t_attn,
+                    "scatter": t_scatter},
+        "host": {"cpu_count": os.cpu_count(),
+                 "affinity": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None,
+                 "processor": platform.processor() or platform.machine()},
+    }
+
+
+# ----------------------------------------------------------------------------
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=W.C3.name, choices=sorted(W.WORKLOADS))
+    ap.add_argument("--compare", default=None,
+                    help="workload timed through the same kernel for the row-major comparison")
+    ap.add_argument("--all", action="store_true",
+                    help="also time every workload and write gpurun_out/bench_all.json")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the hot path has "
+              f"no multi-GPU part in this build.", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+
+    import paper_2511_05832_amd as hla
+    hla.lib()
+    torch.cuda.set_device(0)
+
+    w = W.WORKLOADS[args.workload]
+    pipe = make_pipeline(w, hla)
+    ms = run_timed(pipe, args.steps, args.warmup)
+    res = summarize(pipe, ms)
+    print(f"[bench] {w.name}: {json.dumps(res)}", file=sys.stderr, flush=True)
+
+    compare = args.compare
+    if compare is None:
+        compare = {W.C3.name: W.C3_ROWMAJOR.name, W.C4.name: W.C4_ROWMAJOR.name}.get(w.name)
+    cmp_res = None
+    if compare:
+        cpipe = make_pipeline(W.WORKLOADS[compare], hla)
+        cms = run_timed(cpipe, args.steps, args.warmup)
+        cmp_res = summarize(cpipe, cms)
+        print(f"[bench] {compare}: {json.dumps(cmp_res)}", file=sys.stderr, flush=True)
+        del cpipe
+
+    if args.all:
+        allres = {}
+        for name, wl in W.WORKLOADS.items():
+            p = make_pipeline(wl, hla)
+            r = summarize(p, run_timed(p, args.steps, args.warmup))
+            allres[name] = r
+            print(f"[bench] {name}: {json.dumps(r)}", file=sys.stderr, flush=True)
+            del p
+            torch.cuda.empty_cache()
+        os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
+        with open(os.path.join(ROOT, "gpurun_out", "bench_all.json"), "w") as f:
+            json.dump(allres, f, indent=1)
+
+    flops = res["tile_flops"]
+    attn_s = res["attn_ms"] * 1e-3
+    is_bf16 = getattr(w, "dtype", "bf16") == "bf16"
+    # dominant kernel: attention. HBM-bound when its bytes take longer at peak than
+    # its tile FLOPs do on the matrix cores.
+    t_hbm = pipe.attn_bytes() / (HBM_PEAK_GBS * 1e9)
+    t_mfma = flops / ((BF16_PEAK_TFLOPS if is_bf16 else FP32_PEAK_TFLOPS) * 1e12)
+    if t_hbm >= t_mfma:
+        achieved = pipe.attn_bytes() / attn_s / 1e9
+        roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": achieved / HBM_PEAK_GBS, "traffic": None, "kernel": "attn_fwd",
+                    "algorithmic_bytes": pipe.attn_bytes(),
+                    "mfma_frac": res["attn_tile_tflops"] / (BF16_PEAK_TFLOPS if is_bf16 else FP32_PEAK_TFLOPS)}
+    else:
+        peak = BF16_PEAK_TFLOPS if is_bf16 else FP32_PEAK_TFLOPS
+        roofline = {"bound": "mfma", "achieved": res["attn_tile_tflops"], "peak": peak,
+                    "unit": "TFLOP/s", "frac": res["attn_tile_tflops"] / peak, "traffic": None,
+                    "kernel": "attn_fwd", "algorithmic_flops": flops,
+                    "hbm_frac": pipe.attn_bytes() / attn_s / 1e9 / HBM_PEAK_GBS}
+
+    cpu = None
+    if not args.no_cpu_baseline and isinstance(w, W.AttnWorkload):
+        cpu = cpu_baseline(w, flops)
+
+    line = {
+        "metric": METRIC,
+        "value": flops / (ms * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": getattr(w, "dtype", "bf16"),
+        "data": "synthetic",
+        "config": {"workload": w.name, "description": w.description,
+                   "B": w.B, "heads": w.heads, "tokens": w.N, "head_dim": w.d,
+                   "tile": [w.tile_m, w.tile_n], "parallelism": "single-gpu"},
+        "attn_ms_per_call": res["attn_ms"],
+        "attn_tflops_nonempty_tiles": res["attn_tile_tflops"],
+        "attn_pct_bf16_peak": res["attn_pct_peak"],
+        "perm_gbs": {"gather": res.get("gather_gbs"), "scatter": res.get("scatter_gbs")},
+        "stages_ms": res["stages_ms"],
+        "tiles": {"full": res["tiles_full"], "partial": res["tiles_partial"]},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    if cmp_res:
+        line["rowmajor_comparison"] = {
+            "workload": cmp_res["workload"], "attn_ms_per_call": cmp_res["attn_ms"],
+            "tiles": {"full": cmp_res["tiles_full"], "partial": cmp_res["tiles_partial"]},
+            "hilbert_speedup_attn": cmp_res["attn_ms"] / res["attn_ms"]}
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

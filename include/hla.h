@@ -1,0 +1,212 @@
+/*
+ * hla.h - C ABI of libhla: Hilbert-guided block-sparse local attention on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Method: Li & Xu, "Hilbert-Guided Sparse Local Attention" (arXiv 2511.05832).
+ * Image tokens are reordered along a Hilbert curve, windows or slide bands are
+ * formed on the reordered 1-D sequence (Sec. 3.1), and a block-sparse attention
+ * forward pass skips empty tiles, runs full tiles unmasked and masks only
+ * partial tiles (Sec. 3.1, block types; Eq. 1).
+ *
+ * Conventions shared by every entry point
+ *  - Every call returns hla_status; HLA_OK is 0. No call throws or aborts.
+ *  - Arguments are validated on the host before any HIP call. On a status other
+ *    than HLA_OK nothing has been enqueued and no output has been written; the
+ *    text of the error is available from hla_last_error() on the same thread.
+ *  - Device pointers are plain device addresses owned by the caller. The library
+ *    allocates and frees no device memory.
+ *  - Work is enqueued on the caller's stream (NULL = the default stream) and the
+ *    calls never synchronise, so they may be captured into a HIP graph.
+ *  - Tensors are dense and contiguous, innermost dimension last:
+ *      attention tensors  [B, heads, N, d]
+ *      layer activations  [B, N, C]
+ *  - Base addresses of tensors must be 16-byte aligned; index arrays 4-byte.
+ *  - Element types: HLA_F32 (IEEE binary32) and HLA_BF16 (bfloat16 stored as
+ *    uint16). Conversions to bf16 round to nearest even.
+ *  - Status HLA_ERR_INVALID_ARG: a null or misaligned pointer, a non-positive
+ *    or inconsistent size. HLA_ERR_UNSUPPORTED: valid but outside what this
+ *    build implements (listed per call). HLA_ERR_HIP: a HIP launch failed; the
+ *    HIP error text is in hla_last_error().
+ *  - Thread safety: re-entrant. The only global state is the per-thread error
+ *    text. Calls that write the same buffers on different streams race.
+ */
+#ifndef HLA_H
+#define HLA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t *hla_stream_t; /* a hipStream_t */
+
+typedef enum {
+  HLA_OK = 0,
+  HLA_ERR_INVALID_ARG = 1,
+  HLA_ERR_UNSUPPORTED = 2,
+  HLA_ERR_HIP = 3
+} hla_status;
+
+typedef enum { HLA_F32 = 0, HLA_BF16 = 1 } hla_dtype;
+
+/*
+ * Attention patterns (Sec. 3.1-3.3). i, j are positions of a query and a key in
+ * the sequence as stored. For the Hilbert patterns the sequence is in Hilbert
+ * order (gathered with hla_gather); for the row-major patterns it is in
+ * row-major order and a position t is the grid cell (r, c) = (t / W, t % W).
+ *
+ *  HLA_HILBERT_WINDOW      p0 = w:      floor(i/w) == floor(j/w)
+ *                          (contiguous windows on the Hilbert sequence, HWA)
+ *  HLA_HILBERT_SLIDE       p0 = h:      |i - j| <= h      (band, HSA)
+ *  HLA_ROWMAJOR_WINDOW     p0, p1 = window rows, cols: same (r/p0, c/p1) cell (WSA)
+ *  HLA_ROWMAJOR_SLIDE      p0, p1 = radius rows, cols: |r-r'| <= p0 && |c-c'| <= p1 (SA)
+ *  HLA_HILBERT_NEIGHBORHOOD p0 = k: j in [s, s+k), s = clamp(i - k/2, 0, N-k) (HNA)
+ *  HLA_ROWMAJOR_NEIGHBORHOOD p0, p1 = kernel rows, cols: the same clamp per axis (NA2D)
+ *  HLA_HILBERT_SHIFTED_WINDOW p0 = w, p1 = s: floor((i+w-s)/w) == floor((j+w-s)/w)
+ *                          (windows moved by s along the sequence; the pairs a
+ *                          cyclic shift would join across the ends are masked, HSWA)
+ */
+typedef enum {
+  HLA_HILBERT_WINDOW = 0,
+  HLA_HILBERT_SLIDE = 1,
+  HLA_ROWMAJOR_WINDOW = 2,
+  HLA_ROWMAJOR_SLIDE = 3,
+  HLA_HILBERT_NEIGHBORHOOD = 4,
+  HLA_ROWMAJOR_NEIGHBORHOOD = 5,
+  HLA_HILBERT_SHIFTED_WINDOW = 6
+} hla_pattern;
+
+typedef struct {
+  int32_t pattern; /* hla_pattern */
+  int32_t H, W;    /* token grid; N = H * W */
+  int32_t p0, p1;  /* pattern parameters, see hla_pattern */
+} hla_pattern_desc;
+
+/*
+ * Block-sparse metadata (Sec. 3.1: full / partial / empty blocks; the paper's
+ * engine keeps only this lightweight block metadata, Sec. 4.2).
+ * The N x N score matrix is cut into tiles of tile_m query rows by tile_n key
+ * columns. For query-tile row q:
+ *   n_full[q]            number of full tiles
+ *   full_idx[q*n_ktiles + t], t < n_full[q]: key-tile indices, ascending
+ *   n_part[q], part_idx  the same for partial tiles
+ * Unused list entries are -1. All four arrays are caller-owned device memory:
+ * n_full, n_part hold n_qtiles int32; full_idx, part_idx hold
+ * n_qtiles * n_ktiles int32 (hla_block_mask_dims gives the counts).
+ * totals, if not NULL, is a device int32[2] that receives
+ * {total full tiles, total partial tiles}.
+ */
+typedef struct {
+  int32_t N, tile_m, tile_n, n_qtiles, n_ktiles;
+  hla_pattern_desc pat;
+  int32_t *n_full, *full_idx, *n_part, *part_idx;
+  int32_t *totals;
+} hla_block_mask;
+
+/*
+ * Hilbert index and its inverse (Sec. 3.1-3.2: the path P_(H,W) is computed
+ * once per feature-map size and cached by the caller).
+ * order[d] = row-major id (y*W + x) of the d-th cell on the curve;
+ * rank[t]  = position of row-major token t on the curve (rank[order[d]] = d).
+ * Curve: starts at cell (x,y) = (0,0), first step to (0,1), ends at (W-1,0).
+ * order, rank: device int32[H*W]; either may be NULL to skip it.
+ * UNSUPPORTED unless H == W == 2^k with 0 <= k <= 15.
+ */
+hla_status hla_hilbert_perm(int32_t H, int32_t W, int32_t *order, int32_t *rank,
+                            hla_stream_t stream);
+
+/*
+ * Gather into Hilbert order (the paper's "reshape" step, Sec. 4.2):
+ *   dst[b,h,i,:] = src[b,h,order[i],:]  for i < N.
+ * src, dst: [B, heads, N, d] of dtype, must not overlap. order: device int32[N],
+ * a permutation of [0, N) (not checked; an out-of-range entry is undefined
+ * behaviour). Any d >= 1 with d * sizeof(dtype) a multiple of 4.
+ */
+hla_status hla_gather(const void *src, void *dst, const int32_t *order,
+                      int64_t B, int64_t heads, int64_t N, int64_t d,
+                      hla_dtype dtype, hla_stream_t stream);
+
+/*
+ * Scatter back to row-major order (the inverse of hla_gather):
+ *   dst[b,h,order[i],:] = src[b,h,i,:].
+ * Same arguments and constraints as hla_gather.
+ */
+hla_status hla_scatter(const void *src, void *dst, const int32_t *order,
+                       int64_t B, int64_t heads, int64_t N, int64_t d,
+                       hla_dtype dtype, hla_stream_t stream);
+
+/*
+ * Host-only: tile-grid sizes for a pattern and tile, so the caller can size the
+ * block-mask arrays. N = H*W must be a multiple of tile_m and of tile_n; tile
+ * sizes are powers of two in [16, 1024]. Pattern parameters must be >= 1
+ * (slide radii and half-widths >= 0; neighbourhood kernels <= the grid extent).
+ */
+hla_status hla_block_mask_dims(const hla_pattern_desc *pat, int32_t tile_m,
+                               int32_t tile_n, int32_t *n_qtiles,
+                               int32_t *n_ktiles);
+
+/*
+ * Classify every (query tile, key tile) pair as full, partial or empty and write
+ * the per-row ascending lists (Sec. 3.1). mask->pat, tile_m, tile_n select the
+ * pattern and tiling; the call fills mask->N, n_qtiles, n_ktiles on the host
+ * and the four device arrays (and totals) on the stream. It does not
+ * synchronise. The classification is exact: for every pattern the class of a
+ * tile equals the one obtained by counting its allowed elements.
+ */
+hla_status hla_build_block_mask(hla_block_mask *mask, hla_stream_t stream);
+
+/*
+ * Block-sparse attention forward (Sec. 3.1; Eq. 1's per-tile work). For every
+ * (b, h) and query-tile row, walks only the listed key tiles: full tiles
+ * without a mask, partial tiles with the element mask of mask->pat. Computes
+ *   out[b,h,i,:] = sum_j softmax_j(scale * <q_i, k_j> | allowed(i,j)) v_j
+ *   lse[b,h,i]   = ln sum_{j allowed} exp(scale * <q_i, k_j>)
+ * q, k, v, out: [B, heads, N, d] of dtype; lse: float32 [B, heads, N] or NULL.
+ * A query with no allowed key gets out = 0 and lse = -inf.
+ * out may not alias q, k or v. The mask must have been built for this N.
+ * bf16: products on bf16 matrix cores, fp32 accumulation and softmax, out
+ * rounded to bf16. f32: fp32 arithmetic throughout.
+ * Supported: d in {32, 64}; tile_m in {64, 128}; tile_n == 64;
+ * otherwise UNSUPPORTED.
+ */
+hla_status hla_attn_fwd(const void *q, const void *k, const void *v,
+                        const hla_block_mask *mask, void *out, float *lse,
+                        int64_t B, int64_t heads, int64_t N, int64_t d,
+                        hla_dtype dtype, float scale, hla_stream_t stream);
+
+/*
+ * QKV projection with head split (Sec. 4.2, input processing: the Linear layer
+ * that produces Q, K, V from the token features):
+ *   y = x W_qkv^T,  x [B, N, C],  W_qkv [3C, C] (row f is output feature f),
+ *   q[b,h,n,e] = y[b,n,      h*d + e]
+ *   k[b,h,n,e] = y[b,n,  C + h*d + e]
+ *   v[b,h,n,e] = y[b,n, 2C + h*d + e],   C = heads * d, no bias.
+ * bf16 in and out, fp32 accumulation. q, k, v: [B, heads, N, d].
+ * Supported: d == 32 or 64, C a multiple of 64; otherwise UNSUPPORTED.
+ */
+hla_status hla_qkv_proj(const void *x, const void *w_qkv, void *q, void *k,
+                        void *v, int64_t B, int64_t N, int64_t heads, int64_t d,
+                        hla_stream_t stream);
+
+/*
+ * Output projection with head merge:
+ *   y[b,n,f] = sum_{h,e} o[b,h,n,e] * W_proj[f, h*d + e],  no bias.
+ * o: [B, heads, N, d]; W_proj: [C_out, heads*d]; y: [B, N, C_out]; bf16, fp32
+ * accumulation. Supported: d == 32 or 64, C_out a multiple of 64.
+ */
+hla_status hla_out_proj(const void *o, const void *w_proj, void *y, int64_t B,
+                        int64_t N, int64_t heads, int64_t d, int64_t c_out,
+                        hla_stream_t stream);
+
+/* Text of the last non-OK status returned on this thread ("" if none). */
+const char *hla_last_error(void);
+
+/* Library version string. */
+const char *hla_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HLA_H */

@@ -1,0 +1,337 @@
+// Block-sparse flash-attention forward, bf16 in / bf16 out, fp32 accumulation,
+// on gfx950 bf16 matrix cores (v_mfma_f32_32x32x16_bf16).
+//
+// What it computes (Sec. 3.1; Eq. 1): for every (b, h) and query tile, walk the
+// non-empty key tiles of that tile row only - the full ones without a mask,
+// then the partial ones with the element mask - and keep a running (online)
+// softmax, so empty tiles cost neither loads nor arithmetic.
+//
+// Work decomposition. One workgroup = one query tile of BM = 32*NW rows of one
+// (b, h); wave w owns 32 query rows. Key tiles are BN = 64 keys.
+//
+// Per key tile, per wave:
+//   S^T = K Q^T    (keys x queries): 2 key blocks of 32 x D/16 MFMAs. A = K rows
+//                  from LDS, B = the wave's Q (kept in registers all kernel).
+//   softmax        lane l owns query l%32; its 32 scores of the tile sit in its
+//                  own accumulators (16 per key block, the other half of the keys
+//                  in lane l^32), so row max / sum need one cross-half exchange.
+//   O^T += V^T P^T (d x queries): D/32 blocks x 4 MFMAs. A = V^T from LDS,
+//                  B = P straight from the S^T accumulators (see below).
+//
+// Register-resident P. The accumulator of a 32x32 MFMA holds, in lane
+// (col = l%32, half = l/32) and slot v, row 8*(v/4) + 4*half + v%4. The K rows
+// fed to S^T are permuted (key_of_row) so that accumulator slot v of lane half
+// `half` is key 16*(v/8) + 8*half + v%8 of the block: eight consecutive keys per
+// run, which is exactly the B-operand layout of the PV MFMA over 16 keys. So P
+// goes from fp32 accumulators to bf16 operands in place, with no LDS trip.
+// The contraction over d in S^T is likewise permuted (lane half `half` holds d
+// in [half*D/2, (half+1)*D/2)), so each lane loads its Q slice as one
+// contiguous run.
+//
+// LDS per stage: K as [BN][D+8] and V transposed as [D][BN+8] (bf16, padded so
+// the 16-byte MFMA operand reads of 32 lanes hit distinct banks); two stages,
+// filled from registers that were loaded one tile ahead, one barrier per tile.
+//
+// Masking (partial tiles only). For the 1-D Hilbert patterns each query's
+// allowed keys are one interval [lo, hi] computed once per lane; for the
+// row-major patterns they are one rectangle of grid cells. Masked scores are
+// -inf before the row max; a query with no allowed key so far keeps m = -inf and
+// contributes exactly zero.
+//
+// Grid: one workgroup per (b*h, query tile), remapped so each XCD (workgroups
+// are dealt round-robin to the 8 XCDs) receives a contiguous range of query
+// tiles: neighbouring tiles share key/value tiles (a window is two query tiles;
+// a band overlaps its neighbour almost entirely), and the reuse stays in one
+// XCD's L2.
+#include "hla_internal.h"
+
+namespace hla {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int BN = 64;
+constexpr int VS = BN + 8;  // row stride of transposed V in LDS (elements)
+
+__device__ __forceinline__ int key_of_row(int i) {
+  // accumulator row i = 8a + 4g + b  ->  key 16(a/2) + 8g + 4(a%2) + b
+  const int a = i >> 3, g = (i >> 2) & 1, b = i & 3;
+  return 16 * (a >> 1) + 8 * g + 4 * (a & 1) + b;
+}
+
+__device__ __forceinline__ int xcd_remap(int bid, int total) {
+  const int per = total >> 3, rem = total & 7;
+  const int xcd = bid & 7, slot = bid >> 3;
+  return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+}
+
+__device__ __forceinline__ int clampi(int x, int lo, int hi) { return min(max(x, lo), hi); }
+
+template <int D, int NW>
+__global__ void __launch_bounds__(64 * NW)
+    attn_fwd_bf16(AttnArgs a) {
+  constexpr int BM = 32 * NW;
+  constexpr int NT = 64 * NW;
+  constexpr int KS = D + 8;          // row stride of K in LDS (elements)
+  constexpr int STAGE = BN * KS + D * VS;
+  constexpr int NCH = D / 16;        // MFMA steps over d for S^T
+  constexpr int NDB = D / 32;        // d blocks of O^T
+  constexpr int KUNITS = BN * D / 8; // 16-byte units of a K tile
+  constexpr int KPT = (KUNITS + NT - 1) / NT;
+  constexpr int VUNITS = (D / 2) * (BN / 8);  // (2 d x 8 keys) units of a V tile
+  constexpr int VPT = (VUNITS + NT - 1) / NT;
+
+  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int col = lane & 31, half = lane >> 5;
+
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int bh = logical / a.n_qtiles;
+  const int qt = logical - bh * a.n_qtiles;
+  const int q0 = qt * BM;
+  const int64_t slice = (int64_t)bh * a.N * D;
+  const __bf16 *Q = static_cast<const __bf16 *>(a.q) + slice;
+  const __bf16 *K = static_cast<const __bf16 *>(a.k) + slice;
+  const __bf16 *V = static_cast<const __bf16 *>(a.v) + slice;
+
+  // This lane's query and its Q operand (d = half*D/2 + 8c + s for step c).
+  const int qpos = q0 + wave * 32 + col;
+  bf16x8 qop[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c)
+    qop[c] = *reinterpret_cast<const bf16x8 *>(Q + (int64_t)qpos * D + half * (D / 2) + 8 * c);
+
+  // Allowed-key region of this query (used on partial tiles only).
+  const PatternArgs &P = a.pat;
+  const bool one_d = P.kind == HLA_HILBERT_WINDOW || P.kind == HLA_HILBERT_SLIDE ||
+                     P.kind == HLA_HILBERT_NEIGHBORHOOD || P.kind == HLA_HILBERT_SHIFTED_WINDOW;
+  int lo = 0, hi = 0, rlo = 0, rhi = 0, clo = 0, chi = 0;
+  if (P.kind == HLA_HILBERT_WINDOW) {
+    lo = (qpos / P.p0) * P.p0;
+    hi = lo + P.p0 - 1;
+  } else if (P.kind == HLA_HILBERT_SLIDE) {
+    lo = qpos - P.p0;
+    hi = qpos + P.p0;
+  } else if (P.kind == HLA_HILBERT_NEIGHBORHOOD) {
+    lo = clampi(qpos - P.p0 / 2, 0, P.N - P.p0);
+    hi = lo + P.p0 - 1;
+  } else if (P.kind == HLA_HILBERT_SHIFTED_WINDOW) {
+    const int g = (qpos + P.p0 - P.p1) / P.p0;
+    lo = g * P.p0 - P.p0 + P.p1;
+    hi = lo + P.p0 - 1;
+  } else {
+    const int r = (int)fdiv((uint32_t)qpos, P.wdiv), c = qpos - r * P.W;
+    if (P.kind == HLA_ROWMAJOR_WINDOW) {
+      rlo = (r / P.p0) * P.p0; rhi = rlo + P.p0 - 1;
+      clo = (c / P.p1) * P.p1; chi = clo + P.p1 - 1;
+    } else if (P.kind == HLA_ROWMAJOR_SLIDE) {
+      rlo = r - P.p0; rhi = r + P.p0;
+      clo = c - P.p1; chi = c + P.p1;
+    } else {
+      rlo = clampi(r - P.p0 / 2, 0, P.H - P.p0); rhi = rlo + P.p0 - 1;
+      clo = clampi(c - P.p1 / 2, 0, P.W - P.p1); chi = clo + P.p1 - 1;
+    }
+  }
+
+  const int nf = a.n_full[qt], np = a.n_part[qt], ntot = nf + np;
+  const int32_t *frow = a.full_idx + (int64_t)qt * a.n_ktiles;
+  const int32_t *prow = a.part_idx + (int64_t)qt * a.n_ktiles;
+
+  // Staging registers for the next K/V tile.
+  uint4 kreg[KPT];
+  uint32_t vreg[VPT][8];
+  auto load_tile = [&](int kt) {
+    const __bf16 *Kt = K + (int64_t)kt * BN * D;
+    const __bf16 *Vt = V + (int64_t)kt * BN * D;
+#pragma unroll
+    for (int u = 0; u < KPT; ++u) {
+      const int id = tid + u * NT;
+      if (KUNITS % NT == 0 || id < KUNITS)
+        kreg[u] = *reinterpret_cast<const uint4 *>(Kt + (id / (D / 8)) * D + (id % (D / 8)) * 8);
+    }
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) {
+      const int id = tid + u * NT;
+      if (VUNITS % NT == 0 || id < VUNITS) {
+        const int dp = id % (D / 2), kg = id / (D / 2);
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          vreg[u][j] = *reinterpret_cast<const uint32_t *>(Vt + (kg * 8 + j) * D + 2 * dp);
+      }
+    }
+  };
+  auto store_tile = [&](int stage) {
+    __bf16 *Ks = lds + stage * STAGE;
+    __bf16 *Vs = Ks + BN * KS;
+#pragma unroll
+    for (int u = 0; u < KPT; ++u) {
+      const int id = tid + u * NT;
+      if (KUNITS % NT == 0 || id < KUNITS)
+        *reinterpret_cast<uint4 *>(Ks + (id / (D / 8)) * KS + (id % (D / 8)) * 8) = kreg[u];
+    }
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) {
+      const int id = tid + u * NT;
+      if (VUNITS % NT == 0 || id < VUNITS) {
+        const int dp = id % (D / 2), kg = id / (D / 2);
+        uint4 lo4, hi4;  // d = 2dp (low halves) and d = 2dp+1 (high halves), 8 keys each
+        lo4.x = __builtin_amdgcn_perm(vreg[u][1], vreg[u][0], 0x05040100u);
+        lo4.y = __builtin_amdgcn_perm(vreg[u][3], vreg[u][2], 0x05040100u);
+        lo4.z = __builtin_amdgcn_perm(vreg[u][5], vreg[u][4], 0x05040100u);
+        lo4.w = __builtin_amdgcn_perm(vreg[u][7], vreg[u][6], 0x05040100u);
+        hi4.x = __builtin_amdgcn_perm(vreg[u][1], vreg[u][0], 0x07060302u);
+        hi4.y = __builtin_amdgcn_perm(vreg[u][3], vreg[u][2], 0x07060302u);
+        hi4.z = __builtin_amdgcn_perm(vreg[u][5], vreg[u][4], 0x07060302u);
+        hi4.w = __builtin_amdgcn_perm(vreg[u][7], vreg[u][6], 0x07060302u);
+        *reinterpret_cast<uint4 *>(Vs + (2 * dp) * VS + kg * 8) = lo4;
+        *reinterpret_cast<uint4 *>(Vs + (2 * dp + 1) * VS + kg * 8) = hi4;
+      }
+    }
+  };
+
+  f32x16 oacc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) oacc[db] = f32x16{};
+  float m_run = -__builtin_inff();  // running max, in units of log2
+  float l_run = 0.f;               // this lane's partial sum (its half of the keys)
+  const float sl2 = a.scale_log2;
+  const int krow = key_of_row(col);
+
+  if (ntot > 0) load_tile(nf > 0 ? frow[0] : prow[0]);
+
+  for (int it = 0; it < ntot; ++it) {
+    const int stage = it & 1;
+    const bool masked = it >= nf;
+    const int kt = masked ? prow[it - nf] : frow[it];
+    store_tile(stage);
+    __syncthreads();
+    if (it + 1 < ntot) load_tile(it + 1 < nf ? frow[it + 1] : prow[it + 1 - nf]);
+
+    const __bf16 *Ks = lds + stage * STAGE;
+    const __bf16 *Vs = Ks + BN * KS;
+
+    // S^T for the two 32-key blocks.
+    f32x16 s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      s[kb] = f32x16{};
+      const __bf16 *kr = Ks + (kb * 32 + krow) * KS + half * (D / 2);
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {
+        const bf16x8 kop = *reinterpret_cast<const bf16x8 *>(kr + 8 * c);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[c], s[kb], 0, 0, 0);
+      }
+    }
+
+    if (masked) {
+      const int kbase = kt * BN + 8 * half;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int kpos = kbase + kb * 32 + 16 * (v >> 3) + (v & 7);
+          bool ok;
+          if (one_d) {
+            ok = kpos >= lo && kpos <= hi;
+          } else {
+            const int r = (int)fdiv((uint32_t)kpos, P.wdiv), c = kpos - r * P.W;
+            ok = r >= rlo && r <= rhi && c >= clo && c <= chi;
+          }
+          if (!ok) s[kb][v] = -__builtin_inff();
+        }
+      }
+    }
+
+    // Online softmax (log2 domain).
+    float mx = s[0][0];
+#pragma unroll
+    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[0][v]);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[1][v]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx * sl2);
+    const float m_use = m_new == -__builtin_inff() ? 0.f : m_new;
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+    m_run = m_new;
+    float lsum = 0.f;
+    bf16x8 pop[4];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float p = __builtin_amdgcn_exp2f(s[kb][v] * sl2 - m_use);
+        lsum += p;
+        pop[kb * 2 + (v >> 3)][v & 7] = (__bf16)p;
+      }
+    }
+    l_run = l_run * alpha + lsum;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
+
+    // O^T += V^T P^T over four 16-key steps.
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const __bf16 *vr = Vs + (db * 32 + col) * VS + 8 * half;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const bf16x8 vop = *reinterpret_cast<const bf16x8 *>(vr + 16 * t);
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[t], oacc[db], 0, 0, 0);
+      }
+    }
+  }
+
+  // Epilogue: normalise, stage O through LDS, write rows coalesced.
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  __syncthreads();  // every wave is done reading K/V from LDS
+  constexpr int OS = D + 8;
+  __bf16 *Os = lds + wave * 32 * OS;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      bf16x4 o4;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) o4[b] = (__bf16)(oacc[db][4 * g + b] * inv);
+      *reinterpret_cast<bf16x4 *>(Os + col * OS + db * 32 + 8 * g + 4 * half) = o4;
+    }
+  }
+  __syncthreads();
+  __bf16 *O = static_cast<__bf16 *>(a.out) + slice + (int64_t)(q0 + wave * 32) * D;
+  constexpr int CPR = D / 8;  // 16-byte chunks per row
+#pragma unroll
+  for (int i = lane; i < 32 * CPR; i += 64) {
+    const int r = i / CPR, c = i % CPR;
+    *reinterpret_cast<uint4 *>(O + r * D + c * 8) =
+        *reinterpret_cast<const uint4 *>(Os + r * OS + c * 8);
+  }
+  if (a.lse && half == 0) {
+    const float ln2 = 0.69314718055994530942f;
+    a.lse[(int64_t)bh * a.N + qpos] =
+        l_tot > 0.f ? (m_run + __builtin_amdgcn_logf(l_tot)) * ln2 : -__builtin_inff();
+  }
+}
+
+template <int D, int NW>
+hipError_t launch(const AttnArgs &a, hipStream_t s) {
+  const int64_t blocks = (int64_t)a.BH * a.n_qtiles;
+  hipLaunchKernelGGL((attn_fwd_bf16<D, NW>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attn_bf16(const AttnArgs &a, int d, int tile_m, int tile_n,
+                            hipStream_t s) {
+  if (tile_n != BN) return hipErrorInvalidValue;
+  if (d == 64 && tile_m == 128) return launch<64, 4>(a, s);
+  if (d == 64 && tile_m == 64) return launch<64, 2>(a, s);
+  if (d == 32 && tile_m == 128) return launch<32, 4>(a, s);
+  if (d == 32 && tile_m == 64) return launch<32, 2>(a, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace hla

@@ -1,0 +1,173 @@
+// Block-sparse attention forward in fp32 throughout (fp32 I/O, fp32 products).
+//
+// Same algorithm as the bf16 kernel (Sec. 3.1; Eq. 1: only the listed key
+// tiles are visited, full tiles unmasked, partial tiles masked, online
+// softmax), written for exact fp32 arithmetic: gfx950 has no reduced-precision
+// fp32 matrix mode, and fp32 vector FMA runs at the same 157 TFLOP/s as fp32
+// MFMA, so each thread owns one query row and does plain FMAs. K and V tiles are
+// staged in LDS and read as broadcasts (every lane of a wave reads the same key
+// row at the same time).
+#include "hla_internal.h"
+
+namespace hla {
+namespace {
+
+constexpr int BN = 64;
+constexpr int CH = 16;  // keys per online-softmax step
+
+__device__ __forceinline__ int xcd_remap(int bid, int total) {
+  const int per = total >> 3, rem = total & 7;
+  const int xcd = bid & 7, slot = bid >> 3;
+  return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+}
+
+__device__ __forceinline__ int clampi(int x, int lo, int hi) { return min(max(x, lo), hi); }
+
+template <int D, int BM>
+__global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) float Ks[BN * D];
+  __shared__ __attribute__((aligned(16))) float Vs[BN * D];
+
+  const int tid = threadIdx.x;
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int bh = logical / a.n_qtiles;
+  const int qt = logical - bh * a.n_qtiles;
+  const int qpos = qt * BM + tid;
+  const int64_t slice = (int64_t)bh * a.N * D;
+  const float *Q = static_cast<const float *>(a.q) + slice;
+  const float *K = static_cast<const float *>(a.k) + slice;
+  const float *V = static_cast<const float *>(a.v) + slice;
+
+  float q[D], acc[D];
+#pragma unroll
+  for (int i = 0; i < D; i += 4) {
+    const float4 t = *reinterpret_cast<const float4 *>(Q + (int64_t)qpos * D + i);
+    q[i] = t.x; q[i + 1] = t.y; q[i + 2] = t.z; q[i + 3] = t.w;
+  }
+#pragma unroll
+  for (int i = 0; i < D; ++i) acc[i] = 0.f;
+
+  const PatternArgs &P = a.pat;
+  const bool one_d = P.kind == HLA_HILBERT_WINDOW || P.kind == HLA_HILBERT_SLIDE ||
+                     P.kind == HLA_HILBERT_NEIGHBORHOOD || P.kind == HLA_HILBERT_SHIFTED_WINDOW;
+  int lo = 0, hi = 0, rlo = 0, rhi = 0, clo = 0, chi = 0;
+  if (P.kind == HLA_HILBERT_WINDOW) {
+    lo = (qpos / P.p0) * P.p0;
+    hi = lo + P.p0 - 1;
+  } else if (P.kind == HLA_HILBERT_SLIDE) {
+    lo = qpos - P.p0;
+    hi = qpos + P.p0;
+  } else if (P.kind == HLA_HILBERT_NEIGHBORHOOD) {
+    lo = clampi(qpos - P.p0 / 2, 0, P.N - P.p0);
+    hi = lo + P.p0 - 1;
+  } else if (P.kind == HLA_HILBERT_SHIFTED_WINDOW) {
+    const int g = (qpos + P.p0 - P.p1) / P.p0;
+    lo = g * P.p0 - P.p0 + P.p1;
+    hi = lo + P.p0 - 1;
+  } else {
+    const int r = (int)fdiv((uint32_t)qpos, P.wdiv), c = qpos - r * P.W;
+    if (P.kind == HLA_ROWMAJOR_WINDOW) {
+      rlo = (r / P.p0) * P.p0; rhi = rlo + P.p0 - 1;
+      clo = (c / P.p1) * P.p1; chi = clo + P.p1 - 1;
+    } else if (P.kind == HLA_ROWMAJOR_SLIDE) {
+      rlo = r - P.p0; rhi = r + P.p0;
+      clo = c - P.p1; chi = c + P.p1;
+    } else {
+      rlo = clampi(r - P.p0 / 2, 0, P.H - P.p0); rhi = rlo + P.p0 - 1;
+      clo = clampi(c - P.p1 / 2, 0, P.W - P.p1); chi = clo + P.p1 - 1;
+    }
+  }
+
+  const int nf = a.n_full[qt], np = a.n_part[qt], ntot = nf + np;
+  const int32_t *frow = a.full_idx + (int64_t)qt * a.n_ktiles;
+  const int32_t *prow = a.part_idx + (int64_t)qt * a.n_ktiles;
+  const float sl2 = a.scale_log2;
+  float m_run = -__builtin_inff(), l_run = 0.f;
+
+  for (int it = 0; it < ntot; ++it) {
+    const bool masked = it >= nf;
+    const int kt = masked ? prow[it - nf] : frow[it];
+    __syncthreads();
+    const float *Kt = K + (int64_t)kt * BN * D;
+    const float *Vt = V + (int64_t)kt * BN * D;
+    for (int i = tid; i < BN * D / 4; i += BM) {
+      reinterpret_cast<float4 *>(Ks)[i] = reinterpret_cast<const float4 *>(Kt)[i];
+      reinterpret_cast<float4 *>(Vs)[i] = reinterpret_cast<const float4 *>(Vt)[i];
+    }
+    __syncthreads();
+    for (int j0 = 0; j0 < BN; j0 += CH) {
+      float s[CH];
+#pragma unroll
+      for (int j = 0; j < CH; ++j) {
+        float dot = 0.f;
+#pragma unroll
+        for (int i = 0; i < D; ++i) dot = __builtin_fmaf(q[i], Ks[(j0 + j) * D + i], dot);
+        s[j] = dot;
+      }
+      if (masked) {
+#pragma unroll
+        for (int j = 0; j < CH; ++j) {
+          const int kpos = kt * BN + j0 + j;
+          bool ok;
+          if (one_d) {
+            ok = kpos >= lo && kpos <= hi;
+          } else {
+            const int r = (int)fdiv((uint32_t)kpos, P.wdiv), c = kpos - r * P.W;
+            ok = r >= rlo && r <= rhi && c >= clo && c <= chi;
+          }
+          if (!ok) s[j] = -__builtin_inff();
+        }
+      }
+      float mx = s[0];
+#pragma unroll
+      for (int j = 1; j < CH; ++j) mx = fmaxf(mx, s[j]);
+      const float m_new = fmaxf(m_run, mx * sl2);
+      const float m_use = m_new == -__builtin_inff() ? 0.f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int i = 0; i < D; ++i) acc[i] *= alpha;
+#pragma unroll
+      for (int j = 0; j < CH; ++j) {
+        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[j], sl2, -m_use));
+        l_run += p;
+#pragma unroll
+        for (int i = 0; i < D; ++i) acc[i] = __builtin_fmaf(p, Vs[(j0 + j) * D + i], acc[i]);
+      }
+    }
+  }
+
+  const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+  float *O = static_cast<float *>(a.out) + slice + (int64_t)qpos * D;
+#pragma unroll
+  for (int i = 0; i < D; i += 4)
+    *reinterpret_cast<float4 *>(O + i) =
+        make_float4(acc[i] * inv, acc[i + 1] * inv, acc[i + 2] * inv, acc[i + 3] * inv);
+  if (a.lse) {
+    const float ln2 = 0.69314718055994530942f;
+    a.lse[(int64_t)bh * a.N + qpos] =
+        l_run > 0.f ? (m_run + __builtin_amdgcn_logf(l_run)) * ln2 : -__builtin_inff();
+  }
+}
+
+template <int D, int BM>
+hipError_t launch(const AttnArgs &a, hipStream_t s) {
+  const int64_t blocks = (int64_t)a.BH * a.n_qtiles;
+  hipLaunchKernelGGL((attn_fwd_f32<D, BM>), dim3((uint32_t)blocks), dim3(BM), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attn_f32(const AttnArgs &a, int d, int tile_m, int tile_n,
+                           hipStream_t s) {
+  if (tile_n != BN) return hipErrorInvalidValue;
+  if (d == 32 && tile_m == 64) return launch<32, 64>(a, s);
+  if (d == 32 && tile_m == 128) return launch<32, 128>(a, s);
+  if (d == 64 && tile_m == 64) return launch<64, 64>(a, s);
+  if (d == 64 && tile_m == 128) return launch<64, 128>(a, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace hla

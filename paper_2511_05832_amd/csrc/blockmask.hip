@@ -1,0 +1,216 @@
+// Tile classification and per-row tile lists (Sec. 3.1: full, partial and
+// empty blocks of the N x N score matrix; empty blocks are skipped, full
+// blocks run without a mask, partial blocks need the element mask).
+//
+// Exact closed-form classification, one thread per (query tile, key tile):
+// a tile covers an interval of query positions and an interval of key
+// positions. For the 1-D patterns the allowed pairs of an interval pair are
+// decided per axis from interval end points (window ids, band distances,
+// clamped neighbourhood starts). For the 2-D row-major patterns a position
+// interval is split into at most three grid rectangles (a partial first row,
+// whole middle rows, a partial last row); the pattern is a product of a row
+// condition and a column condition, so each rectangle pair is decided per axis
+// and the tile is non-empty if any pair is, full if every pair is.
+//
+// Layout: one workgroup per query-tile row walks the key tiles in chunks of
+// 256, compacts full and partial indices with wave ballots into ascending
+// lists, then pads the rest of both rows with -1.
+#include "hla_internal.h"
+
+namespace hla {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+
+struct Cls {
+  bool any, all;
+};
+
+enum AxisKind { AX_WINDOW, AX_SLIDE, AX_NEIGH };
+
+// Query interval [x0, x1] against key interval [y0, y1] on one axis.
+//   AX_WINDOW: groups floor((x + off) / g); allowed iff same group
+//   AX_SLIDE:  |x - y| <= g
+//   AX_NEIGH:  y in [s(x), s(x) + g), s(x) = clamp(x - g/2, 0, extent - g)
+__device__ __forceinline__ Cls axis_cls(int kind, int g, int off, int extent, int x0,
+                                        int x1, int y0, int y1) {
+  Cls c;
+  if (kind == AX_WINDOW) {
+    const int ga = (x0 + off) / g, gb = (x1 + off) / g;
+    const int ha = (y0 + off) / g, hb = (y1 + off) / g;
+    c.any = max(ga, ha) <= min(gb, hb);
+    c.all = (ga == gb) && (ha == hb) && (ga == ha);
+  } else if (kind == AX_SLIDE) {
+    const int dmin = max(0, max(y0 - x1, x0 - y1));
+    const int dmax = max(abs(x0 - y1), abs(x1 - y0));
+    c.any = dmin <= g;
+    c.all = dmax <= g;
+  } else {
+    const int s0 = min(max(x0 - g / 2, 0), extent - g);
+    const int s1 = min(max(x1 - g / 2, 0), extent - g);
+    c.any = (s0 <= y1) && (y0 <= s1 + g - 1);
+    c.all = (s1 <= y0) && (y1 <= s0 + g - 1);
+  }
+  return c;
+}
+
+struct Rects {
+  int n;
+  int r0[3], r1[3], c0[3], c1[3];
+};
+
+__device__ __forceinline__ Rects split_rows(int a, int b, int W) {
+  Rects R;
+  const int ra = a / W, ca = a - ra * W;
+  const int rb = b / W, cb = b - rb * W;
+  if (ra == rb) {
+    R.n = 1;
+    R.r0[0] = ra; R.r1[0] = ra; R.c0[0] = ca; R.c1[0] = cb;
+    return R;
+  }
+  R.n = 0;
+  R.r0[R.n] = ra; R.r1[R.n] = ra; R.c0[R.n] = ca; R.c1[R.n] = W - 1; ++R.n;
+  if (rb - ra >= 2) {
+    R.r0[R.n] = ra + 1; R.r1[R.n] = rb - 1; R.c0[R.n] = 0; R.c1[R.n] = W - 1; ++R.n;
+  }
+  R.r0[R.n] = rb; R.r1[R.n] = rb; R.c0[R.n] = 0; R.c1[R.n] = cb; ++R.n;
+  return R;
+}
+
+// 0 = empty, 1 = partial, 2 = full
+__device__ int classify_tile(const PatternArgs &p, int i0, int i1, int j0, int j1) {
+  switch (p.kind) {
+    case HLA_HILBERT_WINDOW: {
+      Cls c = axis_cls(AX_WINDOW, p.p0, 0, p.N, i0, i1, j0, j1);
+      return c.all ? 2 : (c.any ? 1 : 0);
+    }
+    case HLA_HILBERT_SHIFTED_WINDOW: {
+      Cls c = axis_cls(AX_WINDOW, p.p0, p.p0 - p.p1, p.N, i0, i1, j0, j1);
+      return c.all ? 2 : (c.any ? 1 : 0);
+    }
+    case HLA_HILBERT_SLIDE: {
+      Cls c = axis_cls(AX_SLIDE, p.p0, 0, p.N, i0, i1, j0, j1);
+      return c.all ? 2 : (c.any ? 1 : 0);
+    }
+    case HLA_HILBERT_NEIGHBORHOOD: {
+      Cls c = axis_cls(AX_NEIGH, p.p0, 0, p.N, i0, i1, j0, j1);
+      return c.all ? 2 : (c.any ? 1 : 0);
+    }
+    default:
+      break;
+  }
+  const int ax = p.kind == HLA_ROWMAJOR_WINDOW ? AX_WINDOW
+                 : p.kind == HLA_ROWMAJOR_SLIDE ? AX_SLIDE
+                                                : AX_NEIGH;
+  const Rects Q = split_rows(i0, i1, p.W);
+  const Rects K = split_rows(j0, j1, p.W);
+  bool any = false, all = true;
+  for (int a = 0; a < Q.n; ++a) {
+    for (int b = 0; b < K.n; ++b) {
+      const Cls cr = axis_cls(ax, p.p0, 0, p.H, Q.r0[a], Q.r1[a], K.r0[b], K.r1[b]);
+      const Cls cc = axis_cls(ax, p.p1, 0, p.W, Q.c0[a], Q.c1[a], K.c0[b], K.c1[b]);
+      any = any || (cr.any && cc.any);
+      all = all && (cr.all && cc.all);
+    }
+  }
+  return all ? 2 : (any ? 1 : 0);
+}
+
+__device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+__global__ void __launch_bounds__(kThreads)
+    classify_rows(PatternArgs p, int32_t tile_m, int32_t tile_n, int32_t n_ktiles,
+                  int32_t *__restrict__ n_full, int32_t *__restrict__ full_idx,
+                  int32_t *__restrict__ n_part, int32_t *__restrict__ part_idx) {
+  __shared__ int32_t wave_f[kWaves], wave_p[kWaves];
+  const int q = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i0 = q * tile_m, i1 = i0 + tile_m - 1;
+  int32_t *frow = full_idx + (int64_t)q * n_ktiles;
+  int32_t *prow = part_idx + (int64_t)q * n_ktiles;
+  int nf = 0, np = 0;
+  for (int base = 0; base < n_ktiles; base += kThreads) {
+    const int kt = base + tid;
+    int cls = 0;
+    if (kt < n_ktiles) cls = classify_tile(p, i0, i1, kt * tile_n, kt * tile_n + tile_n - 1);
+    const uint64_t bf = __ballot(cls == 2);
+    const uint64_t bp = __ballot(cls == 1);
+    if (lane == 0) {
+      wave_f[wave] = __popcll(bf);
+      wave_p[wave] = __popcll(bp);
+    }
+    __syncthreads();
+    int off_f = 0, off_p = 0, tot_f = 0, tot_p = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      if (w < wave) {
+        off_f += wave_f[w];
+        off_p += wave_p[w];
+      }
+      tot_f += wave_f[w];
+      tot_p += wave_p[w];
+    }
+    if (cls == 2) frow[nf + off_f + lanes_below(bf)] = kt;
+    if (cls == 1) prow[np + off_p + lanes_below(bp)] = kt;
+    nf += tot_f;
+    np += tot_p;
+    __syncthreads();
+  }
+  for (int t = nf + tid; t < n_ktiles; t += kThreads) frow[t] = -1;
+  for (int t = np + tid; t < n_ktiles; t += kThreads) prow[t] = -1;
+  if (tid == 0) {
+    n_full[q] = nf;
+    n_part[q] = np;
+  }
+}
+
+__global__ void __launch_bounds__(kThreads)
+    sum_totals(const int32_t *__restrict__ n_full, const int32_t *__restrict__ n_part,
+               int32_t n, int32_t *__restrict__ totals) {
+  __shared__ int32_t sf[kWaves], sp[kWaves];
+  int f = 0, p = 0;
+  for (int i = threadIdx.x; i < n; i += kThreads) {
+    f += n_full[i];
+    p += n_part[i];
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    f += __shfl_xor(f, o);
+    p += __shfl_xor(p, o);
+  }
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    sf[wave] = f;
+    sp[wave] = p;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int tf = 0, tp = 0;
+    for (int w = 0; w < kWaves; ++w) {
+      tf += sf[w];
+      tp += sp[w];
+    }
+    totals[0] = tf;
+    totals[1] = tp;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_block_mask(const PatternArgs &pat, int32_t tile_m, int32_t tile_n,
+                             int32_t n_qtiles, int32_t n_ktiles, int32_t *n_full,
+                             int32_t *full_idx, int32_t *n_part, int32_t *part_idx,
+                             int32_t *totals, hipStream_t s) {
+  hipLaunchKernelGGL(classify_rows, dim3(n_qtiles), dim3(kThreads), 0, s, pat, tile_m,
+                     tile_n, n_ktiles, n_full, full_idx, n_part, part_idx);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !totals) return e;
+  hipLaunchKernelGGL(sum_totals, dim3(1), dim3(kThreads), 0, s, n_full, n_part, n_qtiles,
+                     totals);
+  return hipGetLastError();
+}
+
+}  // namespace hla

@@ -1,0 +1,278 @@
+// C-ABI entry points of libhla: argument validation on the host, then launch.
+// Every check runs before the first HIP call, so a rejected call enqueues
+// nothing and writes nothing.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "hla_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+hla_status fail(hla_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+hla_status hip_status(hipError_t e, const char *what) {
+  if (e == hipSuccess) return HLA_OK;
+  return fail(HLA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+int64_t dtype_size(hla_dtype dt) { return dt == HLA_F32 ? 4 : (dt == HLA_BF16 ? 2 : 0); }
+
+constexpr int64_t kMaxI32 = 2147483647LL;
+
+hla_status check_pattern(const hla_pattern_desc *p) {
+  if (!p) return fail(HLA_ERR_INVALID_ARG, "pattern descriptor is NULL");
+  if (p->H <= 0 || p->W <= 0) return fail(HLA_ERR_INVALID_ARG, "grid %dx%d must be positive", p->H, p->W);
+  const int64_t N = (int64_t)p->H * p->W;
+  if (N > (1LL << 30)) return fail(HLA_ERR_UNSUPPORTED, "N = %lld exceeds 2^30 tokens", (long long)N);
+  if (p->p0 > (1 << 30) || p->p1 > (1 << 30))
+    return fail(HLA_ERR_UNSUPPORTED, "pattern parameters above 2^30");
+  switch (p->pattern) {
+    case HLA_HILBERT_WINDOW:
+      if (p->p0 < 1) return fail(HLA_ERR_INVALID_ARG, "window length p0 = %d must be >= 1", p->p0);
+      break;
+    case HLA_HILBERT_SLIDE:
+      if (p->p0 < 0) return fail(HLA_ERR_INVALID_ARG, "half-width p0 = %d must be >= 0", p->p0);
+      break;
+    case HLA_HILBERT_NEIGHBORHOOD:
+      if (p->p0 < 1 || p->p0 > N)
+        return fail(HLA_ERR_INVALID_ARG, "neighbourhood length p0 = %d must be in [1, N]", p->p0);
+      break;
+    case HLA_HILBERT_SHIFTED_WINDOW:
+      if (p->p0 < 1) return fail(HLA_ERR_INVALID_ARG, "window length p0 = %d must be >= 1", p->p0);
+      if (p->p1 < 0 || p->p1 >= p->p0)
+        return fail(HLA_ERR_INVALID_ARG, "shift p1 = %d must be in [0, window)", p->p1);
+      break;
+    case HLA_ROWMAJOR_WINDOW:
+      if (p->p0 < 1 || p->p1 < 1)
+        return fail(HLA_ERR_INVALID_ARG, "window %dx%d must be >= 1", p->p0, p->p1);
+      break;
+    case HLA_ROWMAJOR_SLIDE:
+      if (p->p0 < 0 || p->p1 < 0)
+        return fail(HLA_ERR_INVALID_ARG, "radii %d,%d must be >= 0", p->p0, p->p1);
+      break;
+    case HLA_ROWMAJOR_NEIGHBORHOOD:
+      if (p->p0 < 1 || p->p1 < 1 || p->p0 > p->H || p->p1 > p->W)
+        return fail(HLA_ERR_INVALID_ARG, "kernel %dx%d must be in [1,H]x[1,W]", p->p0, p->p1);
+      break;
+    default:
+      return fail(HLA_ERR_INVALID_ARG, "unknown pattern %d", p->pattern);
+  }
+  return HLA_OK;
+}
+
+hla_status check_tiles(const hla_pattern_desc *p, int32_t tile_m, int32_t tile_n) {
+  if (!is_pow2(tile_m) || !is_pow2(tile_n) || tile_m < 16 || tile_n < 16 || tile_m > 1024 ||
+      tile_n > 1024)
+    return fail(HLA_ERR_UNSUPPORTED, "tiles %dx%d must be powers of two in [16, 1024]", tile_m, tile_n);
+  const int64_t N = (int64_t)p->H * p->W;
+  if (N % tile_m || N % tile_n)
+    return fail(HLA_ERR_UNSUPPORTED, "N = %lld is not a multiple of the tiles %dx%d",
+                (long long)N, tile_m, tile_n);
+  return HLA_OK;
+}
+
+hla_status check_tensor_args(const void *a, const char *name) {
+  if (!a) return fail(HLA_ERR_INVALID_ARG, "%s is NULL", name);
+  if (!aligned(a, 16)) return fail(HLA_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+  return HLA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *hla_last_error(void) { return g_last_error.c_str(); }
+
+const char *hla_version(void) { return "libhla 0.1 (gfx950)"; }
+
+hla_status hla_hilbert_perm(int32_t H, int32_t W, int32_t *order, int32_t *rank,
+                            hla_stream_t stream) {
+  if (H != W || !is_pow2(H) || H > (1 << 15))
+    return fail(HLA_ERR_UNSUPPORTED, "Hilbert order needs H == W == 2^k <= 32768 (got %dx%d)", H, W);
+  if (order && !aligned(order, 4)) return fail(HLA_ERR_INVALID_ARG, "order is not 4-byte aligned");
+  if (rank && !aligned(rank, 4)) return fail(HLA_ERR_INVALID_ARG, "rank is not 4-byte aligned");
+  if (!order && !rank) return HLA_OK;
+  return hip_status(hla::launch_hilbert_perm(H, order, rank, (hipStream_t)stream), "hla_hilbert_perm");
+}
+
+static hla_status permute(const void *src, void *dst, const int32_t *order, int64_t B,
+                          int64_t heads, int64_t N, int64_t d, hla_dtype dt,
+                          hla_stream_t stream, bool scatter, const char *name) {
+  hla_status st;
+  if ((st = check_tensor_args(src, "src")) != HLA_OK) return st;
+  if ((st = check_tensor_args(dst, "dst")) != HLA_OK) return st;
+  if (!order) return fail(HLA_ERR_INVALID_ARG, "order is NULL");
+  if (!aligned(order, 4)) return fail(HLA_ERR_INVALID_ARG, "order is not 4-byte aligned");
+  if (B <= 0 || heads <= 0 || N <= 0 || d <= 0)
+    return fail(HLA_ERR_INVALID_ARG, "sizes must be positive (B=%lld heads=%lld N=%lld d=%lld)",
+                (long long)B, (long long)heads, (long long)N, (long long)d);
+  const int64_t es = dtype_size(dt);
+  if (!es) return fail(HLA_ERR_INVALID_ARG, "unknown dtype %d", (int)dt);
+  const int64_t row = d * es;
+  if (row % 4) return fail(HLA_ERR_UNSUPPORTED, "row of %lld bytes is not a multiple of 4", (long long)row);
+  if (N > kMaxI32 || N * (row / 4) > kMaxI32 / 2)
+    return fail(HLA_ERR_UNSUPPORTED, "N * row exceeds 2^30 words per (b, head) slice");
+  if (B * heads > (1LL << 40)) return fail(HLA_ERR_UNSUPPORTED, "B * heads too large");
+  const char *s = static_cast<const char *>(src);
+  const char *e = s + B * heads * N * row;
+  const char *o = static_cast<const char *>(dst);
+  if (o < e && s < o + B * heads * N * row) return fail(HLA_ERR_INVALID_ARG, "src and dst overlap");
+  return hip_status(hla::launch_permute(src, dst, order, B * heads, N, row, scatter, (hipStream_t)stream),
+                    name);
+}
+
+hla_status hla_gather(const void *src, void *dst, const int32_t *order, int64_t B,
+                      int64_t heads, int64_t N, int64_t d, hla_dtype dtype,
+                      hla_stream_t stream) {
+  return permute(src, dst, order, B, heads, N, d, dtype, stream, false, "hla_gather");
+}
+
+hla_status hla_scatter(const void *src, void *dst, const int32_t *order, int64_t B,
+                       int64_t heads, int64_t N, int64_t d, hla_dtype dtype,
+                       hla_stream_t stream) {
+  return permute(src, dst, order, B, heads, N, d, dtype, stream, true, "hla_scatter");
+}
+
+hla_status hla_block_mask_dims(const hla_pattern_desc *pat, int32_t tile_m, int32_t tile_n,
+                               int32_t *n_qtiles, int32_t *n_ktiles) {
+  hla_status st;
+  if ((st = check_pattern(pat)) != HLA_OK) return st;
+  if ((st = check_tiles(pat, tile_m, tile_n)) != HLA_OK) return st;
+  const int64_t N = (int64_t)pat->H * pat->W;
+  if (n_qtiles) *n_qtiles = (int32_t)(N / tile_m);
+  if (n_ktiles) *n_ktiles = (int32_t)(N / tile_n);
+  return HLA_OK;
+}
+
+hla_status hla_build_block_mask(hla_block_mask *mask, hla_stream_t stream) {
+  if (!mask) return fail(HLA_ERR_INVALID_ARG, "mask is NULL");
+  int32_t nq = 0, nk = 0;
+  hla_status st = hla_block_mask_dims(&mask->pat, mask->tile_m, mask->tile_n, &nq, &nk);
+  if (st != HLA_OK) return st;
+  if ((int64_t)nq * nk > kMaxI32) return fail(HLA_ERR_UNSUPPORTED, "tile grid %d x %d too large", nq, nk);
+  int32_t *arrs[4] = {mask->n_full, mask->full_idx, mask->n_part, mask->part_idx};
+  const char *names[4] = {"n_full", "full_idx", "n_part", "part_idx"};
+  for (int i = 0; i < 4; ++i) {
+    if (!arrs[i]) return fail(HLA_ERR_INVALID_ARG, "mask->%s is NULL", names[i]);
+    if (!aligned(arrs[i], 4)) return fail(HLA_ERR_INVALID_ARG, "mask->%s is not 4-byte aligned", names[i]);
+  }
+  if (mask->totals && !aligned(mask->totals, 4))
+    return fail(HLA_ERR_INVALID_ARG, "mask->totals is not 4-byte aligned");
+  mask->N = mask->pat.H * mask->pat.W;
+  mask->n_qtiles = nq;
+  mask->n_ktiles = nk;
+  const hla::PatternArgs pa = hla::make_pattern_args(mask->pat);
+  return hip_status(hla::launch_block_mask(pa, mask->tile_m, mask->tile_n, nq, nk, mask->n_full,
+                                           mask->full_idx, mask->n_part, mask->part_idx,
+                                           mask->totals, (hipStream_t)stream),
+                    "hla_build_block_mask");
+}
+
+hla_status hla_attn_fwd(const void *q, const void *k, const void *v, const hla_block_mask *mask,
+                        void *out, float *lse, int64_t B, int64_t heads, int64_t N, int64_t d,
+                        hla_dtype dtype, float scale, hla_stream_t stream) {
+  hla_status st;
+  if ((st = check_tensor_args(q, "q")) != HLA_OK) return st;
+  if ((st = check_tensor_args(k, "k")) != HLA_OK) return st;
+  if ((st = check_tensor_args(v, "v")) != HLA_OK) return st;
+  if ((st = check_tensor_args(out, "out")) != HLA_OK) return st;
+  if (lse && !aligned(lse, 4)) return fail(HLA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
+  if (!mask) return fail(HLA_ERR_INVALID_ARG, "mask is NULL");
+  if (!mask->n_full || !mask->full_idx || !mask->n_part || !mask->part_idx)
+    return fail(HLA_ERR_INVALID_ARG, "mask arrays are NULL (build the mask first)");
+  if (B <= 0 || heads <= 0 || N <= 0 || d <= 0)
+    return fail(HLA_ERR_INVALID_ARG, "sizes must be positive");
+  if (!(scale > 0.f) || scale > 1e30f) return fail(HLA_ERR_INVALID_ARG, "scale must be positive and finite");
+  if ((st = check_pattern(&mask->pat)) != HLA_OK) return st;
+  if ((st = check_tiles(&mask->pat, mask->tile_m, mask->tile_n)) != HLA_OK) return st;
+  const int64_t mN = (int64_t)mask->pat.H * mask->pat.W;
+  if (mask->N != mN || N != mN || mask->n_qtiles != mN / mask->tile_m ||
+      mask->n_ktiles != mN / mask->tile_n)
+    return fail(HLA_ERR_INVALID_ARG, "mask was built for N = %d, attention has N = %lld",
+                mask->N, (long long)N);
+  if (dtype != HLA_F32 && dtype != HLA_BF16) return fail(HLA_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+  if (d != 32 && d != 64) return fail(HLA_ERR_UNSUPPORTED, "head_dim %lld (supported: 32, 64)", (long long)d);
+  if (mask->tile_n != 64 || (mask->tile_m != 64 && mask->tile_m != 128))
+    return fail(HLA_ERR_UNSUPPORTED, "tile %dx%d (supported: 64x64, 128x64)", mask->tile_m, mask->tile_n);
+  if (N * d > (1LL << 30)) return fail(HLA_ERR_UNSUPPORTED, "N * d exceeds 2^30 per (b, head)");
+  const int64_t BH = B * heads;
+  if (BH * mask->n_qtiles > kMaxI32) return fail(HLA_ERR_UNSUPPORTED, "grid too large");
+  const int64_t bytes = BH * N * d * dtype_size(dtype);
+  const char *o = static_cast<const char *>(out);
+  for (const void *in : {q, k, v}) {
+    const char *s = static_cast<const char *>(in);
+    if (o < s + bytes && s < o + bytes) return fail(HLA_ERR_INVALID_ARG, "out overlaps an input");
+  }
+  hla::AttnArgs a;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.out = out;
+  a.lse = lse;
+  a.n_full = mask->n_full;
+  a.full_idx = mask->full_idx;
+  a.n_part = mask->n_part;
+  a.part_idx = mask->part_idx;
+  a.BH = (int32_t)BH;
+  a.N = (int32_t)N;
+  a.n_qtiles = mask->n_qtiles;
+  a.n_ktiles = mask->n_ktiles;
+  a.scale_log2 = (float)((double)scale * 1.4426950408889634074);
+  a.pat = hla::make_pattern_args(mask->pat);
+  hipError_t e = dtype == HLA_BF16
+                     ? hla::launch_attn_bf16(a, (int)d, mask->tile_m, mask->tile_n, (hipStream_t)stream)
+                     : hla::launch_attn_f32(a, (int)d, mask->tile_m, mask->tile_n, (hipStream_t)stream);
+  return hip_status(e, "hla_attn_fwd");
+}
+
+hla_status hla_qkv_proj(const void *x, const void *w_qkv, void *q, void *k, void *v, int64_t B,
+                        int64_t N, int64_t heads, int64_t d, hla_stream_t stream) {
+  hla_status st;
+  if ((st = check_tensor_args(x, "x")) != HLA_OK) return st;
+  if ((st = check_tensor_args(w_qkv, "w_qkv")) != HLA_OK) return st;
+  if ((st = check_tensor_args(q, "q")) != HLA_OK) return st;
+  if ((st = check_tensor_args(k, "k")) != HLA_OK) return st;
+  if ((st = check_tensor_args(v, "v")) != HLA_OK) return st;
+  if (B <= 0 || N <= 0 || heads <= 0 || d <= 0) return fail(HLA_ERR_INVALID_ARG, "sizes must be positive");
+  if (d != 32 && d != 64) return fail(HLA_ERR_UNSUPPORTED, "head_dim %lld (supported: 32, 64)", (long long)d);
+  const int64_t C = heads * d;
+  if (C % 64 || C > 512) return fail(HLA_ERR_UNSUPPORTED, "C = heads*d = %lld must be a multiple of 64, <= 512", (long long)C);
+  if (B * N * C > (1LL << 31) - 1 || B * N > (1LL << 31) - 256)
+    return fail(HLA_ERR_UNSUPPORTED, "B * N * C exceeds 2^31");
+  return hip_status(hla::launch_qkv_proj(x, w_qkv, q, k, v, B, N, heads, d, (hipStream_t)stream),
+                    "hla_qkv_proj");
+}
+
+hla_status hla_out_proj(const void *o, const void *w_proj, void *y, int64_t B, int64_t N,
+                        int64_t heads, int64_t d, int64_t c_out, hla_stream_t stream) {
+  hla_status st;
+  if ((st = check_tensor_args(o, "o")) != HLA_OK) return st;
+  if ((st = check_tensor_args(w_proj, "w_proj")) != HLA_OK) return st;
+  if ((st = check_tensor_args(y, "y")) != HLA_OK) return st;
+  if (B <= 0 || N <= 0 || heads <= 0 || d <= 0 || c_out <= 0)
+    return fail(HLA_ERR_INVALID_ARG, "sizes must be positive");
+  if (d != 32 && d != 64) return fail(HLA_ERR_UNSUPPORTED, "head_dim %lld (supported: 32, 64)", (long long)d);
+  const int64_t C = heads * d;
+  if (C % 64 || C > 512) return fail(HLA_ERR_UNSUPPORTED, "C = heads*d = %lld must be a multiple of 64, <= 512", (long long)C);
+  if (c_out % 64) return fail(HLA_ERR_UNSUPPORTED, "c_out = %lld must be a multiple of 64", (long long)c_out);
+  if (B * N * (C > c_out ? C : c_out) > (1LL << 31) - 1 || B * N > (1LL << 31) - 256)
+    return fail(HLA_ERR_UNSUPPORTED, "B * N * C exceeds 2^31");
+  return hip_status(hla::launch_out_proj(o, w_proj, y, B, N, heads, d, c_out, (hipStream_t)stream),
+                    "hla_out_proj");
+}
+
+}  // extern "C"

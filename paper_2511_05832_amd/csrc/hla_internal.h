@@ -1,0 +1,96 @@
+// Internal declarations shared by the HIP kernels and the C-ABI layer of libhla.
+// Launchers assume their arguments were validated by the C-ABI layer and return
+// the HIP status of the launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "hla.h"
+
+namespace hla {
+
+// Exact unsigned division by a runtime constant for numerators below 2^31
+// (round-up multiply-high method; Granlund & Montgomery, "Division by invariant
+// integers using multiplication", 1994): q = (umulhi(n, mul) + n) >> shift.
+struct FastDiv {
+  uint32_t div, mul, shift;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+  FastDiv f;
+  f.div = d;
+  uint32_t l = 0;
+  while ((1ull << l) < d) ++l;
+  f.shift = l;
+  f.mul = (uint32_t)(((1ull << 32) * ((1ull << l) - d)) / d + 1);
+  return f;
+}
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv &f) {
+  return (__umulhi(n, f.mul) + n) >> f.shift;
+}
+
+// Pattern in the form the kernels use. For the 1-D (Hilbert) patterns every
+// query's allowed keys form one interval [lo, hi]; for the 2-D row-major
+// patterns they form one rectangle of grid cells. See query_interval() and
+// query_rect() in the kernels.
+struct PatternArgs {
+  int32_t kind;
+  int32_t H, W, N;
+  int32_t p0, p1;
+  FastDiv wdiv;  // division by W (row-major patterns)
+};
+
+inline bool pattern_is_1d(int32_t kind) {
+  return kind == HLA_HILBERT_WINDOW || kind == HLA_HILBERT_SLIDE ||
+         kind == HLA_HILBERT_NEIGHBORHOOD || kind == HLA_HILBERT_SHIFTED_WINDOW;
+}
+
+inline PatternArgs make_pattern_args(const hla_pattern_desc &p) {
+  PatternArgs a;
+  a.kind = p.pattern;
+  a.H = p.H;
+  a.W = p.W;
+  a.N = p.H * p.W;
+  a.p0 = p.p0;
+  a.p1 = p.p1;
+  a.wdiv = make_fastdiv((uint32_t)p.W);
+  return a;
+}
+
+hipError_t launch_hilbert_perm(int32_t side, int32_t *order, int32_t *rank,
+                               hipStream_t s);
+
+hipError_t launch_permute(const void *src, void *dst, const int32_t *order,
+                          int64_t BH, int64_t N, int64_t row_bytes, bool scatter,
+                          hipStream_t s);
+
+hipError_t launch_block_mask(const PatternArgs &pat, int32_t tile_m,
+                             int32_t tile_n, int32_t n_qtiles, int32_t n_ktiles,
+                             int32_t *n_full, int32_t *full_idx, int32_t *n_part,
+                             int32_t *part_idx, int32_t *totals, hipStream_t s);
+
+struct AttnArgs {
+  const void *q, *k, *v;
+  void *out;
+  float *lse;
+  const int32_t *n_full, *full_idx, *n_part, *part_idx;
+  int32_t BH, N, n_qtiles, n_ktiles;
+  float scale_log2;  // scale * log2(e)
+  PatternArgs pat;
+};
+
+hipError_t launch_attn_bf16(const AttnArgs &a, int d, int tile_m, int tile_n,
+                            hipStream_t s);
+hipError_t launch_attn_f32(const AttnArgs &a, int d, int tile_m, int tile_n,
+                           hipStream_t s);
+
+hipError_t launch_qkv_proj(const void *x, const void *w, void *q, void *k, void *v,
+                           int64_t B, int64_t N, int64_t heads, int64_t d,
+                           hipStream_t s);
+hipError_t launch_out_proj(const void *o, const void *w, void *y, int64_t B,
+                           int64_t N, int64_t heads, int64_t d, int64_t c_out,
+                           hipStream_t s);
+
+}  // namespace hla

@@ -22,6 +22,14 @@ class Pat:
     def __init__(self, kind, H, W, p0, p1=0):
         self.kind, self.H, self.W, self.p0, self.p1 = kind, int(H), int(W), int(p0), int(p1)
 
+    @property
+    def N(self):
+        return self.H * self.W
+
+    @property
+    def hilbert(self):
+        return self.kind.startswith("hilbert")
+
     def __repr__(self):
         return f"Pat({self.kind},{self.H}x{self.W},{self.p0},{self.p1})"
 

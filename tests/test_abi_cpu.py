@@ -1,0 +1,163 @@
+"""The C-ABI library loads, exports every entry point include/hla.h declares, and
+rejects invalid arguments on the host before any HIP call (no GPU needed: every
+call here fails validation, so nothing is launched)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2511_05832_amd as hla
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hla.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:hla_status|const char \*)\s*(hla_\w+)\s*\(", text, re.M)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(hla.LIB_PATH):
+        pytest.fail("libhla.so is not built (run python -m paper_2511_05832_amd.build)")
+    return hla.lib()
+
+
+def test_header_declares_the_binding_names():
+    assert declared_functions() == sorted(hla.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol(L):
+    out = subprocess.run(["nm", "-D", "--defined-only", hla.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\s[TW]\s(hla_\w+)$", out, re.M))
+    for name in declared_functions():
+        assert name in exported, name
+        assert hasattr(L, name)
+
+
+def test_version_and_empty_error(L):
+    assert b"gfx950" in L.hla_version()
+
+
+def status_and_msg(L, st):
+    return st, L.hla_last_error().decode()
+
+
+def test_hilbert_rejects_non_power_of_two(L):
+    st, msg = status_and_msg(L, L.hla_hilbert_perm(96, 96, None, None, None))
+    assert st == hla.HLA_ERR_UNSUPPORTED and "2^k" in msg
+    st, _ = status_and_msg(L, L.hla_hilbert_perm(64, 128, None, None, None))
+    assert st == hla.HLA_ERR_UNSUPPORTED
+    st, _ = status_and_msg(L, L.hla_hilbert_perm(64, 64, ctypes.c_void_p(2), None, None))
+    assert st == hla.HLA_ERR_INVALID_ARG
+
+
+def test_permute_validation(L):
+    vp = ctypes.c_void_p
+    a, b, o = vp(0x10000), vp(0x20000), vp(0x30000)
+    cases = [
+        ((None, b, o, 1, 1, 64, 64, hla.HLA_BF16, None), hla.HLA_ERR_INVALID_ARG, "src"),
+        ((a, vp(0x20008), o, 1, 1, 64, 64, hla.HLA_BF16, None), hla.HLA_ERR_INVALID_ARG, "aligned"),
+        ((a, b, None, 1, 1, 64, 64, hla.HLA_BF16, None), hla.HLA_ERR_INVALID_ARG, "order"),
+        ((a, b, o, 0, 1, 64, 64, hla.HLA_BF16, None), hla.HLA_ERR_INVALID_ARG, "positive"),
+        ((a, b, o, 1, 1, 64, 3, hla.HLA_BF16, None), hla.HLA_ERR_UNSUPPORTED, "multiple of 4"),
+        ((a, b, o, 1, 1, 64, 64, 7, None), hla.HLA_ERR_INVALID_ARG, "dtype"),
+        ((a, vp(0x10000 + 4096), o, 1, 1, 64, 64, hla.HLA_BF16, None), hla.HLA_ERR_INVALID_ARG, "overlap"),
+    ]
+    for fn in (L.hla_gather, L.hla_scatter):
+        for args, want, text in cases:
+            st, msg = status_and_msg(L, fn(*args))
+            assert st == want and text in msg, (args, st, msg)
+
+
+def desc(kind, H, W, p0, p1=0):
+    return hla.PatternDesc(hla.PATTERN_IDS[kind], H, W, p0, p1)
+
+
+def test_block_mask_dims(L):
+    nq, nk = ctypes.c_int32(), ctypes.c_int32()
+    d = desc("hilbert_slide", 256, 256, 512)
+    assert L.hla_block_mask_dims(ctypes.byref(d), 128, 64, ctypes.byref(nq), ctypes.byref(nk)) == 0
+    assert (nq.value, nk.value) == (512, 1024)
+    bad = [
+        (desc("hilbert_slide", 64, 64, 128), 96, 64, hla.HLA_ERR_UNSUPPORTED),     # not pow2
+        (desc("hilbert_slide", 56, 56, 24), 128, 128, hla.HLA_ERR_UNSUPPORTED),    # 128 does not divide 3136
+        (desc("hilbert_slide", 64, 64, -1), 128, 64, hla.HLA_ERR_INVALID_ARG),
+        (desc("hilbert_window", 64, 64, 0), 128, 64, hla.HLA_ERR_INVALID_ARG),
+        (desc("hilbert_shifted_window", 64, 64, 16, 16), 128, 64, hla.HLA_ERR_INVALID_ARG),
+        (desc("rowmajor_neighborhood", 64, 64, 65, 3), 128, 64, hla.HLA_ERR_INVALID_ARG),
+        (desc("hilbert_neighborhood", 8, 8, 65), 16, 16, hla.HLA_ERR_INVALID_ARG),
+        (hla.PatternDesc(42, 64, 64, 1, 1), 128, 64, hla.HLA_ERR_INVALID_ARG),
+        (desc("hilbert_window", 0, 64, 4), 128, 64, hla.HLA_ERR_INVALID_ARG),
+        (desc("hilbert_slide", 64, 64, 128), 2048, 64, hla.HLA_ERR_UNSUPPORTED),
+    ]
+    for d, tm, tn, want in bad:
+        st = L.hla_block_mask_dims(ctypes.byref(d), tm, tn, ctypes.byref(nq), ctypes.byref(nk))
+        assert st == want, (d.pattern, tm, tn, st, L.hla_last_error())
+
+
+def test_build_block_mask_rejects_null_arrays(L):
+    m = hla.BlockMaskStruct()
+    m.pat = desc("hilbert_slide", 64, 64, 128)
+    m.tile_m, m.tile_n = 128, 64
+    assert L.hla_build_block_mask(ctypes.byref(m), None) == hla.HLA_ERR_INVALID_ARG
+    assert "n_full" in L.hla_last_error().decode()
+    assert L.hla_build_block_mask(None, None) == hla.HLA_ERR_INVALID_ARG
+
+
+def fake_mask(kind="hilbert_slide", H=64, W=64, p0=128, tm=128, tn=64):
+    m = hla.BlockMaskStruct()
+    m.pat = desc(kind, H, W, p0)
+    m.tile_m, m.tile_n = tm, tn
+    m.N = H * W
+    m.n_qtiles, m.n_ktiles = H * W // tm, H * W // tn
+    m.n_full = m.full_idx = m.n_part = m.part_idx = 0x40000
+    return m
+
+
+def test_attn_validation(L):
+    vp = ctypes.c_void_p
+    q, k, v, o = vp(0x100000), vp(0x200000), vp(0x300000), vp(0x400000)
+    N = 4096
+
+    def call(m, d=64, dt=hla.HLA_BF16, scale=0.125, N_=N, out=o, B=2, heads=4):
+        return L.hla_attn_fwd(q, k, v, ctypes.byref(m), out, None, B, heads, N_, d, dt, scale, None)
+
+    m = fake_mask()
+    assert call(m, d=48) == hla.HLA_ERR_UNSUPPORTED
+    assert call(m, d=128) == hla.HLA_ERR_UNSUPPORTED
+    assert call(m, N_=2048) == hla.HLA_ERR_INVALID_ARG and "built for" in L.hla_last_error().decode()
+    assert call(m, scale=0.0) == hla.HLA_ERR_INVALID_ARG
+    assert call(m, scale=float("nan")) == hla.HLA_ERR_INVALID_ARG
+    assert call(m, dt=5) == hla.HLA_ERR_INVALID_ARG
+    assert call(m, out=vp(0x100000 + 4096)) == hla.HLA_ERR_INVALID_ARG
+    assert call(m, out=vp(0x400004)) == hla.HLA_ERR_INVALID_ARG
+    assert call(fake_mask(tm=64, tn=128)) == hla.HLA_ERR_UNSUPPORTED
+    assert call(fake_mask(tm=256, tn=64)) == hla.HLA_ERR_UNSUPPORTED
+    m0 = fake_mask()
+    m0.n_part = 0
+    assert call(m0) == hla.HLA_ERR_INVALID_ARG
+    assert L.hla_attn_fwd(q, k, v, None, o, None, 2, 4, N, 64, hla.HLA_BF16, 0.1, None) == hla.HLA_ERR_INVALID_ARG
+
+
+def test_proj_validation(L):
+    vp = ctypes.c_void_p
+    x, w, q, k, v = (vp(0x100000 * i) for i in range(1, 6))
+    assert L.hla_qkv_proj(x, w, q, k, v, 16, 4096, 6, 48, None) == hla.HLA_ERR_UNSUPPORTED
+    assert L.hla_qkv_proj(x, w, q, k, v, 16, 4096, 3, 32, None) == hla.HLA_ERR_UNSUPPORTED  # C = 96
+    assert L.hla_qkv_proj(None, w, q, k, v, 16, 4096, 6, 32, None) == hla.HLA_ERR_INVALID_ARG
+    assert L.hla_qkv_proj(x, w, q, k, v, 0, 4096, 6, 32, None) == hla.HLA_ERR_INVALID_ARG
+    assert L.hla_out_proj(x, w, q, 16, 4096, 6, 32, 100, None) == hla.HLA_ERR_UNSUPPORTED
+    assert L.hla_out_proj(x, w, vp(0x300008), 16, 4096, 6, 32, 192, None) == hla.HLA_ERR_INVALID_ARG
+
+
+def test_binding_fails_loudly_without_gpu_tensors():
+    import torch
+    x = torch.zeros(2, 4, 64, 64, dtype=torch.bfloat16)
+    order = torch.arange(64, dtype=torch.int32)
+    with pytest.raises(hla.HLAError):
+        hla.gather(x, order)

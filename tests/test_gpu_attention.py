@@ -1,0 +1,150 @@
+"""GPU parity: block-sparse attention forward against the oracle's dense masked
+attention in float64 on the same seeded inputs.
+
+Bars: out max-abs <= 2e-2 for bf16 I/O (fp32 accumulation) and <= 1e-4 for fp32;
+log-sum-exp max-abs <= 1e-3. The measured workloads run in the launch
+configuration the bench times; the largest ones are checked on sampled query rows
+the oracle computes one by one (tile edges, both sequence ends, random rows).
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2511_05832_amd as hla
+import workloads as W
+from conftest import Pat
+from helpers import (TOL_LSE, TOL_OUT, max_abs, np64, oracle_attention,
+                     run_hip_attention, sample_rows)
+
+pytestmark = pytest.mark.gpu
+
+
+def check(pattern, q, k, v, tile_m, tile_n, scale, dtype, rows=None, gather=None):
+    out, lse, _ = run_hip_attention(pattern, q, k, v, tile_m, tile_n, scale, gather)
+    ref_out, ref_lse = oracle_attention(pattern, q, k, v, scale, rows=rows, gather=gather)
+    got_out = np64(out) if rows is None else np64(out)[:, :, rows]
+    got_lse = np64(lse) if rows is None else np64(lse)[:, :, rows]
+    e_out, e_lse = max_abs(got_out, ref_out), max_abs(got_lse, ref_lse)
+    print(f"{pattern} tiles {tile_m}x{tile_n} {dtype}: out err {e_out:.3e}, lse err {e_lse:.3e}")
+    assert e_out <= TOL_OUT[dtype], e_out
+    assert e_lse <= TOL_LSE, e_lse
+    assert np.isfinite(got_out).all()
+    return out, lse
+
+
+@pytest.mark.parametrize("w", [W.C1, W.C2], ids=lambda w: w.name)
+def test_small_workloads_every_row(w):
+    q, k, v = W.workload_inputs(w)
+    check(w.pattern, q, k, v, w.tile_m, w.tile_n, w.scale, w.dtype)
+
+
+@pytest.mark.parametrize("w", [W.C3, W.C3_ROWMAJOR, W.C4, W.C4_ROWMAJOR], ids=lambda w: w.name)
+def test_full_size_workloads_sampled_rows(w):
+    q, k, v = W.workload_inputs(w)
+    rows = sample_rows(w.N, w.tile_m, w.seed, n_random=96)
+    check(w.pattern, q, k, v, w.tile_m, w.tile_n, w.scale, w.dtype, rows=rows)
+
+
+def random_cases(n):
+    rng = np.random.default_rng(77)
+    kinds = list(hla.PATTERN_IDS)
+    cases = []
+    for i in range(n):
+        kind = kinds[i % len(kinds)]
+        dtype = "bf16" if i % 3 else "f32"
+        d = int(rng.choice([32, 64]))
+        tm = int(rng.choice([64, 128]))
+        H = int(rng.choice([16, 24, 32]))
+        Wd = int(rng.choice([16, 32, 40]))
+        N = H * Wd
+        if N % tm:
+            tm = 64
+        if N % 64:
+            Wd, N = 16, H * 16
+        if kind == "hilbert_window":
+            pat = Pat(kind, H, Wd, int(rng.choice([1, 16, 64, 100, 256, N])))
+        elif kind == "hilbert_slide":
+            pat = Pat(kind, H, Wd, int(rng.choice([0, 1, 5, 40, 128, N])))
+        elif kind == "hilbert_neighborhood":
+            pat = Pat(kind, H, Wd, int(rng.choice([1, 9, 49, 81, min(N, 300)])))
+        elif kind == "hilbert_shifted_window":
+            w = int(rng.choice([16, 64, 100]))
+            pat = Pat(kind, H, Wd, w, int(rng.integers(0, w)))
+        elif kind == "rowmajor_window":
+            pat = Pat(kind, H, Wd, int(rng.choice([1, 2, 4, 7])), int(rng.choice([2, 4, 5, 16])))
+        elif kind == "rowmajor_slide":
+            pat = Pat(kind, H, Wd, int(rng.choice([0, 1, 3])), int(rng.choice([0, 2, 4])))
+        else:
+            pat = Pat(kind, H, Wd, int(rng.choice([1, 3, 7])), int(rng.choice([1, 3, 5])))
+        B, Hh = int(rng.integers(1, 3)), int(rng.integers(1, 4))
+        cases.append((pat, B, Hh, d, dtype, tm, 1000 + i))
+    return cases
+
+
+@pytest.mark.parametrize("pat,B,Hh,d,dtype,tm,seed", random_cases(42),
+                         ids=lambda x: repr(x) if isinstance(x, Pat) else str(x))
+def test_random_shapes_every_row(pat, B, Hh, d, dtype, tm, seed):
+    """Tensors taken as already in sequence order (most of these grids have no Hilbert
+    curve; the Hilbert patterns only look at sequence positions)."""
+    q, k, v = W.random_shape_inputs(seed, B, Hh, pat.N, d, dtype)
+    check(pat, q, k, v, tm, 64, 1.0 / d ** 0.5, dtype, gather=False)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_diagonal_mask_returns_v(dtype):
+    """Band h = 0: each query attends only itself, so out = v (exactly after rounding
+    to bf16; within an ulp in fp32) and lse = scale * <q_i, k_i>."""
+    pat = Pat("hilbert_slide", 32, 32, 0)
+    q, k, v = W.random_shape_inputs(5, 2, 2, 1024, 64, dtype)
+    out, lse, order = run_hip_attention(pat, q, k, v, 128, 64, 0.125)
+    vh = v[:, :, torch.from_numpy(order.astype(np.int64))]
+    if dtype == "bf16":
+        assert torch.equal(out, vh)
+    else:
+        assert max_abs(np64(out), np64(vh)) <= 1e-6
+    qh = np64(q)[:, :, order]
+    kh = np64(k)[:, :, order]
+    ref = 0.125 * np.einsum("bhnd,bhnd->bhn", qh, kh)
+    assert max_abs(np64(lse), ref) <= 1e-4
+
+
+def test_dense_limit_matches_unmasked_softmax():
+    """Window longer than the sequence: every tile full, plain softmax attention."""
+    pat = Pat("hilbert_window", 32, 32, 4096)
+    q, k, v = W.random_shape_inputs(6, 1, 2, 1024, 64, "bf16")
+    mask = hla.build_block_mask(pat, 128, 64)
+    assert mask.host_totals() == (8 * 16, 0)
+    check(pat, q, k, v, 128, 64, 0.125, "bf16")
+
+
+def test_deterministic_and_out_of_place():
+    w = W.C2
+    q, k, v = W.workload_inputs(w)
+    a = run_hip_attention(w.pattern, q, k, v, w.tile_m, w.tile_n, w.scale)
+    b = run_hip_attention(w.pattern, q, k, v, w.tile_m, w.tile_n, w.scale)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+def test_large_logits_stay_finite():
+    """q, k scaled up so scores reach hundreds: the online softmax must not overflow.
+    v stays N(0, 1), the regime the 2e-2 bar is stated for."""
+    pat = Pat("hilbert_slide", 32, 32, 100)
+    q, k, _ = W.random_shape_inputs(8, 1, 2, 1024, 64, "bf16", std=4.0)
+    _, _, v = W.random_shape_inputs(9, 1, 2, 1024, 64, "bf16")
+    check(pat, q, k, v, 128, 64, 1.0, "bf16")
+
+
+def test_without_lse():
+    pat = Pat("hilbert_window", 32, 32, 64)
+    q, k, v = (t.cuda() for t in W.random_shape_inputs(9, 1, 1, 1024, 64, "bf16"))
+    mask = hla.build_block_mask(pat, 128, 64)
+    out, lse = hla.attn_fwd(q, k, v, mask, 0.125, with_lse=False)
+    out2, _ = hla.attn_fwd(q, k, v, mask, 0.125)
+    assert lse is None and torch.equal(out, out2)
+
+
+def test_mask_size_mismatch_is_rejected():
+    mask = hla.build_block_mask(Pat("hilbert_window", 32, 32, 64), 128, 64)
+    q = torch.zeros((1, 1, 4096, 64), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(hla.HLAError):
+        hla.attn_fwd(q, q.clone(), q.clone(), mask)

@@ -38,6 +38,9 @@ def common_flags(debug: bool):
     flags = [f"--offload-arch={ARCH}", "-std=c++17", "-fPIC", "-I", INCLUDE, "-I", CSRC,
              # keep the compiler from forming packed fp32 ops on its own
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+             # matrix-core accumulators in ordinary VGPRs: the softmax and rescale
+             # work on them with VALU ops, which cannot read AGPRs
+             "-mllvm", "-amdgpu-mfma-vgpr-form=1",
              "-Wall", "-Wno-unused-result", "-Wno-unused-variable",
              "-Wno-unknown-pragmas"]
     flags += ["-O1", "-g"] if debug else ["-O3"]

@@ -30,7 +30,11 @@
 //
 // LDS per stage: K as [BN][D+8] and V transposed as [D][BN+8] (bf16, padded so
 // the 16-byte MFMA operand reads of 32 lanes hit distinct banks); two stages,
-// filled from registers that were loaded one tile ahead, one barrier per tile.
+// filled from registers that were loaded two tiles ahead, one barrier per tile.
+// Tile-list entries are read with scalar loads, so waiting for one never waits
+// for the K/V vector loads in flight. Accumulators live in ordinary VGPRs (the
+// library is built with the VGPR form of MFMA), so the softmax touches them
+// without copies.
 //
 // Masking (partial tiles only). For the 1-D Hilbert patterns each query's
 // allowed keys are one interval [lo, hi] computed once per lane; for the
@@ -51,6 +55,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int BN = 64;
 constexpr int VS = BN + 8;  // row stride of transposed V in LDS (elements)
@@ -68,6 +73,73 @@ __device__ __forceinline__ int xcd_remap(int bid, int total) {
 }
 
 __device__ __forceinline__ int clampi(int x, int lo, int hi) { return min(max(x, lo), hi); }
+
+// Scalar (SMEM) load of a wave-uniform int through the constant address space.
+__device__ __forceinline__ int sload(const int32_t *p) {
+  return *(const __attribute__((address_space(4))) int32_t *)p;
+}
+
+// K tile rows are copied as 16-byte units; V is read as (2 d x 8 keys) units of
+// eight 4-byte loads and written transposed (8 keys contiguous per d) after a
+// byte permute, so the PV operand reads are 16 contiguous bytes.
+template <int D, int NT>
+__device__ __forceinline__ void load_tile(u32x4 (&k)[(BN * D / 8 + NT - 1) / NT],
+                                          uint32_t (&v)[((D / 2) * (BN / 8) + NT - 1) / NT][8],
+                                          const __bf16 *K, const __bf16 *V, int kt, int tid) {
+  constexpr int KUNITS = BN * D / 8, KPT = (KUNITS + NT - 1) / NT;
+  constexpr int VUNITS = (D / 2) * (BN / 8), VPT = (VUNITS + NT - 1) / NT;
+  const __bf16 *Kt = K + (int64_t)kt * BN * D;
+  const __bf16 *Vt = V + (int64_t)kt * BN * D;
+#pragma unroll
+  for (int u = 0; u < KPT; ++u) {
+    const int id = tid + u * NT;
+    if (KUNITS % NT == 0 || id < KUNITS)
+      k[u] = *reinterpret_cast<const u32x4 *>(Kt + (id / (D / 8)) * D + (id % (D / 8)) * 8);
+  }
+#pragma unroll
+  for (int u = 0; u < VPT; ++u) {
+    const int id = tid + u * NT;
+    if (VUNITS % NT == 0 || id < VUNITS) {
+      const int dp = id % (D / 2), kg = id / (D / 2);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        v[u][j] = *reinterpret_cast<const uint32_t *>(Vt + (kg * 8 + j) * D + 2 * dp);
+    }
+  }
+}
+
+template <int D, int NT>
+__device__ __forceinline__ void store_tile(const u32x4 (&k)[(BN * D / 8 + NT - 1) / NT],
+                                           const uint32_t (&v)[((D / 2) * (BN / 8) + NT - 1) / NT][8],
+                                           __bf16 *Ks, __bf16 *Vs, int tid) {
+  constexpr int KS = D + 8;
+  constexpr int KUNITS = BN * D / 8, KPT = (KUNITS + NT - 1) / NT;
+  constexpr int VUNITS = (D / 2) * (BN / 8), VPT = (VUNITS + NT - 1) / NT;
+#pragma unroll
+  for (int u = 0; u < KPT; ++u) {
+    const int id = tid + u * NT;
+    if (KUNITS % NT == 0 || id < KUNITS)
+      *reinterpret_cast<u32x4 *>(Ks + (id / (D / 8)) * KS + (id % (D / 8)) * 8) = k[u];
+  }
+#pragma unroll
+  for (int u = 0; u < VPT; ++u) {
+    const int id = tid + u * NT;
+    if (VUNITS % NT == 0 || id < VUNITS) {
+      const int dp = id % (D / 2), kg = id / (D / 2);
+      u32x4 lo4, hi4;  // d = 2dp (low halves) and d = 2dp+1 (high halves), 8 keys each
+      lo4.x = __builtin_amdgcn_perm(v[u][1], v[u][0], 0x05040100u);
+      lo4.y = __builtin_amdgcn_perm(v[u][3], v[u][2], 0x05040100u);
+      lo4.z = __builtin_amdgcn_perm(v[u][5], v[u][4], 0x05040100u);
+      lo4.w = __builtin_amdgcn_perm(v[u][7], v[u][6], 0x05040100u);
+      hi4.x = __builtin_amdgcn_perm(v[u][1], v[u][0], 0x07060302u);
+      hi4.y = __builtin_amdgcn_perm(v[u][3], v[u][2], 0x07060302u);
+      hi4.z = __builtin_amdgcn_perm(v[u][5], v[u][4], 0x07060302u);
+      hi4.w = __builtin_amdgcn_perm(v[u][7], v[u][6], 0x07060302u);
+      *reinterpret_cast<u32x4 *>(Vs + (2 * dp) * VS + kg * 8) = lo4;
+      *reinterpret_cast<u32x4 *>(Vs + (2 * dp + 1) * VS + kg * 8) = hi4;
+    }
+  }
+}
 
 template <int D, int NW>
 __global__ void __launch_bounds__(64 * NW)
@@ -136,61 +208,12 @@ __global__ void __launch_bounds__(64 * NW)
     }
   }
 
-  const int nf = a.n_full[qt], np = a.n_part[qt], ntot = nf + np;
+  // Tile-list reads are uniform: load them through the scalar unit so that
+  // waiting for one never waits for the K/V vector loads in flight.
+  const int nf = sload(a.n_full + qt), np = sload(a.n_part + qt), ntot = nf + np;
   const int32_t *frow = a.full_idx + (int64_t)qt * a.n_ktiles;
   const int32_t *prow = a.part_idx + (int64_t)qt * a.n_ktiles;
-
-  // Staging registers for the next K/V tile.
-  uint4 kreg[KPT];
-  uint32_t vreg[VPT][8];
-  auto load_tile = [&](int kt) {
-    const __bf16 *Kt = K + (int64_t)kt * BN * D;
-    const __bf16 *Vt = V + (int64_t)kt * BN * D;
-#pragma unroll
-    for (int u = 0; u < KPT; ++u) {
-      const int id = tid + u * NT;
-      if (KUNITS % NT == 0 || id < KUNITS)
-        kreg[u] = *reinterpret_cast<const uint4 *>(Kt + (id / (D / 8)) * D + (id % (D / 8)) * 8);
-    }
-#pragma unroll
-    for (int u = 0; u < VPT; ++u) {
-      const int id = tid + u * NT;
-      if (VUNITS % NT == 0 || id < VUNITS) {
-        const int dp = id % (D / 2), kg = id / (D / 2);
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          vreg[u][j] = *reinterpret_cast<const uint32_t *>(Vt + (kg * 8 + j) * D + 2 * dp);
-      }
-    }
-  };
-  auto store_tile = [&](int stage) {
-    __bf16 *Ks = lds + stage * STAGE;
-    __bf16 *Vs = Ks + BN * KS;
-#pragma unroll
-    for (int u = 0; u < KPT; ++u) {
-      const int id = tid + u * NT;
-      if (KUNITS % NT == 0 || id < KUNITS)
-        *reinterpret_cast<uint4 *>(Ks + (id / (D / 8)) * KS + (id % (D / 8)) * 8) = kreg[u];
-    }
-#pragma unroll
-    for (int u = 0; u < VPT; ++u) {
-      const int id = tid + u * NT;
-      if (VUNITS % NT == 0 || id < VUNITS) {
-        const int dp = id % (D / 2), kg = id / (D / 2);
-        uint4 lo4, hi4;  // d = 2dp (low halves) and d = 2dp+1 (high halves), 8 keys each
-        lo4.x = __builtin_amdgcn_perm(vreg[u][1], vreg[u][0], 0x05040100u);
-        lo4.y = __builtin_amdgcn_perm(vreg[u][3], vreg[u][2], 0x05040100u);
-        lo4.z = __builtin_amdgcn_perm(vreg[u][5], vreg[u][4], 0x05040100u);
-        lo4.w = __builtin_amdgcn_perm(vreg[u][7], vreg[u][6], 0x05040100u);
-        hi4.x = __builtin_amdgcn_perm(vreg[u][1], vreg[u][0], 0x07060302u);
-        hi4.y = __builtin_amdgcn_perm(vreg[u][3], vreg[u][2], 0x07060302u);
-        hi4.z = __builtin_amdgcn_perm(vreg[u][5], vreg[u][4], 0x07060302u);
-        hi4.w = __builtin_amdgcn_perm(vreg[u][7], vreg[u][6], 0x07060302u);
-        *reinterpret_cast<uint4 *>(Vs + (2 * dp) * VS + kg * 8) = lo4;
-        *reinterpret_cast<uint4 *>(Vs + (2 * dp + 1) * VS + kg * 8) = hi4;
-      }
-    }
-  };
+  auto tile_of = [&](int i) { return i < nf ? sload(frow + i) : sload(prow + i - nf); };
 
   f32x16 oacc[NDB];
 #pragma unroll
@@ -200,87 +223,107 @@ __global__ void __launch_bounds__(64 * NW)
   const float sl2 = a.scale_log2;
   const int krow = key_of_row(col);
 
-  if (ntot > 0) load_tile(nf > 0 ? frow[0] : prow[0]);
+  // Two register stagings for the K/V tiles in flight (each tile is loaded two
+  // iterations ahead of its use) and two LDS stages. Iteration `it` writes LDS
+  // stage it % 2; the last reader of that stage was iteration it - 2, and every
+  // wave has passed iteration it - 1's barrier since, so one barrier per tile
+  // suffices. The stagings are separate named arrays (not one array indexed by
+  // the iteration) so they stay in registers.
+  u32x4 kA[KPT], kB[KPT];
+  uint32_t vA[VPT][8], vB[VPT][8];
+  if (ntot > 0) load_tile<D, NT>(kA, vA, K, V, tile_of(0), tid);
+  if (ntot > 1) load_tile<D, NT>(kB, vB, K, V, tile_of(1), tid);
 
-  for (int it = 0; it < ntot; ++it) {
-    const int stage = it & 1;
-    const bool masked = it >= nf;
-    const int kt = masked ? prow[it - nf] : frow[it];
-    store_tile(stage);
-    __syncthreads();
-    if (it + 1 < ntot) load_tile(it + 1 < nf ? frow[it + 1] : prow[it + 1 - nf]);
+  auto step = [&](auto &kst, auto &vst, const int it) __attribute__((always_inline)) {
+      const int stage = it & 1;
+      const int kt = tile_of(it);
+      __bf16 *Ks = lds + stage * STAGE;
+      __bf16 *Vs = Ks + BN * KS;
+      store_tile<D, NT>(kst, vst, Ks, Vs, tid);
+      __syncthreads();
+      if (it + 2 < ntot) load_tile<D, NT>(kst, vst, K, V, tile_of(it + 2), tid);
 
-    const __bf16 *Ks = lds + stage * STAGE;
-    const __bf16 *Vs = Ks + BN * KS;
-
-    // S^T for the two 32-key blocks.
-    f32x16 s[2];
+      // S^T for the two 32-key blocks.
+      f32x16 s[2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      s[kb] = f32x16{};
-      const __bf16 *kr = Ks + (kb * 32 + krow) * KS + half * (D / 2);
+      for (int kb = 0; kb < 2; ++kb) {
+        s[kb] = f32x16{};
+        const __bf16 *kr = Ks + (kb * 32 + krow) * KS + half * (D / 2);
 #pragma unroll
-      for (int c = 0; c < NCH; ++c) {
-        const bf16x8 kop = *reinterpret_cast<const bf16x8 *>(kr + 8 * c);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[c], s[kb], 0, 0, 0);
+        for (int c = 0; c < NCH; ++c) {
+          const bf16x8 kop = *reinterpret_cast<const bf16x8 *>(kr + 8 * c);
+          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[c], s[kb], 0, 0, 0);
+        }
       }
-    }
 
-    if (masked) {
-      const int kbase = kt * BN + 8 * half;
+      if (it >= nf) {  // partial tile: element mask
+        const int kbase = kt * BN + 8 * half;
+        if (one_d) {
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+              const int kpos = kbase + kb * 32 + 16 * (v >> 3) + (v & 7);
+              const bool ok = (kpos >= lo) & (kpos <= hi);
+              s[kb][v] = ok ? s[kb][v] : -__builtin_inff();
+            }
+        } else {
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+              const int kpos = kbase + kb * 32 + 16 * (v >> 3) + (v & 7);
+              const int r = (int)fdiv((uint32_t)kpos, P.wdiv), c = kpos - r * P.W;
+              const bool ok = (r >= rlo) & (r <= rhi) & (c >= clo) & (c <= chi);
+              s[kb][v] = ok ? s[kb][v] : -__builtin_inff();
+            }
+        }
+      }
+
+      // Online softmax (log2 domain).
+      float mx = s[0][0];
+#pragma unroll
+      for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[0][v]);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[1][v]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run, mx * sl2);
+      const float m_use = m_new == -__builtin_inff() ? 0.f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+      m_run = m_new;
+      float lsum = 0.f;
+      bf16x8 pop[4];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int kpos = kbase + kb * 32 + 16 * (v >> 3) + (v & 7);
-          bool ok;
-          if (one_d) {
-            ok = kpos >= lo && kpos <= hi;
-          } else {
-            const int r = (int)fdiv((uint32_t)kpos, P.wdiv), c = kpos - r * P.W;
-            ok = r >= rlo && r <= rhi && c >= clo && c <= chi;
-          }
-          if (!ok) s[kb][v] = -__builtin_inff();
+          const float pv = __builtin_amdgcn_exp2f(s[kb][v] * sl2 - m_use);
+          lsum += pv;
+          pop[kb * 2 + (v >> 3)][v & 7] = (__bf16)pv;
         }
       }
-    }
-
-    // Online softmax (log2 domain).
-    float mx = s[0][0];
+      l_run = l_run * alpha + lsum;
+      // Rescale O only when some row's max moved (alpha != 1 somewhere in the wave).
+      if (__ballot(alpha != 1.f)) {
 #pragma unroll
-    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[0][v]);
-#pragma unroll
-    for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[1][v]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx * sl2);
-    const float m_use = m_new == -__builtin_inff() ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    m_run = m_new;
-    float lsum = 0.f;
-    bf16x8 pop[4];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(s[kb][v] * sl2 - m_use);
-        lsum += p;
-        pop[kb * 2 + (v >> 3)][v & 7] = (__bf16)p;
+        for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
       }
-    }
-    l_run = l_run * alpha + lsum;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
 
-    // O^T += V^T P^T over four 16-key steps.
+      // O^T += V^T P^T over four 16-key steps.
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      const __bf16 *vr = Vs + (db * 32 + col) * VS + 8 * half;
+      for (int db = 0; db < NDB; ++db) {
+        const __bf16 *vr = Vs + (db * 32 + col) * VS + 8 * half;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const bf16x8 vop = *reinterpret_cast<const bf16x8 *>(vr + 16 * t);
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[t], oacc[db], 0, 0, 0);
+        for (int t = 0; t < 4; ++t) {
+          const bf16x8 vop = *reinterpret_cast<const bf16x8 *>(vr + 16 * t);
+          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[t], oacc[db], 0, 0, 0);
+        }
       }
-    }
+  };
+
+  for (int it = 0; it < ntot; it += 2) {
+    step(kA, vA, it);
+    if (it + 1 < ntot) step(kB, vB, it + 1);
   }
 
   // Epilogue: normalise, stage O through LDS, write rows coalesced.

@@ -208,6 +208,32 @@ class LayerPipeline:
         return 2 * w.B * w.N * w.C * 2 + 4 * w.N
 
 
+ATTN_SOURCES = ("paper_2511_05832_amd/csrc/attn_bf16.hip", "paper_2511_05832_amd/csrc/hla_internal.h")
+
+
+def measured_traffic(workload_name):
+    """HBM bytes per attention dispatch from the committed rocprofv3 counter summary
+    for this workload, or None if there is none or the kernel source changed since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"attn_fwd_bf16_{workload_name}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        k, sep, v = line.partition(":")
+        if sep:
+            fields[k.strip()] = v.strip()
+    h = hashlib.sha256()
+    for src in ATTN_SOURCES:
+        h.update(open(os.path.join(ROOT, src), "rb").read())
+    if fields.get("kernel_source_sha256") != h.hexdigest():
+        return None
+    try:
+        return int(fields["traffic_bytes_per_dispatch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def make_pipeline(w, hla):
     return LayerPipeline(w, hla) if isinstance(w, W.LayerWorkload) else AttnPipeline(w, hla)
 
@@ -336,6 +362,9 @@ def main():
     ap.add_argument("--all", action="store_true",
                     help="also time every workload and write gpurun_out/bench_all.json")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="before the steps, time a plain device-to-device copy of this many MiB "
+                         "(a kernel of known traffic, to calibrate HBM byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -350,6 +379,15 @@ def main():
     hla.lib()
     torch.cuda.set_device(0)
 
+    if args.copy_mib:
+        src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] copied {args.copy_mib} MiB x 5", file=sys.stderr, flush=True)
+        del src, dst
+
     w = W.WORKLOADS[args.workload]
     pipe = make_pipeline(w, hla)
     ms = run_timed(pipe, args.steps, args.warmup)
@@ -357,7 +395,7 @@ def main():
     print(f"[bench] {w.name}: {json.dumps(res)}", file=sys.stderr, flush=True)
 
     compare = args.compare
-    if compare is None:
+    if compare is None and not args.copy_mib:
         compare = {W.C3.name: W.C3_ROWMAJOR.name, W.C4.name: W.C4_ROWMAJOR.name}.get(w.name)
     cmp_res = None
     if compare:
@@ -390,13 +428,15 @@ def main():
     if t_hbm >= t_mfma:
         achieved = pipe.attn_bytes() / attn_s / 1e9
         roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": achieved / HBM_PEAK_GBS, "traffic": None, "kernel": "attn_fwd",
+                    "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(w.name),
+                    "kernel": "attn_fwd",
                     "algorithmic_bytes": pipe.attn_bytes(),
                     "mfma_frac": res["attn_tile_tflops"] / (BF16_PEAK_TFLOPS if is_bf16 else FP32_PEAK_TFLOPS)}
     else:
         peak = BF16_PEAK_TFLOPS if is_bf16 else FP32_PEAK_TFLOPS
         roofline = {"bound": "mfma", "achieved": res["attn_tile_tflops"], "peak": peak,
-                    "unit": "TFLOP/s", "frac": res["attn_tile_tflops"] / peak, "traffic": None,
+                    "unit": "TFLOP/s", "frac": res["attn_tile_tflops"] / peak,
+                    "traffic": measured_traffic(w.name),
                     "kernel": "attn_fwd", "algorithmic_flops": flops,
                     "hbm_frac": pipe.attn_bytes() / attn_s / 1e9 / HBM_PEAK_GBS}
 

@@ -59,6 +59,11 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int BN = 64;
 constexpr int VS = BN + 8;  // row stride of transposed V in LDS (elements)
+constexpr float kRescaleSlack = 8.f;  // log2 units the softmax reference may lag the max
+
+// Combine a value of lane l with lane l ^ 32 (the other half of a query's keys).
+__device__ __forceinline__ float xhalf_max(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
+__device__ __forceinline__ float xhalf_sum(float x) { return x + __shfl_xor(x, 32); }
 
 __device__ __forceinline__ int key_of_row(int i) {
   // accumulator row i = 8a + 4g + b  ->  key 16(a/2) + 8g + 4(a%2) + b
@@ -180,6 +185,7 @@ __global__ void __launch_bounds__(64 * NW)
   const PatternArgs &P = a.pat;
   const bool one_d = P.kind == HLA_HILBERT_WINDOW || P.kind == HLA_HILBERT_SLIDE ||
                      P.kind == HLA_HILBERT_NEIGHBORHOOD || P.kind == HLA_HILBERT_SHIFTED_WINDOW;
+  const bool row_runs = (P.W & 7) == 0;
   int lo = 0, hi = 0, rlo = 0, rhi = 0, clo = 0, chi = 0;
   if (P.kind == HLA_HILBERT_WINDOW) {
     lo = (qpos / P.p0) * P.p0;
@@ -243,29 +249,62 @@ __global__ void __launch_bounds__(64 * NW)
       __syncthreads();
       if (it + 2 < ntot) load_tile<D, NT>(kst, vst, K, V, tile_of(it + 2), tid);
 
-      // S^T for the two 32-key blocks.
-      f32x16 s[2];
+      // S^T for the two 32-key blocks: all K operand reads issued first, then the
+      // MFMAs with the two independent accumulators interleaved.
+      bf16x8 kop[2][NCH];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        s[kb] = f32x16{};
         const __bf16 *kr = Ks + (kb * 32 + krow) * KS + half * (D / 2);
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-          const bf16x8 kop = *reinterpret_cast<const bf16x8 *>(kr + 8 * c);
-          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[c], s[kb], 0, 0, 0);
-        }
+        for (int c = 0; c < NCH; ++c) kop[kb][c] = *reinterpret_cast<const bf16x8 *>(kr + 8 * c);
+      }
+      f32x16 s[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+      for (int c = 0; c < NCH; ++c)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kb][c], qop[c], s[kb], 0, 0, 0);
+
+      // V operand reads do not depend on the softmax: issue them now so their
+      // latency hides behind it.
+      bf16x8 vop[NDB][4];
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const __bf16 *vr = Vs + (db * 32 + col) * VS + 8 * half;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) vop[db][t] = *reinterpret_cast<const bf16x8 *>(vr + 16 * t);
       }
 
       if (it >= nf) {  // partial tile: element mask
-        const int kbase = kt * BN + 8 * half;
+        const int kbase = kt * BN + 8 * half;  // first key of this lane's runs (multiple of 8)
         if (one_d) {
+          // allowed iff lo <= key <= hi, as one unsigned compare
+          const int base = kbase - lo;
+          const uint32_t span = (uint32_t)(hi - lo);
 #pragma unroll
           for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-              const int kpos = kbase + kb * 32 + 16 * (v >> 3) + (v & 7);
-              const bool ok = (kpos >= lo) & (kpos <= hi);
+              const bool ok = (uint32_t)(base + kb * 32 + 16 * (v >> 3) + (v & 7)) <= span;
               s[kb][v] = ok ? s[kb][v] : -__builtin_inff();
+            }
+        } else if (row_runs) {
+          // W % 8 == 0: each aligned run of 8 keys lies in one grid row, so one
+          // division per run gives the row and the first column
+          const uint32_t rspan = (uint32_t)(rhi - rlo), cspan = (uint32_t)(chi - clo);
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int g = 0; g < 2; ++g) {
+              const int k0 = kbase + kb * 32 + 16 * g;
+              const int r = (int)fdiv((uint32_t)k0, P.wdiv);
+              const int c0 = k0 - r * P.W - clo;
+              const bool row_ok = (uint32_t)(r - rlo) <= rspan;
+#pragma unroll
+              for (int t = 0; t < 8; ++t) {
+                const bool ok = row_ok & ((uint32_t)(c0 + t) <= cspan);
+                s[kb][8 * g + t] = ok ? s[kb][8 * g + t] : -__builtin_inff();
+              }
             }
         } else {
 #pragma unroll
@@ -280,45 +319,48 @@ __global__ void __launch_bounds__(64 * NW)
         }
       }
 
-      // Online softmax (log2 domain).
+      // Online softmax in the log2 domain with a lazily moved reference: the
+      // exponent reference m_run only moves when a row's tile max exceeds it by
+      // more than kRescaleSlack, so the O / l rescale is rare. Weights stay
+      // <= 2^kRescaleSlack; the result is unchanged because O and l always share
+      // the same reference.
       float mx = s[0][0];
 #pragma unroll
       for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[0][v]);
 #pragma unroll
       for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[1][v]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run, mx * sl2);
-      const float m_use = m_new == -__builtin_inff() ? 0.f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-      m_run = m_new;
-      float lsum = 0.f;
+      mx = xhalf_max(mx);
+      const float mt = mx * sl2;
+      const bool grow = mt > m_run + kRescaleSlack;
+      if (__ballot(grow)) {
+        const float m_new = grow ? mt : m_run;
+        // 1 where unchanged; a row with no allowed key yet has nothing to rescale
+        const float alpha = m_new == -__builtin_inff() ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
+        m_run = m_new;
+      }
+      const float m_use = m_run == -__builtin_inff() ? 0.f : m_run;
+      // Row sums in fp32 from the unrounded weights (the log-sum-exp needs them to
+      // better than bf16 precision); P goes to the PV product rounded to bf16.
       bf16x8 pop[4];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const float pv = __builtin_amdgcn_exp2f(s[kb][v] * sl2 - m_use);
-          lsum += pv;
+          l_run += pv;
           pop[kb * 2 + (v >> 3)][v & 7] = (__bf16)pv;
         }
       }
-      l_run = l_run * alpha + lsum;
-      // Rescale O only when some row's max moved (alpha != 1 somewhere in the wave).
-      if (__ballot(alpha != 1.f)) {
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
-      }
 
-      // O^T += V^T P^T over four 16-key steps.
+      // O^T += V^T P^T over four 16-key steps, d blocks interleaved.
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        const __bf16 *vr = Vs + (db * 32 + col) * VS + 8 * half;
+      for (int t = 0; t < 4; ++t)
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const bf16x8 vop = *reinterpret_cast<const bf16x8 *>(vr + 16 * t);
-          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[t], oacc[db], 0, 0, 0);
-        }
-      }
+        for (int db = 0; db < NDB; ++db)
+          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[db][t], pop[t], oacc[db], 0, 0, 0);
   };
 
   for (int it = 0; it < ntot; it += 2) {
@@ -327,7 +369,7 @@ __global__ void __launch_bounds__(64 * NW)
   }
 
   // Epilogue: normalise, stage O through LDS, write rows coalesced.
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = xhalf_sum(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   __syncthreads();  // every wave is done reading K/V from LDS
   constexpr int OS = D + 8;

@@ -15,8 +15,9 @@
 //   softmax        lane l owns query l%32; its 32 scores of the tile sit in its
 //                  own accumulators (16 per key block, the other half of the keys
 //                  in lane l^32), so row max / sum need one cross-half exchange.
-//   O^T += V^T P^T (d x queries): D/32 blocks x 4 MFMAs. A = V^T from LDS,
-//                  B = P straight from the S^T accumulators (see below).
+//   O^T += V^T P^T (d x queries): D/32 blocks x 4 MFMAs. A = V^T read from LDS
+//                  with the transposing ds_read_b64_tr_b16, B = P straight from
+//                  the S^T accumulators (see below).
 //
 // Register-resident P. The accumulator of a 32x32 MFMA holds, in lane
 // (col = l%32, half = l/32) and slot v, row 8*(v/4) + 4*half + v%4. The K rows
@@ -28,13 +29,19 @@
 // in [half*D/2, (half+1)*D/2)), so each lane loads its Q slice as one
 // contiguous run.
 //
-// LDS per stage: K as [BN][D+8] and V transposed as [D][BN+8] (bf16, padded so
-// the 16-byte MFMA operand reads of 32 lanes hit distinct banks); two stages,
-// filled from registers that were loaded two tiles ahead, one barrier per tile.
-// Tile-list entries are read with scalar loads, so waiting for one never waits
-// for the K/V vector loads in flight. Accumulators live in ordinary VGPRs (the
-// library is built with the VGPR form of MFMA), so the softmax touches them
-// without copies.
+// K/V staging. K and V tiles go from global memory straight into LDS with
+// global_load_lds_dwordx4 (no register round trip), into a ring of kStages
+// stages kept kStages-1 tiles ahead. Both are stored row-major, 16-byte chunks
+// XOR-swizzled per row so that the K operand reads (ds_read_b128, eight lanes on
+// eight rows) and the transposing V reads (ds_read_b64_tr_b16, sixteen lanes on
+// four rows) each touch distinct bank groups; the swizzle is applied on the
+// source side (each lane fetches the chunk that belongs in its LDS slot). Before
+// each tile, a wave waits only for its own loads of that tile (an explicit
+// vmcnt that leaves the later tiles in flight), then one barrier makes the
+// stage visible to all waves.
+//
+// Tile-list entries are read with scalar loads. Accumulators live in ordinary
+// VGPRs (the library is built with the VGPR form of MFMA).
 //
 // Masking (partial tiles only). For the 1-D Hilbert patterns each query's
 // allowed keys are one interval [lo, hi] computed once per lane; for the
@@ -54,12 +61,18 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int BN = 64;
-constexpr int VS = BN + 8;  // row stride of transposed V in LDS (elements)
 constexpr float kRescaleSlack = 8.f;  // log2 units the softmax reference may lag the max
+// LDS ring depth. Three 16 KiB stages (d = 64) let three workgroups share a
+// CU's 160 KiB; with the launch bound below that is the occupancy that measured
+// fastest (four stages at two workgroups per CU, and two stages at four per CU,
+// were both slower).
+constexpr int kStages = 3;
 
 // Combine a value of lane l with lane l ^ 32 (the other half of a query's keys).
 __device__ __forceinline__ float xhalf_max(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
@@ -69,6 +82,18 @@ __device__ __forceinline__ int key_of_row(int i) {
   // accumulator row i = 8a + 4g + b  ->  key 16(a/2) + 8g + 4(a%2) + b
   const int a = i >> 3, g = (i >> 2) & 1, b = i & 3;
   return 16 * (a >> 1) + 8 * g + 4 * (a & 1) + b;
+}
+
+// Per-row XOR swizzle of the 16-byte chunks of a K / V tile row in LDS.
+template <int D>
+__device__ __forceinline__ int swz_k(int r) {
+  if (D == 64) return (r & 3) | (((r >> 3) & 1) << 2);
+  return ((r >> 1) & 1) | (((r >> 3) & 1) << 1);
+}
+template <int D>
+__device__ __forceinline__ int swz_v(int r) {
+  if (D == 64) return 2 * (r & 3);
+  return 2 * ((r >> 1) & 1);
 }
 
 __device__ __forceinline__ int xcd_remap(int bid, int total) {
@@ -84,85 +109,67 @@ __device__ __forceinline__ int sload(const int32_t *p) {
   return *(const __attribute__((address_space(4))) int32_t *)p;
 }
 
-// K tile rows are copied as 16-byte units; V is read as (2 d x 8 keys) units of
-// eight 4-byte loads and written transposed (8 keys contiguous per d) after a
-// byte permute, so the PV operand reads are 16 contiguous bytes.
-template <int D, int NT>
-__device__ __forceinline__ void load_tile(u32x4 (&k)[(BN * D / 8 + NT - 1) / NT],
-                                          uint32_t (&v)[((D / 2) * (BN / 8) + NT - 1) / NT][8],
-                                          const __bf16 *K, const __bf16 *V, int kt, int tid) {
-  constexpr int KUNITS = BN * D / 8, KPT = (KUNITS + NT - 1) / NT;
-  constexpr int VUNITS = (D / 2) * (BN / 8), VPT = (VUNITS + NT - 1) / NT;
-  const __bf16 *Kt = K + (int64_t)kt * BN * D;
-  const __bf16 *Vt = V + (int64_t)kt * BN * D;
-#pragma unroll
-  for (int u = 0; u < KPT; ++u) {
-    const int id = tid + u * NT;
-    if (KUNITS % NT == 0 || id < KUNITS)
-      k[u] = *reinterpret_cast<const u32x4 *>(Kt + (id / (D / 8)) * D + (id % (D / 8)) * 8);
-  }
-#pragma unroll
-  for (int u = 0; u < VPT; ++u) {
-    const int id = tid + u * NT;
-    if (VUNITS % NT == 0 || id < VUNITS) {
-      const int dp = id % (D / 2), kg = id / (D / 2);
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        v[u][j] = *reinterpret_cast<const uint32_t *>(Vt + (kg * 8 + j) * D + 2 * dp);
+// gfx950 LDS DMA (16 bytes per lane; lane l lands at dst + 16 l) and the
+// transposing 64-bit LDS read. Only the device pass may see these builtins:
+// the host pass of the HIP compiler rejects them silently and then emits no
+// launch stub for the kernel that calls them.
+__device__ __forceinline__ void lds_dma16(const void *src, lds_void *dst) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+#endif
+}
+__device__ __forceinline__ i16x4 lds_read_tr16(const char *p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p);
+#else
+  return i16x4{};
+#endif
+}
+
+// Wait until this wave's LDS reads are done and at most N of its vector memory
+// operations (here: K/V tile copies) are in flight, then barrier the workgroup.
+// One asm statement with a memory clobber, so the compiler moves no memory
+// access across it (a fence would instead wait for every copy in flight).
+template <int N>
+__device__ __forceinline__ void wait_then_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt out of range");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+// Dispatch on the number of tiles still allowed in flight (0 .. MAXA).
+template <int LPT, int MAXA>
+__device__ __forceinline__ void wait_tiles_then_barrier(int after) {
+  if constexpr (MAXA > 0) {
+    if (after >= MAXA) {
+      wait_then_barrier<MAXA * LPT>();
+      return;
     }
+    wait_tiles_then_barrier<LPT, MAXA - 1>(after);
+  } else {
+    wait_then_barrier<0>();
   }
 }
 
-template <int D, int NT>
-__device__ __forceinline__ void store_tile(const u32x4 (&k)[(BN * D / 8 + NT - 1) / NT],
-                                           const uint32_t (&v)[((D / 2) * (BN / 8) + NT - 1) / NT][8],
-                                           __bf16 *Ks, __bf16 *Vs, int tid) {
-  constexpr int KS = D + 8;
-  constexpr int KUNITS = BN * D / 8, KPT = (KUNITS + NT - 1) / NT;
-  constexpr int VUNITS = (D / 2) * (BN / 8), VPT = (VUNITS + NT - 1) / NT;
-#pragma unroll
-  for (int u = 0; u < KPT; ++u) {
-    const int id = tid + u * NT;
-    if (KUNITS % NT == 0 || id < KUNITS)
-      *reinterpret_cast<u32x4 *>(Ks + (id / (D / 8)) * KS + (id % (D / 8)) * 8) = k[u];
-  }
-#pragma unroll
-  for (int u = 0; u < VPT; ++u) {
-    const int id = tid + u * NT;
-    if (VUNITS % NT == 0 || id < VUNITS) {
-      const int dp = id % (D / 2), kg = id / (D / 2);
-      u32x4 lo4, hi4;  // d = 2dp (low halves) and d = 2dp+1 (high halves), 8 keys each
-      lo4.x = __builtin_amdgcn_perm(v[u][1], v[u][0], 0x05040100u);
-      lo4.y = __builtin_amdgcn_perm(v[u][3], v[u][2], 0x05040100u);
-      lo4.z = __builtin_amdgcn_perm(v[u][5], v[u][4], 0x05040100u);
-      lo4.w = __builtin_amdgcn_perm(v[u][7], v[u][6], 0x05040100u);
-      hi4.x = __builtin_amdgcn_perm(v[u][1], v[u][0], 0x07060302u);
-      hi4.y = __builtin_amdgcn_perm(v[u][3], v[u][2], 0x07060302u);
-      hi4.z = __builtin_amdgcn_perm(v[u][5], v[u][4], 0x07060302u);
-      hi4.w = __builtin_amdgcn_perm(v[u][7], v[u][6], 0x07060302u);
-      *reinterpret_cast<u32x4 *>(Vs + (2 * dp) * VS + kg * 8) = lo4;
-      *reinterpret_cast<u32x4 *>(Vs + (2 * dp + 1) * VS + kg * 8) = hi4;
-    }
-  }
-}
-
+// Launch bound (second argument: minimum waves per SIMD): three waves, i.e. at
+// most 168 VGPRs per lane and three 4-wave workgroups per CU.
 template <int D, int NW>
-__global__ void __launch_bounds__(64 * NW)
+__global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
     attn_fwd_bf16(AttnArgs a) {
   constexpr int BM = 32 * NW;
   constexpr int NT = 64 * NW;
-  constexpr int KS = D + 8;          // row stride of K in LDS (elements)
-  constexpr int STAGE = BN * KS + D * VS;
-  constexpr int NCH = D / 16;        // MFMA steps over d for S^T
-  constexpr int NDB = D / 32;        // d blocks of O^T
-  constexpr int KUNITS = BN * D / 8; // 16-byte units of a K tile
-  constexpr int KPT = (KUNITS + NT - 1) / NT;
-  constexpr int VUNITS = (D / 2) * (BN / 8);  // (2 d x 8 keys) units of a V tile
-  constexpr int VPT = (VUNITS + NT - 1) / NT;
+  constexpr int CPR = D / 8;                  // 16-byte chunks per K/V row
+  constexpr int TILE = BN * D * 2;            // bytes of one K or V tile
+  constexpr int STAGE = 2 * TILE;             // K tile then V tile
+  constexpr int CPW = BN * CPR / NT;          // 16-byte copies per thread per tile (K or V)
+  constexpr int LPT = 2 * CPW;                // vector memory ops per wave per tile
+  constexpr int NCH = D / 16;                 // MFMA steps over d for S^T
+  constexpr int NDB = D / 32;                 // d blocks of O^T
+  static_assert(BN * CPR % NT == 0, "tile copies must split evenly over the workgroup");
+  static_assert((kStages - 2) * LPT < 64, "too many copies in flight for vmcnt");
 
-  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * STAGE];
+  __shared__ __attribute__((aligned(16))) char lds[kStages * STAGE];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 31, half = lane >> 5;
 
   const int logical = xcd_remap(blockIdx.x, gridDim.x);
@@ -214,166 +221,189 @@ __global__ void __launch_bounds__(64 * NW)
     }
   }
 
-  // Tile-list reads are uniform: load them through the scalar unit so that
-  // waiting for one never waits for the K/V vector loads in flight.
+  // Tile lists, read through the scalar unit.
   const int nf = sload(a.n_full + qt), np = sload(a.n_part + qt), ntot = nf + np;
   const int32_t *frow = a.full_idx + (int64_t)qt * a.n_ktiles;
   const int32_t *prow = a.part_idx + (int64_t)qt * a.n_ktiles;
   auto tile_of = [&](int i) { return i < nf ? sload(frow + i) : sload(prow + i - nf); };
 
+  // Per-thread source offsets (elements, within a tile) of this thread's K and V
+  // chunk copies: LDS slot p = (j*NW + wave)*64 + lane holds row p / CPR, chunk
+  // (p % CPR) ^ swizzle(row).
+  int koff[CPW], voff[CPW];
+#pragma unroll
+  for (int j = 0; j < CPW; ++j) {
+    const int p = (j * NW + wave) * 64 + lane;
+    const int r = p / CPR, cs = p % CPR;
+    koff[j] = r * D + (cs ^ swz_k<D>(r)) * 8;
+    voff[j] = r * D + (cs ^ swz_v<D>(r)) * 8;
+  }
+  auto issue_tile = [&](int kt, int stage) {
+    const __bf16 *Kt = K + (int64_t)kt * BN * D;
+    const __bf16 *Vt = V + (int64_t)kt * BN * D;
+    char *base = lds + stage * STAGE;
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) {
+      char *dk = base + (j * NW + wave) * 1024;
+      lds_dma16(Kt + koff[j], (lds_void *)dk);
+    }
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) {
+      char *dv = base + TILE + (j * NW + wave) * 1024;
+      lds_dma16(Vt + voff[j], (lds_void *)dv);
+    }
+  };
+
+  // LDS byte offsets (within a stage) of this lane's operand reads.
+  int kaddr[2][NCH];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const int r = kb * 32 + key_of_row(col);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+      kaddr[kb][c] = r * D * 2 + (((half * NCH + c) ^ swz_k<D>(r)) * 16);
+  }
+  // V^T operand for (db, t): two transposing reads e = 0, 1. Lane i of 16-lane
+  // group g points at row 16t + 8(g/2) + 4e + i/4, columns db*32 + 16(g%2) + 4(i%4).
+  // The swizzle of those rows depends only on i/4, so (t, e) only add a constant
+  // row offset (16t + 4e) * D * 2 bytes.
+  const int g16 = lane >> 4, i16 = lane & 15;
+  int vbase[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) {
+    const int r = 8 * (g16 >> 1) + (i16 >> 2);
+    const int cl = db * 32 + 16 * (g16 & 1) + 4 * (i16 & 3);
+    vbase[db] = TILE + r * D * 2 + (((cl >> 3) ^ swz_v<D>(r)) * 16) + (cl & 7) * 2;
+  }
+
   f32x16 oacc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) oacc[db] = f32x16{};
-  float m_run = -__builtin_inff();  // running max, in units of log2
+  float m_run = -__builtin_inff();  // running reference, in units of log2
   float l_run = 0.f;               // this lane's partial sum (its half of the keys)
   const float sl2 = a.scale_log2;
-  const int krow = key_of_row(col);
 
-  // Two register stagings for the K/V tiles in flight (each tile is loaded two
-  // iterations ahead of its use) and two LDS stages. Iteration `it` writes LDS
-  // stage it % 2; the last reader of that stage was iteration it - 2, and every
-  // wave has passed iteration it - 1's barrier since, so one barrier per tile
-  // suffices. The stagings are separate named arrays (not one array indexed by
-  // the iteration) so they stay in registers.
-  u32x4 kA[KPT], kB[KPT];
-  uint32_t vA[VPT][8], vB[VPT][8];
-  if (ntot > 0) load_tile<D, NT>(kA, vA, K, V, tile_of(0), tid);
-  if (ntot > 1) load_tile<D, NT>(kB, vB, K, V, tile_of(1), tid);
+#pragma unroll
+  for (int p = 0; p < kStages - 1; ++p)
+    if (p < ntot) issue_tile(tile_of(p), p);
 
-  auto step = [&](auto &kst, auto &vst, const int it) __attribute__((always_inline)) {
-      const int stage = it & 1;
-      const int kt = tile_of(it);
-      __bf16 *Ks = lds + stage * STAGE;
-      __bf16 *Vs = Ks + BN * KS;
-      store_tile<D, NT>(kst, vst, Ks, Vs, tid);
-      __syncthreads();
-      if (it + 2 < ntot) load_tile<D, NT>(kst, vst, K, V, tile_of(it + 2), tid);
+  for (int it = 0; it < ntot; ++it) {
+    const int stage = it % kStages;
+    // Wait for this wave's copies of tile `it`; copies of the tiles after it
+    // (at most kStages - 2 of them) may stay in flight.
+    wait_tiles_then_barrier<LPT, kStages - 2>(min(ntot - 1 - it, kStages - 2));
+    // The stage refilled next was last read in iteration it - 1, which every
+    // wave has finished (it is behind the barrier above).
+    if (it + kStages - 1 < ntot) issue_tile(tile_of(it + kStages - 1), (it + kStages - 1) % kStages);
 
-      // S^T for the two 32-key blocks: all K operand reads issued first, then the
-      // MFMAs with the two independent accumulators interleaved.
-      bf16x8 kop[2][NCH];
+    const char *st = lds + stage * STAGE;
+    const int kt = tile_of(it);
+
+    // S^T for the two 32-key blocks, independent accumulators interleaved.
+    f32x16 s[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const __bf16 *kr = Ks + (kb * 32 + krow) * KS + half * (D / 2);
-#pragma unroll
-        for (int c = 0; c < NCH; ++c) kop[kb][c] = *reinterpret_cast<const bf16x8 *>(kr + 8 * c);
+        const bf16x8 kop = *reinterpret_cast<const bf16x8 *>(st + kaddr[kb][c]);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[c], s[kb], 0, 0, 0);
       }
-      f32x16 s[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-      for (int c = 0; c < NCH; ++c)
+
+    if (it >= nf) {  // partial tile: element mask
+      const int kbase = kt * BN + 8 * half;  // first key of this lane's runs (multiple of 8)
+      if (one_d) {
+        const int base = kbase - lo;
+        const uint32_t span = (uint32_t)(hi - lo);
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
-          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kb][c], qop[c], s[kb], 0, 0, 0);
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const bool ok = (uint32_t)(base + kb * 32 + 16 * (v >> 3) + (v & 7)) <= span;
+            s[kb][v] = ok ? s[kb][v] : -__builtin_inff();
+          }
+      } else if (row_runs) {
+        const uint32_t rspan = (uint32_t)(rhi - rlo), cspan = (uint32_t)(chi - clo);
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int g = 0; g < 2; ++g) {
+            const int k0 = kbase + kb * 32 + 16 * g;
+            const int r = (int)fdiv((uint32_t)k0, P.wdiv);
+            const int c0 = k0 - r * P.W - clo;
+            const bool row_ok = (uint32_t)(r - rlo) <= rspan;
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+              const bool ok = row_ok & ((uint32_t)(c0 + t) <= cspan);
+              s[kb][8 * g + t] = ok ? s[kb][8 * g + t] : -__builtin_inff();
+            }
+          }
+      } else {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int kpos = kbase + kb * 32 + 16 * (v >> 3) + (v & 7);
+            const int r = (int)fdiv((uint32_t)kpos, P.wdiv), c = kpos - r * P.W;
+            const bool ok = (r >= rlo) & (r <= rhi) & (c >= clo) & (c <= chi);
+            s[kb][v] = ok ? s[kb][v] : -__builtin_inff();
+          }
+      }
+    }
 
-      // V operand reads do not depend on the softmax: issue them now so their
-      // latency hides behind it.
-      bf16x8 vop[NDB][4];
+    // Online softmax in the log2 domain with a lazily moved reference: m_run only
+    // moves when a row's tile max exceeds it by more than kRescaleSlack, so the
+    // O / l rescale is rare; weights stay <= 2^kRescaleSlack and O and l always
+    // share the same reference.
+    float mx = s[0][0];
+#pragma unroll
+    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[0][v]);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[1][v]);
+    mx = xhalf_max(mx);
+    const float mt = mx * sl2;
+    const bool grow = mt > m_run + kRescaleSlack;
+    if (__ballot(grow)) {
+      const float m_new = grow ? mt : m_run;
+      // 1 where unchanged; a row with no allowed key yet has nothing to rescale
+      const float alpha = m_new == -__builtin_inff() ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
+      m_run = m_new;
+    }
+    const float m_use = m_run == -__builtin_inff() ? 0.f : m_run;
+    // Row sums in fp32 from the unrounded weights; P goes to the PV product
+    // rounded to bf16.
+    bf16x8 pop[4];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float pv = __builtin_amdgcn_exp2f(s[kb][v] * sl2 - m_use);
+        l_run += pv;
+        pop[kb * 2 + (v >> 3)][v & 7] = (__bf16)pv;
+      }
+    }
+
+    // O^T += V^T P^T over four 16-key steps, d blocks interleaved; V^T
+    // operands read with the transposing LDS read right before use.
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        const __bf16 *vr = Vs + (db * 32 + col) * VS + 8 * half;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) vop[db][t] = *reinterpret_cast<const bf16x8 *>(vr + 16 * t);
+        const i16x4 lo4 = lds_read_tr16(st + vbase[db] + (16 * t) * D * 2);
+        const i16x4 hi4 = lds_read_tr16(st + vbase[db] + (16 * t + 4) * D * 2);
+        const bf16x8 vop = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[t], oacc[db], 0, 0, 0);
       }
-
-      if (it >= nf) {  // partial tile: element mask
-        const int kbase = kt * BN + 8 * half;  // first key of this lane's runs (multiple of 8)
-        if (one_d) {
-          // allowed iff lo <= key <= hi, as one unsigned compare
-          const int base = kbase - lo;
-          const uint32_t span = (uint32_t)(hi - lo);
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-              const bool ok = (uint32_t)(base + kb * 32 + 16 * (v >> 3) + (v & 7)) <= span;
-              s[kb][v] = ok ? s[kb][v] : -__builtin_inff();
-            }
-        } else if (row_runs) {
-          // W % 8 == 0: each aligned run of 8 keys lies in one grid row, so one
-          // division per run gives the row and the first column
-          const uint32_t rspan = (uint32_t)(rhi - rlo), cspan = (uint32_t)(chi - clo);
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int g = 0; g < 2; ++g) {
-              const int k0 = kbase + kb * 32 + 16 * g;
-              const int r = (int)fdiv((uint32_t)k0, P.wdiv);
-              const int c0 = k0 - r * P.W - clo;
-              const bool row_ok = (uint32_t)(r - rlo) <= rspan;
-#pragma unroll
-              for (int t = 0; t < 8; ++t) {
-                const bool ok = row_ok & ((uint32_t)(c0 + t) <= cspan);
-                s[kb][8 * g + t] = ok ? s[kb][8 * g + t] : -__builtin_inff();
-              }
-            }
-        } else {
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-              const int kpos = kbase + kb * 32 + 16 * (v >> 3) + (v & 7);
-              const int r = (int)fdiv((uint32_t)kpos, P.wdiv), c = kpos - r * P.W;
-              const bool ok = (r >= rlo) & (r <= rhi) & (c >= clo) & (c <= chi);
-              s[kb][v] = ok ? s[kb][v] : -__builtin_inff();
-            }
-        }
-      }
-
-      // Online softmax in the log2 domain with a lazily moved reference: the
-      // exponent reference m_run only moves when a row's tile max exceeds it by
-      // more than kRescaleSlack, so the O / l rescale is rare. Weights stay
-      // <= 2^kRescaleSlack; the result is unchanged because O and l always share
-      // the same reference.
-      float mx = s[0][0];
-#pragma unroll
-      for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[0][v]);
-#pragma unroll
-      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[1][v]);
-      mx = xhalf_max(mx);
-      const float mt = mx * sl2;
-      const bool grow = mt > m_run + kRescaleSlack;
-      if (__ballot(grow)) {
-        const float m_new = grow ? mt : m_run;
-        // 1 where unchanged; a row with no allowed key yet has nothing to rescale
-        const float alpha = m_new == -__builtin_inff() ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-        l_run *= alpha;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
-        m_run = m_new;
-      }
-      const float m_use = m_run == -__builtin_inff() ? 0.f : m_run;
-      // Row sums in fp32 from the unrounded weights (the log-sum-exp needs them to
-      // better than bf16 precision); P goes to the PV product rounded to bf16.
-      bf16x8 pop[4];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float pv = __builtin_amdgcn_exp2f(s[kb][v] * sl2 - m_use);
-          l_run += pv;
-          pop[kb * 2 + (v >> 3)][v & 7] = (__bf16)pv;
-        }
-      }
-
-      // O^T += V^T P^T over four 16-key steps, d blocks interleaved.
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-#pragma unroll
-        for (int db = 0; db < NDB; ++db)
-          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[db][t], pop[t], oacc[db], 0, 0, 0);
-  };
-
-  for (int it = 0; it < ntot; it += 2) {
-    step(kA, vA, it);
-    if (it + 1 < ntot) step(kB, vB, it + 1);
   }
 
   // Epilogue: normalise, stage O through LDS, write rows coalesced.
   const float l_tot = xhalf_sum(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  __syncthreads();  // every wave is done reading K/V from LDS
+  wait_then_barrier<0>();  // no copy in flight; every wave is done reading K/V
   constexpr int OS = D + 8;
-  __bf16 *Os = lds + wave * 32 * OS;
+  __bf16 *Os = reinterpret_cast<__bf16 *>(lds) + wave * 32 * OS;
 #pragma unroll
   for (int db = 0; db < NDB; ++db) {
 #pragma unroll
@@ -386,10 +416,10 @@ __global__ void __launch_bounds__(64 * NW)
   }
   __syncthreads();
   __bf16 *O = static_cast<__bf16 *>(a.out) + slice + (int64_t)(q0 + wave * 32) * D;
-  constexpr int CPR = D / 8;  // 16-byte chunks per row
+  constexpr int OCPR = D / 8;  // 16-byte chunks per row
 #pragma unroll
-  for (int i = lane; i < 32 * CPR; i += 64) {
-    const int r = i / CPR, c = i % CPR;
+  for (int i = lane; i < 32 * OCPR; i += 64) {
+    const int r = i / OCPR, c = i % OCPR;
     *reinterpret_cast<uint4 *>(O + r * D + c * 8) =
         *reinterpret_cast<const uint4 *>(Os + r * OS + c * 8);
   }

@@ -15,10 +15,12 @@ computes, in float64 with NumPy:
              row-major window / slide / neighbourhood baselines (Sec. 3.1-3.3,
              Fig. 3).
   blockmask  tile classification full / partial / empty, by brute force from
-             the element mask, and the per-row tile lists (Sec. 3.1).
+             the element mask, and the per-row tile lists and per-column lists
+             (Sec. 3.1).
   attention  dense element-wise-masked softmax attention and its log-sum-exp
              (Sec. 3.1, Eq. 1 context; the block-sparse kernel computes exactly
-             this result faster).
+             this result faster), and its gradients with respect to q, k, v
+             (the backward pass the paper times beside the forward).
   layer      the Hilbert-neighbourhood-style layer: QKV projection, Hilbert
              slide attention, output projection, computed in row-major order
              (Sec. 3.3, Sec. 4.2 "input processing").

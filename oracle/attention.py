@@ -60,3 +60,73 @@ def attention(q, k, v, pattern, scale: float, rows=None, positions=None,
                 out[b, h, c0:c0 + len(r)] = (p @ v[b, h]) / l_safe[:, None]
                 lse[b, h, c0:c0 + len(r)] = np.where(any_allowed, m + np.log(l_safe), -np.inf)
     return out, lse
+
+
+def attention_backward(q, k, v, dout, pattern, scale: float, rows=None, key_rows=None,
+                       positions=None, chunk: int = 256):
+    """Gradients of ``attention`` for an upstream gradient ``dout``, in float64.
+
+    The paper times the backward pass of every attention it measures (Tables 1-3
+    and 6-11, Backward columns) but writes no formula for it; the gradients are
+    those of the forward definition above. Per (b, h), with P_ij the softmax
+    weights (0 where masked) and out_i = sum_j P_ij v_j:
+
+      dv_j  = sum_i P_ij dout_i
+      dP_ij = <dout_i, v_j>
+      dS_ij = P_ij (dP_ij - sum_j' P_ij' dP_ij')
+      dq_i  = scale * sum_j dS_ij k_j
+      dk_j  = scale * sum_i dS_ij q_i
+
+    A query with no allowed key has out = 0 whatever the inputs, so it adds
+    nothing to any gradient. ``rows`` restricts dq to those query indices and
+    ``key_rows`` restricts dk and dv to those key indices; only the queries the
+    requested outputs depend on are evaluated (each over all N keys).
+    ``positions`` is as in ``attention``. Returns (dq, dk, dv).
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    dout = np.asarray(dout, dtype=np.float64)
+    B, Hh, N, d = q.shape
+    if k.shape != (B, Hh, N, d) or v.shape[:3] != (B, Hh, N) or dout.shape != v.shape:
+        raise ValueError("q, k, v, dout shapes disagree")
+    pos = np.arange(N, dtype=np.int64) if positions is None else np.asarray(positions, dtype=np.int64)
+    rows = np.arange(N, dtype=np.int64) if rows is None else np.asarray(rows, dtype=np.int64)
+    keys = np.arange(N, dtype=np.int64) if key_rows is None else np.asarray(key_rows, dtype=np.int64)
+    # queries whose softmax rows the requested outputs need
+    need = np.zeros(N, dtype=bool)
+    need[rows] = True
+    if key_rows is None:
+        need[:] = True
+    else:
+        for c0 in range(0, keys.shape[0], chunk):
+            kk = keys[c0:c0 + chunk]
+            need |= masks.allowed(pattern, pos[:, None], pos[kk][None, :]).any(axis=1)
+    qidx = np.nonzero(need)[0]
+    slot_of_row = {int(r): n for n, r in enumerate(rows)}
+    dv_ = v.shape[3]
+    dq = np.zeros((B, Hh, rows.shape[0], d), dtype=np.float64)
+    dk = np.zeros((B, Hh, keys.shape[0], d), dtype=np.float64)
+    dv = np.zeros((B, Hh, keys.shape[0], dv_), dtype=np.float64)
+    for c0 in range(0, qidx.shape[0], chunk):
+        r = qidx[c0:c0 + chunk]
+        allow = masks.allowed(pattern, pos[r][:, None], pos[None, :])     # [R, N]
+        any_allowed = allow.any(axis=1)
+        dst = [slot_of_row.get(int(i), -1) for i in r]
+        sel = np.array([t for t, s in enumerate(dst) if s >= 0], dtype=np.int64)
+        out_slots = np.array([dst[t] for t in sel], dtype=np.int64)
+        for b in range(B):
+            for h in range(Hh):
+                s = scale * (q[b, h, r] @ k[b, h].T)
+                s = np.where(allow, s, -np.inf)
+                m = np.where(any_allowed, s.max(axis=1), 0.0)
+                e = np.exp(s - m[:, None])
+                l = np.where(any_allowed, e.sum(axis=1), 1.0)
+                p = e / l[:, None]                                         # softmax, 0 if masked
+                dp = dout[b, h, r] @ v[b, h].T                             # [R, N]
+                ds = p * (dp - (p * dp).sum(axis=1, keepdims=True))
+                if sel.size:
+                    dq[b, h, out_slots] = scale * (ds[sel] @ k[b, h])
+                dk[b, h] += scale * (ds[:, keys].T @ q[b, h, r])
+                dv[b, h] += p[:, keys].T @ dout[b, h, r]
+    return dq, dk, dv

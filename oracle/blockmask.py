@@ -93,3 +93,10 @@ def build(pattern, tile_m: int, tile_n: int, qtiles=None) -> BlockMask:
 
 def empty_fraction(pattern, tile_m: int, tile_n: int) -> float:
     return float((classify(pattern, tile_m, tile_n) == EMPTY).mean())
+
+
+def column_lists(cls: np.ndarray) -> BlockMask:
+    """Per key-tile column: the query tiles whose tile with it is full / partial,
+    ascending, -1 padded (the same lists read down the columns of ``cls``; the
+    backward pass walks them to accumulate key and value gradients)."""
+    return lists_from_classes(np.ascontiguousarray(cls.T))

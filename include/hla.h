@@ -96,12 +96,22 @@ typedef struct {
  * n_qtiles * n_ktiles int32 (hla_block_mask_dims gives the counts).
  * totals, if not NULL, is a device int32[2] that receives
  * {total full tiles, total partial tiles}.
+ *
+ * Optional transposed lists, read by the backward pass (hla_attn_bwd) to
+ * accumulate key and value gradients per key tile. For key-tile column k:
+ *   n_full_t[k]            number of full tiles in the column
+ *   full_idx_t[k*n_qtiles + t], t < n_full_t[k]: query-tile indices, ascending
+ *   n_part_t[k], part_idx_t  the same for partial tiles
+ * n_full_t, n_part_t hold n_ktiles int32; full_idx_t, part_idx_t hold
+ * n_ktiles * n_qtiles int32; unused entries are -1. Set all four or none
+ * (NULL: not built).
  */
 typedef struct {
   int32_t N, tile_m, tile_n, n_qtiles, n_ktiles;
   hla_pattern_desc pat;
   int32_t *n_full, *full_idx, *n_part, *part_idx;
   int32_t *totals;
+  int32_t *n_full_t, *full_idx_t, *n_part_t, *part_idx_t;
 } hla_block_mask;
 
 /*
@@ -150,9 +160,10 @@ hla_status hla_block_mask_dims(const hla_pattern_desc *pat, int32_t tile_m,
  * Classify every (query tile, key tile) pair as full, partial or empty and write
  * the per-row ascending lists (Sec. 3.1). mask->pat, tile_m, tile_n select the
  * pattern and tiling; the call fills mask->N, n_qtiles, n_ktiles on the host
- * and the four device arrays (and totals) on the stream. It does not
- * synchronise. The classification is exact: for every pattern the class of a
- * tile equals the one obtained by counting its allowed elements.
+ * and the four device arrays (and totals) on the stream, plus the transposed
+ * lists when their four pointers are set. It does not synchronise. The
+ * classification is exact: for every pattern the class of a tile equals the
+ * one obtained by counting its allowed elements.
  */
 hla_status hla_build_block_mask(hla_block_mask *mask, hla_stream_t stream);
 
@@ -174,6 +185,38 @@ hla_status hla_attn_fwd(const void *q, const void *k, const void *v,
                         const hla_block_mask *mask, void *out, float *lse,
                         int64_t B, int64_t heads, int64_t N, int64_t d,
                         hla_dtype dtype, float scale, hla_stream_t stream);
+
+/*
+ * Block-sparse attention backward: the gradients of hla_attn_fwd's out with
+ * respect to q, k and v for an upstream gradient dout, over the same tiles as
+ * the forward (empty tiles skipped, partial tiles masked; the paper times this
+ * pass beside the forward for every pattern, Tables 1-3). With the forward's lse:
+ *   P[i,j]  = exp(scale * <q_i, k_j> - lse_i)  if allowed(i, j), else 0
+ *   delta_i = <dout_i, out_i>                  (= sum_j P[i,j] <dout_i, v_j>)
+ *   dS[i,j] = P[i,j] * (<dout_i, v_j> - delta_i)
+ *   dq_i = scale * sum_j dS[i,j] k_j,   dk_j = scale * sum_i dS[i,j] q_i,
+ *   dv_j = sum_i P[i,j] dout_i.
+ * q, k, v, out, dout: [B, heads, N, d] of dtype, with out and lse exactly as
+ * returned by hla_attn_fwd for these q, k, v, mask and scale.
+ * lse: float32 [B, heads, N] (required).
+ * stats: caller-owned float32 [B, heads, N, 2] workspace, overwritten with
+ * (lse_i * log2(e), delta_i) per row (+inf in place of the first where
+ * lse_i = -inf).
+ * dq, dk, dv: [B, heads, N, d] of dtype; they may not overlap each other or any
+ * input. A query with no allowed key contributes nothing.
+ * The mask must carry the transposed lists (see hla_block_mask).
+ * Deterministic: every output element is written by exactly one thread, with a
+ * fixed summation order (no atomics).
+ * bf16: products on bf16 matrix cores with P and dS rounded to bf16 as
+ * operands, fp32 accumulation, gradients rounded to bf16. f32: fp32 throughout.
+ * Supported: d in {32, 64}; tile_m in {64, 128}; tile_n == 64;
+ * otherwise UNSUPPORTED.
+ */
+hla_status hla_attn_bwd(const void *q, const void *k, const void *v, const void *out,
+                        const void *dout, const float *lse, const hla_block_mask *mask,
+                        void *dq, void *dk, void *dv, float *stats, int64_t B,
+                        int64_t heads, int64_t N, int64_t d, hla_dtype dtype, float scale,
+                        hla_stream_t stream);
 
 /*
  * QKV projection with head split (Sec. 4.2, input processing: the Linear layer

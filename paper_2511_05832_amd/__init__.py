@@ -11,6 +11,9 @@ fallback path.
     out, lse = attn_fwd(qh, kh, vh, mask, scale)
     o = scatter(out, order)                     # back to row-major
 
+    mask = build_block_mask(pattern, 128, 64, columns=True)   # + per-column lists
+    dq, dk, dv = attn_bwd(qh, kh, vh, out, dout, lse, mask, scale)
+
 Patterns are given as any object with attributes kind, H, W, p0, p1 (kind is one
 of PATTERN_IDS), or as a tuple (kind, H, W, p0, p1).
 """
@@ -24,7 +27,7 @@ from typing import Optional, Tuple
 import torch
 
 __all__ = ["HLAError", "lib", "hilbert_perm", "gather", "scatter", "block_mask_dims",
-           "build_block_mask", "BlockMask", "attn_fwd", "qkv_proj", "out_proj",
+           "build_block_mask", "BlockMask", "attn_fwd", "attn_bwd", "qkv_proj", "out_proj",
            "PATTERN_IDS", "LIB_PATH", "EXPORTED"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhla.so")
@@ -43,7 +46,7 @@ HLA_OK, HLA_ERR_INVALID_ARG, HLA_ERR_UNSUPPORTED, HLA_ERR_HIP = 0, 1, 2, 3
 HLA_F32, HLA_BF16 = 0, 1
 
 EXPORTED = ("hla_hilbert_perm", "hla_gather", "hla_scatter", "hla_block_mask_dims",
-            "hla_build_block_mask", "hla_attn_fwd", "hla_qkv_proj", "hla_out_proj",
+            "hla_build_block_mask", "hla_attn_fwd", "hla_attn_bwd", "hla_qkv_proj", "hla_out_proj",
             "hla_last_error", "hla_version")
 
 
@@ -67,7 +70,9 @@ class BlockMaskStruct(ctypes.Structure):
                 ("pat", PatternDesc),
                 ("n_full", ctypes.c_void_p), ("full_idx", ctypes.c_void_p),
                 ("n_part", ctypes.c_void_p), ("part_idx", ctypes.c_void_p),
-                ("totals", ctypes.c_void_p)]
+                ("totals", ctypes.c_void_p),
+                ("n_full_t", ctypes.c_void_p), ("full_idx_t", ctypes.c_void_p),
+                ("n_part_t", ctypes.c_void_p), ("part_idx_t", ctypes.c_void_p)]
 
 
 _lib = None
@@ -94,6 +99,8 @@ def lib() -> ctypes.CDLL:
             "hla_build_block_mask": [ctypes.POINTER(BlockMaskStruct), vp],
             "hla_attn_fwd": [vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp,
                              i64, i64, i64, i64, ctypes.c_int, f32, vp],
+            "hla_attn_bwd": [vp, vp, vp, vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp, vp,
+                             vp, i64, i64, i64, i64, ctypes.c_int, f32, vp],
             "hla_qkv_proj": [vp, vp, vp, vp, vp, i64, i64, i64, i64, vp],
             "hla_out_proj": [vp, vp, vp, i64, i64, i64, i64, i64, vp],
         }
@@ -211,9 +218,12 @@ def block_mask_dims(pattern, tile_m: int, tile_n: int) -> Tuple[int, int]:
 
 
 class BlockMask:
-    """Device tile lists of one (pattern, tile) pair; owns its buffers."""
+    """Device tile lists of one (pattern, tile) pair; owns its buffers.
 
-    def __init__(self, pattern, tile_m: int, tile_n: int, device="cuda"):
+    ``columns=True`` also allocates and builds the per-key-tile-column lists
+    that the backward pass walks."""
+
+    def __init__(self, pattern, tile_m: int, tile_n: int, device="cuda", columns: bool = False):
         nq, nk = block_mask_dims(pattern, tile_m, tile_n)
         self.pattern = pattern
         self.tile_m, self.tile_n, self.n_qtiles, self.n_ktiles = tile_m, tile_n, nq, nk
@@ -230,6 +240,16 @@ class BlockMask:
         self.struct.n_part = self.n_part.data_ptr()
         self.struct.part_idx = self.part_idx.data_ptr()
         self.struct.totals = self.totals.data_ptr()
+        self.columns = columns
+        if columns:
+            self.n_full_t = torch.empty(nk, dtype=torch.int32, device=device)
+            self.n_part_t = torch.empty(nk, dtype=torch.int32, device=device)
+            self.full_idx_t = torch.empty((nk, nq), dtype=torch.int32, device=device)
+            self.part_idx_t = torch.empty((nk, nq), dtype=torch.int32, device=device)
+            self.struct.n_full_t = self.n_full_t.data_ptr()
+            self.struct.full_idx_t = self.full_idx_t.data_ptr()
+            self.struct.n_part_t = self.n_part_t.data_ptr()
+            self.struct.part_idx_t = self.part_idx_t.data_ptr()
 
     def build(self):
         _check(lib().hla_build_block_mask(ctypes.byref(self.struct), _stream(self.n_full)))
@@ -244,9 +264,11 @@ class BlockMask:
         return int(t[0]), int(t[1])
 
 
-def build_block_mask(pattern, tile_m: int, tile_n: int, device="cuda") -> BlockMask:
-    """Classify all tiles and build the per-row lists (hla_build_block_mask)."""
-    return BlockMask(pattern, tile_m, tile_n, device).build()
+def build_block_mask(pattern, tile_m: int, tile_n: int, device="cuda",
+                     columns: bool = False) -> BlockMask:
+    """Classify all tiles and build the per-row lists (hla_build_block_mask);
+    ``columns=True`` adds the per-column lists for the backward pass."""
+    return BlockMask(pattern, tile_m, tile_n, device, columns).build()
 
 
 def attn_fwd(q, k, v, mask: BlockMask, scale: Optional[float] = None,
@@ -273,6 +295,36 @@ def attn_fwd(q, k, v, mask: BlockMask, scale: Optional[float] = None,
     _check(lib().hla_attn_fwd(_ptr(q), _ptr(k), _ptr(v), ctypes.byref(mask.struct), _ptr(out),
                               _ptr(lse), B, Hh, N, d, _dtype_code(q), float(scale), _stream(q)))
     return out, lse
+
+
+def attn_bwd(q, k, v, out, dout, lse, mask: BlockMask, scale: Optional[float] = None,
+             dq: Optional[torch.Tensor] = None, dk: Optional[torch.Tensor] = None,
+             dv: Optional[torch.Tensor] = None, stats: Optional[torch.Tensor] = None):
+    """Block-sparse attention backward (hla_attn_bwd). ``out`` and ``lse`` are the
+    forward's results for these q, k, v, mask and scale. Returns (dq, dk, dv).
+    ``stats`` is the float32 [B, heads, N, 2] workspace (allocated if None)."""
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (out, "out"), (dout, "dout"), (lse, "lse")):
+        _require(t, n)
+    if q.dim() != 4 or any(t.shape != q.shape for t in (k, v, out, dout)):
+        raise HLAError(HLA_ERR_INVALID_ARG, "q, k, v, out, dout must all be [B, heads, N, d] of one shape")
+    if any(t.dtype != q.dtype for t in (k, v, out, dout)):
+        raise HLAError(HLA_ERR_INVALID_ARG, "q, k, v, out, dout must share a dtype")
+    B, Hh, N, d = q.shape
+    if lse.dtype != torch.float32 or tuple(lse.shape) != (B, Hh, N):
+        raise HLAError(HLA_ERR_INVALID_ARG, "lse must be float32 [B, heads, N]")
+    if scale is None:
+        scale = 1.0 / float(d) ** 0.5
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    if stats is None:
+        stats = torch.empty((B, Hh, N, 2), dtype=torch.float32, device=q.device)
+    for t, n in ((dq, "dq"), (dk, "dk"), (dv, "dv"), (stats, "stats")):
+        _require(t, n)
+    _check(lib().hla_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse),
+                              ctypes.byref(mask.struct), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(stats),
+                              B, Hh, N, d, _dtype_code(q), float(scale), _stream(q)))
+    return dq, dk, dv
 
 
 def qkv_proj(x: torch.Tensor, w_qkv: torch.Tensor, heads: int, outs=None):

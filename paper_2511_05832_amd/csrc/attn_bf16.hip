@@ -21,7 +21,7 @@
 //
 // Register-resident P. The accumulator of a 32x32 MFMA holds, in lane
 // (col = l%32, half = l/32) and slot v, row 8*(v/4) + 4*half + v%4. The K rows
-// fed to S^T are permuted (key_of_row) so that accumulator slot v of lane half
+// fed to S^T are permuted (row_perm) so that accumulator slot v of lane half
 // `half` is key 16*(v/8) + 8*half + v%8 of the block: eight consecutive keys per
 // run, which is exactly the B-operand layout of the PV MFMA over 16 keys. So P
 // goes from fp32 accumulators to bf16 operands in place, with no LDS trip.
@@ -54,17 +54,10 @@
 // tiles: neighbouring tiles share key/value tiles (a window is two query tiles;
 // a band overlaps its neighbour almost entirely), and the reuse stays in one
 // XCD's L2.
-#include "hla_internal.h"
+#include "attn_common.h"
 
 namespace hla {
 namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int BN = 64;
 constexpr float kRescaleSlack = 8.f;  // log2 units the softmax reference may lag the max
@@ -78,12 +71,6 @@ constexpr int kStages = 3;
 __device__ __forceinline__ float xhalf_max(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
 __device__ __forceinline__ float xhalf_sum(float x) { return x + __shfl_xor(x, 32); }
 
-__device__ __forceinline__ int key_of_row(int i) {
-  // accumulator row i = 8a + 4g + b  ->  key 16(a/2) + 8g + 4(a%2) + b
-  const int a = i >> 3, g = (i >> 2) & 1, b = i & 3;
-  return 16 * (a >> 1) + 8 * g + 4 * (a & 1) + b;
-}
-
 // Per-row XOR swizzle of the 16-byte chunks of a K / V tile row in LDS.
 template <int D>
 __device__ __forceinline__ int swz_k(int r) {
@@ -94,59 +81,6 @@ template <int D>
 __device__ __forceinline__ int swz_v(int r) {
   if (D == 64) return 2 * (r & 3);
   return 2 * ((r >> 1) & 1);
-}
-
-__device__ __forceinline__ int xcd_remap(int bid, int total) {
-  const int per = total >> 3, rem = total & 7;
-  const int xcd = bid & 7, slot = bid >> 3;
-  return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
-}
-
-__device__ __forceinline__ int clampi(int x, int lo, int hi) { return min(max(x, lo), hi); }
-
-// Scalar (SMEM) load of a wave-uniform int through the constant address space.
-__device__ __forceinline__ int sload(const int32_t *p) {
-  return *(const __attribute__((address_space(4))) int32_t *)p;
-}
-
-// gfx950 LDS DMA (16 bytes per lane; lane l lands at dst + 16 l) and the
-// transposing 64-bit LDS read. Only the device pass may see these builtins:
-// the host pass of the HIP compiler rejects them silently and then emits no
-// launch stub for the kernel that calls them.
-__device__ __forceinline__ void lds_dma16(const void *src, lds_void *dst) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
-#endif
-}
-__device__ __forceinline__ i16x4 lds_read_tr16(const char *p) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p);
-#else
-  return i16x4{};
-#endif
-}
-
-// Wait until this wave's LDS reads are done and at most N of its vector memory
-// operations (here: K/V tile copies) are in flight, then barrier the workgroup.
-// One asm statement with a memory clobber, so the compiler moves no memory
-// access across it (a fence would instead wait for every copy in flight).
-template <int N>
-__device__ __forceinline__ void wait_then_barrier() {
-  static_assert(N >= 0 && N < 64, "vmcnt out of range");
-  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
-}
-// Dispatch on the number of tiles still allowed in flight (0 .. MAXA).
-template <int LPT, int MAXA>
-__device__ __forceinline__ void wait_tiles_then_barrier(int after) {
-  if constexpr (MAXA > 0) {
-    if (after >= MAXA) {
-      wait_then_barrier<MAXA * LPT>();
-      return;
-    }
-    wait_tiles_then_barrier<LPT, MAXA - 1>(after);
-  } else {
-    wait_then_barrier<0>();
-  }
 }
 
 // Launch bound (second argument: minimum waves per SIMD): three waves, i.e. at
@@ -190,36 +124,7 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
 
   // Allowed-key region of this query (used on partial tiles only).
   const PatternArgs &P = a.pat;
-  const bool one_d = P.kind == HLA_HILBERT_WINDOW || P.kind == HLA_HILBERT_SLIDE ||
-                     P.kind == HLA_HILBERT_NEIGHBORHOOD || P.kind == HLA_HILBERT_SHIFTED_WINDOW;
-  const bool row_runs = (P.W & 7) == 0;
-  int lo = 0, hi = 0, rlo = 0, rhi = 0, clo = 0, chi = 0;
-  if (P.kind == HLA_HILBERT_WINDOW) {
-    lo = (qpos / P.p0) * P.p0;
-    hi = lo + P.p0 - 1;
-  } else if (P.kind == HLA_HILBERT_SLIDE) {
-    lo = qpos - P.p0;
-    hi = qpos + P.p0;
-  } else if (P.kind == HLA_HILBERT_NEIGHBORHOOD) {
-    lo = clampi(qpos - P.p0 / 2, 0, P.N - P.p0);
-    hi = lo + P.p0 - 1;
-  } else if (P.kind == HLA_HILBERT_SHIFTED_WINDOW) {
-    const int g = (qpos + P.p0 - P.p1) / P.p0;
-    lo = g * P.p0 - P.p0 + P.p1;
-    hi = lo + P.p0 - 1;
-  } else {
-    const int r = (int)fdiv((uint32_t)qpos, P.wdiv), c = qpos - r * P.W;
-    if (P.kind == HLA_ROWMAJOR_WINDOW) {
-      rlo = (r / P.p0) * P.p0; rhi = rlo + P.p0 - 1;
-      clo = (c / P.p1) * P.p1; chi = clo + P.p1 - 1;
-    } else if (P.kind == HLA_ROWMAJOR_SLIDE) {
-      rlo = r - P.p0; rhi = r + P.p0;
-      clo = c - P.p1; chi = c + P.p1;
-    } else {
-      rlo = clampi(r - P.p0 / 2, 0, P.H - P.p0); rhi = rlo + P.p0 - 1;
-      clo = clampi(c - P.p1 / 2, 0, P.W - P.p1); chi = clo + P.p1 - 1;
-    }
-  }
+  const Region R = region_of<true>(P, qpos);
 
   // Tile lists, read through the scalar unit.
   const int nf = sload(a.n_full + qt), np = sload(a.n_part + qt), ntot = nf + np;
@@ -258,7 +163,7 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
   int kaddr[2][NCH];
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
-    const int r = kb * 32 + key_of_row(col);
+    const int r = kb * 32 + row_perm(col);
 #pragma unroll
     for (int c = 0; c < NCH; ++c)
       kaddr[kb][c] = r * D * 2 + (((half * NCH + c) ^ swz_k<D>(r)) * 16);
@@ -310,44 +215,7 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
       }
 
     if (it >= nf) {  // partial tile: element mask
-      const int kbase = kt * BN + 8 * half;  // first key of this lane's runs (multiple of 8)
-      if (one_d) {
-        const int base = kbase - lo;
-        const uint32_t span = (uint32_t)(hi - lo);
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const bool ok = (uint32_t)(base + kb * 32 + 16 * (v >> 3) + (v & 7)) <= span;
-            s[kb][v] = ok ? s[kb][v] : -__builtin_inff();
-          }
-      } else if (row_runs) {
-        const uint32_t rspan = (uint32_t)(rhi - rlo), cspan = (uint32_t)(chi - clo);
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int g = 0; g < 2; ++g) {
-            const int k0 = kbase + kb * 32 + 16 * g;
-            const int r = (int)fdiv((uint32_t)k0, P.wdiv);
-            const int c0 = k0 - r * P.W - clo;
-            const bool row_ok = (uint32_t)(r - rlo) <= rspan;
-#pragma unroll
-            for (int t = 0; t < 8; ++t) {
-              const bool ok = row_ok & ((uint32_t)(c0 + t) <= cspan);
-              s[kb][8 * g + t] = ok ? s[kb][8 * g + t] : -__builtin_inff();
-            }
-          }
-      } else {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int kpos = kbase + kb * 32 + 16 * (v >> 3) + (v & 7);
-            const int r = (int)fdiv((uint32_t)kpos, P.wdiv), c = kpos - r * P.W;
-            const bool ok = (r >= rlo) & (r <= rhi) & (c >= clo) & (c <= chi);
-            s[kb][v] = ok ? s[kb][v] : -__builtin_inff();
-          }
-      }
+      mask_blocks<2>(s, R, P, kt * BN + 8 * half);
     }
 
     // Online softmax in the log2 domain with a lazily moved reference: m_run only
@@ -391,9 +259,7 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
     for (int t = 0; t < 4; ++t)
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        const i16x4 lo4 = lds_read_tr16(st + vbase[db] + (16 * t) * D * 2);
-        const i16x4 hi4 = lds_read_tr16(st + vbase[db] + (16 * t + 4) * D * 2);
-        const bf16x8 vop = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+        const bf16x8 vop = lds_read_tr16x2(st + vbase[db] + (16 * t) * D * 2, D * 2);
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[t], oacc[db], 0, 0, 0);
       }
   }

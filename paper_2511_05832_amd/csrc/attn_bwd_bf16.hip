@@ -1,0 +1,461 @@
+// Block-sparse flash-attention backward, bf16 in / bf16 out, fp32 accumulation,
+// on gfx950 bf16 matrix cores (v_mfma_f32_32x32x16_bf16).
+//
+// What it computes: the gradients of the forward pass (the paper times the
+// backward of every attention it measures, Tables 1-3 and 6-11) over the same
+// tile structure - empty tiles skipped, full tiles unmasked, partial tiles with
+// the element mask (Sec. 3.1; Eq. 1's per-block cost applies to both passes).
+// With the forward's lse and delta_i = <dout_i, out_i> (row statistics kernel):
+//   P_ij  = exp(scale <q_i, k_j> - lse_i)   (0 where masked)
+//   dS_ij = P_ij (<dout_i, v_j> - delta_i)
+//   dq_i  = scale sum_j dS_ij k_j       dk_j = scale sum_i dS_ij q_i
+//   dv_j  = sum_i P_ij dout_i
+// Two kernels and no atomics, so every result is deterministic:
+//   dq kernel    one workgroup per (b*h, query tile), walking that tile row's list
+//                of key tiles (as the forward does);
+//   dkdv kernel  one workgroup per (b*h, key tile), walking that key tile
+//                column's list of query tiles (the transposed lists).
+// P and dP are recomputed in both; the recomputation costs two of the seven
+// products but removes every cross-workgroup reduction.
+//
+// Operand placement. In each kernel the operands that stay fixed over the walk
+// (q and dout rows in dq; k and v rows in dkdv) live in registers as B operands,
+// and the walked tiles are staged in LDS by global_load_lds_dwordx4 (no register
+// round trip), in a ring kept ahead of the compute. A tile is read twice from
+// LDS: by rows (A operand of S and dP) and transposed (A operand of the products
+// that contract over the walked index, via ds_read_b64_tr_b16). One XOR swizzle
+// of the 16-byte chunks serves both reads without bank conflicts:
+//   d = 64: chunk ^= 2*(r%4) + (r/8)%2;   d = 32: chunk ^= 2*((r/2)%2) + (r/8)%2.
+// The row reads touch rows {0..3, 8..11} (+16k) eight lanes at a time, which the
+// low bit and (for d = 32) the row pairing make distinct; the transposing reads
+// touch four consecutive rows times two adjacent chunks, which the upper two
+// bits make distinct.
+//
+// Register-resident weights. The A rows of S (dq: key rows; dkdv: query rows) are
+// fed permuted by row_perm, so the S and dP accumulators come out in the B-operand
+// layout of the next product, and P / dS go to bf16 operands in place.
+#include "attn_common.h"
+
+namespace hla {
+namespace {
+
+constexpr int BN = 64;  // keys per key tile
+
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+  if (D == 64) return (2 * (r & 3)) | ((r >> 3) & 1);
+  return (2 * ((r >> 1) & 1)) | ((r >> 3) & 1);
+}
+
+// A-operand byte offsets of a transposing read, relative to the first row of a
+// 16-row step: lane i of 16-lane group g reads row 8(g/2) + i/4 (+4 for the
+// second read), columns db*32 + 16(g%2) + 4(i%4). Row offsets that are multiples
+// of 16 leave the swizzle unchanged, so a step adds a constant.
+template <int D>
+__device__ __forceinline__ int tr_base(int lane, int db) {
+  const int g16 = lane >> 4, i16 = lane & 15;
+  const int r = 8 * (g16 >> 1) + (i16 >> 2);
+  const int cl = db * 32 + 16 * (g16 & 1) + 4 * (i16 & 3);
+  return r * D * 2 + (((cl >> 3) ^ swz<D>(r)) * 16) + (cl & 7) * 2;
+}
+
+// Store a [d x 32] fp32 accumulator set (NDB blocks of 32x32, rows = d) scaled
+// by `mul` as 32 bf16 rows of d, through this wave's LDS staging area `Os`
+// (32 x (D + 8) bf16), to `dst` (row stride D). The caller barriers between
+// the staging writes and the reads.
+template <int D>
+__device__ __forceinline__ void stage_rows(const f32x16 *acc, float mul, __bf16 *Os, int col,
+                                           int half) {
+  constexpr int OS = D + 8;
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      bf16x4 o4;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) o4[b] = (__bf16)(acc[db][4 * g + b] * mul);
+      *reinterpret_cast<bf16x4 *>(Os + col * OS + db * 32 + 8 * g + 4 * half) = o4;
+    }
+}
+template <int D>
+__device__ __forceinline__ void write_rows(const __bf16 *Os, __bf16 *dst, int lane) {
+  constexpr int OS = D + 8, CPR = D / 8;
+#pragma unroll
+  for (int i = lane; i < 32 * CPR; i += 64) {
+    const int r = i / CPR, c = i % CPR;
+    *reinterpret_cast<uint4 *>(dst + r * D + c * 8) =
+        *reinterpret_cast<const uint4 *>(Os + r * OS + c * 8);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dq: one workgroup per (b*h, query tile of BM = 32*NW rows); wave w owns 32
+// queries. Per key tile, per wave:
+//   S^T  = K Q^T      A = K rows (LDS), B = the wave's q (registers)
+//   dP^T = V dout^T   A = V rows (LDS), B = the wave's dout (registers)
+//   dS^T = P^T (dP^T - delta), P^T = exp2(S^T scale log2e - lse log2e)
+//   dq^T += K^T dS^T  A = K^T (transposing LDS reads), B = dS^T (registers)
+constexpr int kStagesDq = 3;
+
+template <int D, int NW>
+__global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
+  constexpr int BM = 32 * NW;
+  constexpr int NT = 64 * NW;
+  constexpr int CPR = D / 8;
+  constexpr int TILE = BN * D * 2;
+  constexpr int STAGE = 2 * TILE;  // K tile then V tile
+  constexpr int CPW = BN * CPR / NT;
+  constexpr int LPT = 2 * CPW;
+  constexpr int NCH = D / 16;
+  constexpr int NDB = D / 32;
+  static_assert(BN * CPR % NT == 0, "tile copies must split evenly over the workgroup");
+  static_assert((kStagesDq - 2) * LPT < 64, "too many copies in flight for vmcnt");
+
+  __shared__ __attribute__((aligned(16))) char lds[kStagesDq * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 31, half = lane >> 5;
+
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int bh = logical / a.n_qtiles;
+  const int qt = logical - bh * a.n_qtiles;
+  const int q0 = qt * BM;
+  const int64_t slice = (int64_t)bh * a.N * D;
+  const __bf16 *Q = static_cast<const __bf16 *>(a.q) + slice;
+  const __bf16 *K = static_cast<const __bf16 *>(a.k) + slice;
+  const __bf16 *V = static_cast<const __bf16 *>(a.v) + slice;
+  const __bf16 *G = static_cast<const __bf16 *>(a.dout) + slice;
+
+  const int qpos = q0 + wave * 32 + col;
+  bf16x8 qop[NCH], gop[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    qop[c] = *reinterpret_cast<const bf16x8 *>(Q + (int64_t)qpos * D + half * (D / 2) + 8 * c);
+    gop[c] = *reinterpret_cast<const bf16x8 *>(G + (int64_t)qpos * D + half * (D / 2) + 8 * c);
+  }
+  const float2 rs = *reinterpret_cast<const float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qpos));
+  const float lse2 = rs.x, delta = rs.y;
+
+  const PatternArgs &P = a.pat;
+  const Region R = region_of<true>(P, qpos);
+
+  const int nf = sload(a.n_full + qt), np = sload(a.n_part + qt), ntot = nf + np;
+  const int32_t *frow = a.full_idx + (int64_t)qt * a.n_ktiles;
+  const int32_t *prow = a.part_idx + (int64_t)qt * a.n_ktiles;
+  auto tile_of = [&](int i) { return i < nf ? sload(frow + i) : sload(prow + i - nf); };
+
+  int off[CPW];
+#pragma unroll
+  for (int j = 0; j < CPW; ++j) {
+    const int p = (j * NW + wave) * 64 + lane;
+    const int r = p / CPR, cs = p % CPR;
+    off[j] = r * D + (cs ^ swz<D>(r)) * 8;
+  }
+  auto issue_tile = [&](int kt, int stage) {
+    const __bf16 *Kt = K + (int64_t)kt * BN * D;
+    const __bf16 *Vt = V + (int64_t)kt * BN * D;
+    char *base = lds + stage * STAGE;
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) lds_dma16(Kt + off[j], (lds_void *)(base + (j * NW + wave) * 1024));
+#pragma unroll
+    for (int j = 0; j < CPW; ++j)
+      lds_dma16(Vt + off[j], (lds_void *)(base + TILE + (j * NW + wave) * 1024));
+  };
+
+  int raddr[2][NCH];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const int r = kb * 32 + row_perm(col);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) raddr[kb][c] = r * D * 2 + (((half * NCH + c) ^ swz<D>(r)) * 16);
+  }
+  int tbase[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) tbase[db] = tr_base<D>(lane, db);
+
+  f32x16 acc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
+  const float sl2 = a.scale_log2;
+
+#pragma unroll
+  for (int p = 0; p < kStagesDq - 1; ++p)
+    if (p < ntot) issue_tile(tile_of(p), p);
+
+  for (int it = 0; it < ntot; ++it) {
+    const int stage = it % kStagesDq;
+    wait_tiles_then_barrier<LPT, kStagesDq - 2>(min(ntot - 1 - it, kStagesDq - 2));
+    if (it + kStagesDq - 1 < ntot)
+      issue_tile(tile_of(it + kStagesDq - 1), (it + kStagesDq - 1) % kStagesDq);
+    const char *st = lds + stage * STAGE;
+    const int kt = tile_of(it);
+
+    f32x16 s[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const bf16x8 kop = *reinterpret_cast<const bf16x8 *>(st + raddr[kb][c]);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[c], s[kb], 0, 0, 0);
+        const bf16x8 vop = *reinterpret_cast<const bf16x8 *>(st + TILE + raddr[kb][c]);
+        dp[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, gop[c], dp[kb], 0, 0, 0);
+      }
+    if (it >= nf) mask_blocks<2>(s, R, P, kt * BN + 8 * half);
+
+    bf16x8 dsop[4];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float p = __builtin_amdgcn_exp2f(s[kb][v] * sl2 - lse2);
+        dsop[kb * 2 + (v >> 3)][v & 7] = (__bf16)(p * (dp[kb][v] - delta));
+      }
+
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const bf16x8 kto = lds_read_tr16x2(st + tbase[db] + (16 * t) * D * 2, D * 2);
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kto, dsop[t], acc[db], 0, 0, 0);
+      }
+  }
+
+  wait_then_barrier<0>();
+  __bf16 *Os = reinterpret_cast<__bf16 *>(lds) + wave * 32 * (D + 8);
+  stage_rows<D>(acc, a.scale, Os, col, half);
+  __syncthreads();
+  write_rows<D>(Os, static_cast<__bf16 *>(a.dq) + slice + (int64_t)(q0 + wave * 32) * D, lane);
+}
+
+// ---------------------------------------------------------------------------
+// dkdv: one workgroup (4 waves) per (b*h, key tile of 64). Wave w owns the 32
+// keys of block kb = w%2 and the query rows of half qh = w/2 of every query
+// tile (BMQ/2 rows, QB blocks of 32). Per query tile, per wave and block:
+//   S  = Q K^T       A = Q rows (LDS), B = the wave's k (registers)
+//   dP = dout V^T    A = dout rows (LDS), B = the wave's v (registers)
+//   P, dS as above, with lse and delta per query row from the staged stats
+//   dv^T += dout^T P   A = dout^T (transposing reads), B = P (registers)
+//   dk^T += Q^T dS     A = Q^T (transposing reads), B = dS (registers)
+// The two query halves of a key block are summed through LDS at the end.
+constexpr int kStagesKv = 2;
+
+template <int D, int BMQ>
+__global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
+  constexpr int NT = 256;
+  constexpr int CPR = D / 8;
+  constexpr int QT = BMQ * D * 2;       // bytes of a Q (or dout) tile
+  constexpr int SOFF = 2 * QT;          // stats pairs after Q and dout
+  constexpr int STAGE = 2 * QT + BMQ * 8;
+  constexpr int CPW = BMQ * CPR / NT;   // 16-byte copies per thread per tile (Q or dout)
+  constexpr int SL = BMQ / 8;           // stats copies per wave (16 bytes = 2 rows each)
+  constexpr int LPT = 2 * CPW + 1;
+  constexpr int QB = BMQ / 64;
+  constexpr int HALF = BMQ / 2;
+  constexpr int NCH = D / 16;
+  constexpr int NDB = D / 32;
+  constexpr int XCH = 2 * 2 * NDB * 16 * 64 * 4;           // partial-sum exchange
+  constexpr int EPI = XCH > 4 * 32 * (D + 8) * 2 ? XCH : 4 * 32 * (D + 8) * 2;
+  constexpr int LDSB = kStagesKv * STAGE > EPI ? kStagesKv * STAGE : EPI;
+  static_assert(CPW >= 1 && BMQ * CPR % NT == 0, "tile copies must split evenly");
+  static_assert(SL <= 64, "stats copies exceed a wave");
+
+  __shared__ __attribute__((aligned(16))) char lds[LDSB];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 31, half = lane >> 5;
+  const int kb = wave & 1, qh = wave >> 1;
+
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int bh = logical / a.n_ktiles;
+  const int kt = logical - bh * a.n_ktiles;
+  const int k0 = kt * BN;
+  const int64_t slice = (int64_t)bh * a.N * D;
+  const __bf16 *Q = static_cast<const __bf16 *>(a.q) + slice;
+  const __bf16 *K = static_cast<const __bf16 *>(a.k) + slice;
+  const __bf16 *V = static_cast<const __bf16 *>(a.v) + slice;
+  const __bf16 *G = static_cast<const __bf16 *>(a.dout) + slice;
+  const float *S = a.stats + 2 * (int64_t)bh * a.N;
+
+  const int kpos = k0 + kb * 32 + col;
+  bf16x8 kop[NCH], vop[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    kop[c] = *reinterpret_cast<const bf16x8 *>(K + (int64_t)kpos * D + half * (D / 2) + 8 * c);
+    vop[c] = *reinterpret_cast<const bf16x8 *>(V + (int64_t)kpos * D + half * (D / 2) + 8 * c);
+  }
+
+  const PatternArgs &P = a.pat;
+  const Region R = region_of<false>(P, kpos);
+
+  const int nf = sload(a.n_full_t + kt), np = sload(a.n_part_t + kt), ntot = nf + np;
+  const int32_t *fcol = a.full_idx_t + (int64_t)kt * a.n_qtiles;
+  const int32_t *pcol = a.part_idx_t + (int64_t)kt * a.n_qtiles;
+  auto tile_of = [&](int i) { return i < nf ? sload(fcol + i) : sload(pcol + i - nf); };
+
+  int off[CPW];
+#pragma unroll
+  for (int j = 0; j < CPW; ++j) {
+    const int p = (j * 4 + wave) * 64 + lane;
+    const int r = p / CPR, cs = p % CPR;
+    off[j] = r * D + (cs ^ swz<D>(r)) * 8;
+  }
+  auto issue_tile = [&](int qt, int stage) {
+    const __bf16 *Qt = Q + (int64_t)qt * BMQ * D;
+    const __bf16 *Gt = G + (int64_t)qt * BMQ * D;
+    char *base = lds + stage * STAGE;
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) lds_dma16(Qt + off[j], (lds_void *)(base + (j * 4 + wave) * 1024));
+#pragma unroll
+    for (int j = 0; j < CPW; ++j)
+      lds_dma16(Gt + off[j], (lds_void *)(base + QT + (j * 4 + wave) * 1024));
+    if (lane < SL)
+      lds_dma16(S + 2 * ((int64_t)qt * BMQ) + 4 * (wave * SL + lane),
+                (lds_void *)(base + SOFF + wave * SL * 16));
+  };
+
+  int raddr[QB][NCH];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int r = qh * HALF + qb * 32 + row_perm(col);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) raddr[qb][c] = r * D * 2 + (((half * NCH + c) ^ swz<D>(r)) * 16);
+  }
+  int tbase[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) tbase[db] = tr_base<D>(lane, db) + qh * HALF * D * 2;
+
+  f32x16 dk[NDB], dv[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) {
+    dk[db] = f32x16{};
+    dv[db] = f32x16{};
+  }
+  const float sl2 = a.scale_log2;
+
+  if (ntot > 0) issue_tile(tile_of(0), 0);
+
+  for (int it = 0; it < ntot; ++it) {
+    const int stage = it % kStagesKv;
+    wait_then_barrier<0>();
+    if (it + 1 < ntot) issue_tile(tile_of(it + 1), (it + 1) % kStagesKv);
+    const char *st = lds + stage * STAGE;
+    const int qt = tile_of(it);
+
+    f32x16 s[QB], dp[QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      s[qb] = f32x16{};
+      dp[qb] = f32x16{};
+    }
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const bf16x8 qa = *reinterpret_cast<const bf16x8 *>(st + raddr[qb][c]);
+        s[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kop[c], s[qb], 0, 0, 0);
+        const bf16x8 ga = *reinterpret_cast<const bf16x8 *>(st + QT + raddr[qb][c]);
+        dp[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, vop[c], dp[qb], 0, 0, 0);
+      }
+    if (it >= nf) mask_blocks<QB>(s, R, P, qt * BMQ + qh * HALF + 8 * half);
+
+    bf16x8 pop[2 * QB], dsop[2 * QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        // rows qh*HALF + 32qb + 16g + 8half + (0..7): four 16-byte reads of
+        // (lse log2e, delta) pairs, every lane of a half on the same address
+        const float4 *sp = reinterpret_cast<const float4 *>(
+            st + SOFF + (qh * HALF + 32 * qb + 16 * g + 8 * half) * 8);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float4 pr = sp[i];
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            const int v = 8 * g + 2 * i + e;
+            const float l2 = e ? pr.z : pr.x, dl = e ? pr.w : pr.y;
+            const float p = __builtin_amdgcn_exp2f(s[qb][v] * sl2 - l2);
+            pop[2 * qb + g][2 * i + e] = (__bf16)p;
+            dsop[2 * qb + g][2 * i + e] = (__bf16)(p * (dp[qb][v] - dl));
+          }
+        }
+      }
+
+#pragma unroll
+    for (int t = 0; t < 2 * QB; ++t)
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const bf16x8 gt = lds_read_tr16x2(st + QT + tbase[db] + (16 * t) * D * 2, D * 2);
+        dv[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(gt, pop[t], dv[db], 0, 0, 0);
+        const bf16x8 qto = lds_read_tr16x2(st + tbase[db] + (16 * t) * D * 2, D * 2);
+        dk[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qto, dsop[t], dk[db], 0, 0, 0);
+      }
+  }
+
+  // Sum the two query halves: half 1 hands its dk to half 0, half 0 hands its dv
+  // to half 1; then half 0 writes dk and half 1 writes dv.
+  wait_then_barrier<0>();
+  float *xch = reinterpret_cast<float *>(lds);
+  auto xidx = [&](int which, int db, int v) {
+    return (((kb * 2 + which) * NDB + db) * 16 + v) * 64 + lane;
+  };
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      if (qh == 1) xch[xidx(0, db, v)] = dk[db][v];
+      else xch[xidx(1, db, v)] = dv[db][v];
+    }
+  __syncthreads();
+  f32x16 res[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int v = 0; v < 16; ++v)
+      res[db][v] = qh == 0 ? dk[db][v] + xch[xidx(0, db, v)] : dv[db][v] + xch[xidx(1, db, v)];
+  __syncthreads();
+  __bf16 *Os = reinterpret_cast<__bf16 *>(lds) + wave * 32 * (D + 8);
+  stage_rows<D>(res, qh == 0 ? a.scale : 1.f, Os, col, half);
+  __syncthreads();
+  __bf16 *dst = static_cast<__bf16 *>(qh == 0 ? a.dk : a.dv) + slice + (int64_t)(k0 + kb * 32) * D;
+  write_rows<D>(Os, dst, lane);
+}
+
+template <int D, int NW>
+hipError_t launch_dq(const AttnBwdArgs &a, hipStream_t s) {
+  const int64_t blocks = (int64_t)a.BH * a.n_qtiles;
+  hipLaunchKernelGGL((attn_bwd_dq_bf16<D, NW>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int D, int BMQ>
+hipError_t launch_dkdv(const AttnBwdArgs &a, hipStream_t s) {
+  const int64_t blocks = (int64_t)a.BH * a.n_ktiles;
+  hipLaunchKernelGGL((attn_bwd_dkdv_bf16<D, BMQ>), dim3((uint32_t)blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int D, int BM>
+hipError_t launch_all(const AttnBwdArgs &a, hipStream_t s) {
+  hipError_t e = launch_bwd_stats(a, D, true, s);
+  if (e != hipSuccess) return e;
+  e = launch_dq<D, BM / 32>(a, s);
+  if (e != hipSuccess) return e;
+  return launch_dkdv<D, BM>(a, s);
+}
+
+}  // namespace
+
+hipError_t launch_attn_bwd_bf16(const AttnBwdArgs &a, int d, int tile_m, int tile_n,
+                                hipStream_t s) {
+  if (tile_n != BN) return hipErrorInvalidValue;
+  if (d == 64 && tile_m == 128) return launch_all<64, 128>(a, s);
+  if (d == 64 && tile_m == 64) return launch_all<64, 64>(a, s);
+  if (d == 32 && tile_m == 128) return launch_all<32, 128>(a, s);
+  if (d == 32 && tile_m == 64) return launch_all<32, 64>(a, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace hla

@@ -7,21 +7,13 @@
 // MFMA, so each thread owns one query row and does plain FMAs. K and V tiles are
 // staged in LDS and read as broadcasts (every lane of a wave reads the same key
 // row at the same time).
-#include "hla_internal.h"
+#include "attn_common.h"
 
 namespace hla {
 namespace {
 
 constexpr int BN = 64;
 constexpr int CH = 16;  // keys per online-softmax step
-
-__device__ __forceinline__ int xcd_remap(int bid, int total) {
-  const int per = total >> 3, rem = total & 7;
-  const int xcd = bid & 7, slot = bid >> 3;
-  return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
-}
-
-__device__ __forceinline__ int clampi(int x, int lo, int hi) { return min(max(x, lo), hi); }
 
 template <int D, int BM>
 __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
@@ -48,35 +40,7 @@ __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
   for (int i = 0; i < D; ++i) acc[i] = 0.f;
 
   const PatternArgs &P = a.pat;
-  const bool one_d = P.kind == HLA_HILBERT_WINDOW || P.kind == HLA_HILBERT_SLIDE ||
-                     P.kind == HLA_HILBERT_NEIGHBORHOOD || P.kind == HLA_HILBERT_SHIFTED_WINDOW;
-  int lo = 0, hi = 0, rlo = 0, rhi = 0, clo = 0, chi = 0;
-  if (P.kind == HLA_HILBERT_WINDOW) {
-    lo = (qpos / P.p0) * P.p0;
-    hi = lo + P.p0 - 1;
-  } else if (P.kind == HLA_HILBERT_SLIDE) {
-    lo = qpos - P.p0;
-    hi = qpos + P.p0;
-  } else if (P.kind == HLA_HILBERT_NEIGHBORHOOD) {
-    lo = clampi(qpos - P.p0 / 2, 0, P.N - P.p0);
-    hi = lo + P.p0 - 1;
-  } else if (P.kind == HLA_HILBERT_SHIFTED_WINDOW) {
-    const int g = (qpos + P.p0 - P.p1) / P.p0;
-    lo = g * P.p0 - P.p0 + P.p1;
-    hi = lo + P.p0 - 1;
-  } else {
-    const int r = (int)fdiv((uint32_t)qpos, P.wdiv), c = qpos - r * P.W;
-    if (P.kind == HLA_ROWMAJOR_WINDOW) {
-      rlo = (r / P.p0) * P.p0; rhi = rlo + P.p0 - 1;
-      clo = (c / P.p1) * P.p1; chi = clo + P.p1 - 1;
-    } else if (P.kind == HLA_ROWMAJOR_SLIDE) {
-      rlo = r - P.p0; rhi = r + P.p0;
-      clo = c - P.p1; chi = c + P.p1;
-    } else {
-      rlo = clampi(r - P.p0 / 2, 0, P.H - P.p0); rhi = rlo + P.p0 - 1;
-      clo = clampi(c - P.p1 / 2, 0, P.W - P.p1); chi = clo + P.p1 - 1;
-    }
-  }
+  const Region R = region_of<true>(P, qpos);
 
   const int nf = a.n_full[qt], np = a.n_part[qt], ntot = nf + np;
   const int32_t *frow = a.full_idx + (int64_t)qt * a.n_ktiles;
@@ -106,17 +70,8 @@ __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
       }
       if (masked) {
 #pragma unroll
-        for (int j = 0; j < CH; ++j) {
-          const int kpos = kt * BN + j0 + j;
-          bool ok;
-          if (one_d) {
-            ok = kpos >= lo && kpos <= hi;
-          } else {
-            const int r = (int)fdiv((uint32_t)kpos, P.wdiv), c = kpos - r * P.W;
-            ok = r >= rlo && r <= rhi && c >= clo && c <= chi;
-          }
-          if (!ok) s[j] = -__builtin_inff();
-        }
+        for (int j = 0; j < CH; ++j)
+          if (!region_has(R, P, kt * BN + j0 + j)) s[j] = -__builtin_inff();
       }
       float mx = s[0];
 #pragma unroll

@@ -1,4 +1,4 @@
-// Tile classification and per-row tile lists (Sec. 3.1: full, partial and
+// Tile classification and per-row / per-column tile lists (Sec. 3.1: full, partial and
 // empty blocks of the N x N score matrix; empty blocks are skipped, full
 // blocks run without a mask, partial blocks need the element mask).
 //
@@ -12,9 +12,11 @@
 // condition and a column condition, so each rectangle pair is decided per axis
 // and the tile is non-empty if any pair is, full if every pair is.
 //
-// Layout: one workgroup per query-tile row walks the key tiles in chunks of
-// 256, compacts full and partial indices with wave ballots into ascending
-// lists, then pads the rest of both rows with -1.
+// Layout: one workgroup per line walks the tiles of that line in chunks of 256,
+// compacts full and partial indices with wave ballots into ascending lists,
+// then pads the rest of both lists with -1. A line is a query-tile row (the
+// forward pass and the query gradients walk these) or, for the optional
+// transposed lists, a key-tile column (the key and value gradients walk these).
 #include "hla_internal.h"
 
 namespace hla {
@@ -122,21 +124,27 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
                                    __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
+// COLS = false: line = query-tile row q, entries = key tiles.
+// COLS = true:  line = key-tile column k, entries = query tiles.
+template <bool COLS>
 __global__ void __launch_bounds__(kThreads)
-    classify_rows(PatternArgs p, int32_t tile_m, int32_t tile_n, int32_t n_ktiles,
-                  int32_t *__restrict__ n_full, int32_t *__restrict__ full_idx,
-                  int32_t *__restrict__ n_part, int32_t *__restrict__ part_idx) {
+    classify_lines(PatternArgs p, int32_t tile_m, int32_t tile_n, int32_t n_entries,
+                   int32_t *__restrict__ n_full, int32_t *__restrict__ full_idx,
+                   int32_t *__restrict__ n_part, int32_t *__restrict__ part_idx) {
   __shared__ int32_t wave_f[kWaves], wave_p[kWaves];
-  const int q = blockIdx.x;
+  const int line = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int i0 = q * tile_m, i1 = i0 + tile_m - 1;
-  int32_t *frow = full_idx + (int64_t)q * n_ktiles;
-  int32_t *prow = part_idx + (int64_t)q * n_ktiles;
+  int32_t *flist = full_idx + (int64_t)line * n_entries;
+  int32_t *plist = part_idx + (int64_t)line * n_entries;
   int nf = 0, np = 0;
-  for (int base = 0; base < n_ktiles; base += kThreads) {
-    const int kt = base + tid;
+  for (int base = 0; base < n_entries; base += kThreads) {
+    const int e = base + tid;
     int cls = 0;
-    if (kt < n_ktiles) cls = classify_tile(p, i0, i1, kt * tile_n, kt * tile_n + tile_n - 1);
+    if (e < n_entries) {
+      const int qt = COLS ? e : line, kt = COLS ? line : e;
+      cls = classify_tile(p, qt * tile_m, qt * tile_m + tile_m - 1, kt * tile_n,
+                          kt * tile_n + tile_n - 1);
+    }
     const uint64_t bf = __ballot(cls == 2);
     const uint64_t bp = __ballot(cls == 1);
     if (lane == 0) {
@@ -154,17 +162,17 @@ __global__ void __launch_bounds__(kThreads)
       tot_f += wave_f[w];
       tot_p += wave_p[w];
     }
-    if (cls == 2) frow[nf + off_f + lanes_below(bf)] = kt;
-    if (cls == 1) prow[np + off_p + lanes_below(bp)] = kt;
+    if (cls == 2) flist[nf + off_f + lanes_below(bf)] = e;
+    if (cls == 1) plist[np + off_p + lanes_below(bp)] = e;
     nf += tot_f;
     np += tot_p;
     __syncthreads();
   }
-  for (int t = nf + tid; t < n_ktiles; t += kThreads) frow[t] = -1;
-  for (int t = np + tid; t < n_ktiles; t += kThreads) prow[t] = -1;
+  for (int t = nf + tid; t < n_entries; t += kThreads) flist[t] = -1;
+  for (int t = np + tid; t < n_entries; t += kThreads) plist[t] = -1;
   if (tid == 0) {
-    n_full[q] = nf;
-    n_part[q] = np;
+    n_full[line] = nf;
+    n_part[line] = np;
   }
 }
 
@@ -201,15 +209,22 @@ __global__ void __launch_bounds__(kThreads)
 }  // namespace
 
 hipError_t launch_block_mask(const PatternArgs &pat, int32_t tile_m, int32_t tile_n,
-                             int32_t n_qtiles, int32_t n_ktiles, int32_t *n_full,
-                             int32_t *full_idx, int32_t *n_part, int32_t *part_idx,
-                             int32_t *totals, hipStream_t s) {
-  hipLaunchKernelGGL(classify_rows, dim3(n_qtiles), dim3(kThreads), 0, s, pat, tile_m,
-                     tile_n, n_ktiles, n_full, full_idx, n_part, part_idx);
+                             int32_t n_qtiles, int32_t n_ktiles, const BlockLists &rows,
+                             const BlockLists *cols, int32_t *totals, hipStream_t s) {
+  hipLaunchKernelGGL(classify_lines<false>, dim3(n_qtiles), dim3(kThreads), 0, s, pat, tile_m,
+                     tile_n, n_ktiles, rows.n_full, rows.full_idx, rows.n_part, rows.part_idx);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || !totals) return e;
-  hipLaunchKernelGGL(sum_totals, dim3(1), dim3(kThreads), 0, s, n_full, n_part, n_qtiles,
-                     totals);
+  if (e != hipSuccess) return e;
+  if (cols) {
+    hipLaunchKernelGGL(classify_lines<true>, dim3(n_ktiles), dim3(kThreads), 0, s, pat, tile_m,
+                       tile_n, n_qtiles, cols->n_full, cols->full_idx, cols->n_part,
+                       cols->part_idx);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (!totals) return hipSuccess;
+  hipLaunchKernelGGL(sum_totals, dim3(1), dim3(kThreads), 0, s, rows.n_full, rows.n_part,
+                     n_qtiles, totals);
   return hipGetLastError();
 }
 

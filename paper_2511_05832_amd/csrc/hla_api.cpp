@@ -172,25 +172,35 @@ hla_status hla_build_block_mask(hla_block_mask *mask, hla_stream_t stream) {
   }
   if (mask->totals && !aligned(mask->totals, 4))
     return fail(HLA_ERR_INVALID_ARG, "mask->totals is not 4-byte aligned");
+  int32_t *cols[4] = {mask->n_full_t, mask->full_idx_t, mask->n_part_t, mask->part_idx_t};
+  const char *cnames[4] = {"n_full_t", "full_idx_t", "n_part_t", "part_idx_t"};
+  const int nset = (cols[0] != nullptr) + (cols[1] != nullptr) + (cols[2] != nullptr) +
+                   (cols[3] != nullptr);
+  if (nset != 0 && nset != 4)
+    return fail(HLA_ERR_INVALID_ARG, "set all four transposed-list pointers or none");
+  for (int i = 0; i < 4 && nset; ++i)
+    if (!aligned(cols[i], 4)) return fail(HLA_ERR_INVALID_ARG, "mask->%s is not 4-byte aligned", cnames[i]);
   mask->N = mask->pat.H * mask->pat.W;
   mask->n_qtiles = nq;
   mask->n_ktiles = nk;
   const hla::PatternArgs pa = hla::make_pattern_args(mask->pat);
-  return hip_status(hla::launch_block_mask(pa, mask->tile_m, mask->tile_n, nq, nk, mask->n_full,
-                                           mask->full_idx, mask->n_part, mask->part_idx,
-                                           mask->totals, (hipStream_t)stream),
+  const hla::BlockLists rows = {mask->n_full, mask->full_idx, mask->n_part, mask->part_idx};
+  const hla::BlockLists tcols = {mask->n_full_t, mask->full_idx_t, mask->n_part_t, mask->part_idx_t};
+  return hip_status(hla::launch_block_mask(pa, mask->tile_m, mask->tile_n, nq, nk, rows,
+                                           nset ? &tcols : nullptr, mask->totals,
+                                           (hipStream_t)stream),
                     "hla_build_block_mask");
 }
 
-hla_status hla_attn_fwd(const void *q, const void *k, const void *v, const hla_block_mask *mask,
-                        void *out, float *lse, int64_t B, int64_t heads, int64_t N, int64_t d,
-                        hla_dtype dtype, float scale, hla_stream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Checks shared by the attention passes: the mask, sizes, dtype, scale and the
+// supported shapes. Pointers are checked by the callers.
+hla_status check_attn(const hla_block_mask *mask, int64_t B, int64_t heads, int64_t N,
+                      int64_t d, hla_dtype dtype, float scale) {
   hla_status st;
-  if ((st = check_tensor_args(q, "q")) != HLA_OK) return st;
-  if ((st = check_tensor_args(k, "k")) != HLA_OK) return st;
-  if ((st = check_tensor_args(v, "v")) != HLA_OK) return st;
-  if ((st = check_tensor_args(out, "out")) != HLA_OK) return st;
-  if (lse && !aligned(lse, 4)) return fail(HLA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
   if (!mask) return fail(HLA_ERR_INVALID_ARG, "mask is NULL");
   if (!mask->n_full || !mask->full_idx || !mask->n_part || !mask->part_idx)
     return fail(HLA_ERR_INVALID_ARG, "mask arrays are NULL (build the mask first)");
@@ -210,13 +220,36 @@ hla_status hla_attn_fwd(const void *q, const void *k, const void *v, const hla_b
     return fail(HLA_ERR_UNSUPPORTED, "tile %dx%d (supported: 64x64, 128x64)", mask->tile_m, mask->tile_n);
   if (N * d > (1LL << 30)) return fail(HLA_ERR_UNSUPPORTED, "N * d exceeds 2^30 per (b, head)");
   const int64_t BH = B * heads;
-  if (BH * mask->n_qtiles > kMaxI32) return fail(HLA_ERR_UNSUPPORTED, "grid too large");
+  if (BH * mask->n_qtiles > kMaxI32 || BH * mask->n_ktiles > kMaxI32 || BH * N > kMaxI32)
+    return fail(HLA_ERR_UNSUPPORTED, "grid too large");
+  return HLA_OK;
+}
+
+bool overlaps(const void *a, int64_t na, const void *b, int64_t nb) {
+  const char *x = static_cast<const char *>(a), *y = static_cast<const char *>(b);
+  return x < y + nb && y < x + na;
+}
+
+}  // namespace
+
+extern "C" {
+
+hla_status hla_attn_fwd(const void *q, const void *k, const void *v, const hla_block_mask *mask,
+                        void *out, float *lse, int64_t B, int64_t heads, int64_t N, int64_t d,
+                        hla_dtype dtype, float scale, hla_stream_t stream) {
+  hla_status st;
+  if ((st = check_tensor_args(q, "q")) != HLA_OK) return st;
+  if ((st = check_tensor_args(k, "k")) != HLA_OK) return st;
+  if ((st = check_tensor_args(v, "v")) != HLA_OK) return st;
+  if ((st = check_tensor_args(out, "out")) != HLA_OK) return st;
+  if (lse && !aligned(lse, 4)) return fail(HLA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
+  if ((st = check_attn(mask, B, heads, N, d, dtype, scale)) != HLA_OK) return st;
+  const int64_t BH = B * heads;
   const int64_t bytes = BH * N * d * dtype_size(dtype);
-  const char *o = static_cast<const char *>(out);
-  for (const void *in : {q, k, v}) {
-    const char *s = static_cast<const char *>(in);
-    if (o < s + bytes && s < o + bytes) return fail(HLA_ERR_INVALID_ARG, "out overlaps an input");
-  }
+  for (const void *in : {q, k, v})
+    if (overlaps(out, bytes, in, bytes)) return fail(HLA_ERR_INVALID_ARG, "out overlaps an input");
+  if (lse && overlaps(lse, BH * N * 4, out, bytes))
+    return fail(HLA_ERR_INVALID_ARG, "lse overlaps out");
   hla::AttnArgs a;
   a.q = q;
   a.k = k;
@@ -237,6 +270,74 @@ hla_status hla_attn_fwd(const void *q, const void *k, const void *v, const hla_b
                      ? hla::launch_attn_bf16(a, (int)d, mask->tile_m, mask->tile_n, (hipStream_t)stream)
                      : hla::launch_attn_f32(a, (int)d, mask->tile_m, mask->tile_n, (hipStream_t)stream);
   return hip_status(e, "hla_attn_fwd");
+}
+
+hla_status hla_attn_bwd(const void *q, const void *k, const void *v, const void *out,
+                        const void *dout, const float *lse, const hla_block_mask *mask, void *dq,
+                        void *dk, void *dv, float *stats, int64_t B, int64_t heads, int64_t N,
+                        int64_t d, hla_dtype dtype, float scale, hla_stream_t stream) {
+  hla_status st;
+  const void *ins[5] = {q, k, v, out, dout};
+  const char *in_names[5] = {"q", "k", "v", "out", "dout"};
+  for (int i = 0; i < 5; ++i)
+    if ((st = check_tensor_args(ins[i], in_names[i])) != HLA_OK) return st;
+  void *outs[3] = {dq, dk, dv};
+  const char *out_names[3] = {"dq", "dk", "dv"};
+  for (int i = 0; i < 3; ++i)
+    if ((st = check_tensor_args(outs[i], out_names[i])) != HLA_OK) return st;
+  if ((st = check_tensor_args(lse, "lse")) != HLA_OK) return st;
+  if ((st = check_tensor_args(stats, "stats")) != HLA_OK) return st;
+  if ((st = check_attn(mask, B, heads, N, d, dtype, scale)) != HLA_OK) return st;
+  if (!mask->n_full_t || !mask->full_idx_t || !mask->n_part_t || !mask->part_idx_t)
+    return fail(HLA_ERR_INVALID_ARG, "the mask has no transposed lists (set them before building it)");
+  const int64_t BH = B * heads;
+  const int64_t bytes = BH * N * d * dtype_size(dtype);
+  for (int i = 0; i < 3; ++i) {
+    for (int j = 0; j < 5; ++j)
+      if (overlaps(outs[i], bytes, ins[j], bytes))
+        return fail(HLA_ERR_INVALID_ARG, "%s overlaps %s", out_names[i], in_names[j]);
+    for (int j = i + 1; j < 3; ++j)
+      if (overlaps(outs[i], bytes, outs[j], bytes))
+        return fail(HLA_ERR_INVALID_ARG, "%s overlaps %s", out_names[i], out_names[j]);
+    if (overlaps(outs[i], bytes, stats, BH * N * 8))
+      return fail(HLA_ERR_INVALID_ARG, "%s overlaps stats", out_names[i]);
+  }
+  for (int j = 0; j < 5; ++j)
+    if (overlaps(stats, BH * N * 8, ins[j], bytes))
+      return fail(HLA_ERR_INVALID_ARG, "stats overlaps %s", in_names[j]);
+  if (overlaps(stats, BH * N * 8, lse, BH * N * 4))
+    return fail(HLA_ERR_INVALID_ARG, "stats overlaps lse");
+  hla::AttnBwdArgs a;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.out = out;
+  a.dout = dout;
+  a.lse = lse;
+  a.stats = stats;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.n_full = mask->n_full;
+  a.full_idx = mask->full_idx;
+  a.n_part = mask->n_part;
+  a.part_idx = mask->part_idx;
+  a.n_full_t = mask->n_full_t;
+  a.full_idx_t = mask->full_idx_t;
+  a.n_part_t = mask->n_part_t;
+  a.part_idx_t = mask->part_idx_t;
+  a.BH = (int32_t)BH;
+  a.N = (int32_t)N;
+  a.n_qtiles = mask->n_qtiles;
+  a.n_ktiles = mask->n_ktiles;
+  a.scale = scale;
+  a.scale_log2 = (float)((double)scale * 1.4426950408889634074);
+  a.pat = hla::make_pattern_args(mask->pat);
+  hipError_t e =
+      dtype == HLA_BF16
+          ? hla::launch_attn_bwd_bf16(a, (int)d, mask->tile_m, mask->tile_n, (hipStream_t)stream)
+          : hla::launch_attn_bwd_f32(a, (int)d, mask->tile_m, mask->tile_n, (hipStream_t)stream);
+  return hip_status(e, "hla_attn_bwd");
 }
 
 hla_status hla_qkv_proj(const void *x, const void *w_qkv, void *q, void *k, void *v, int64_t B,

@@ -66,10 +66,18 @@ hipError_t launch_permute(const void *src, void *dst, const int32_t *order,
                           int64_t BH, int64_t N, int64_t row_bytes, bool scatter,
                           hipStream_t s);
 
+// One direction of tile lists: per line, the count and ascending -1-padded list
+// of the full tiles and of the partial tiles.
+struct BlockLists {
+  int32_t *n_full, *full_idx, *n_part, *part_idx;
+};
+
+// Row lists always; column lists when cols is not NULL; totals (of the row
+// lists) when totals is not NULL.
 hipError_t launch_block_mask(const PatternArgs &pat, int32_t tile_m,
                              int32_t tile_n, int32_t n_qtiles, int32_t n_ktiles,
-                             int32_t *n_full, int32_t *full_idx, int32_t *n_part,
-                             int32_t *part_idx, int32_t *totals, hipStream_t s);
+                             const BlockLists &rows, const BlockLists *cols,
+                             int32_t *totals, hipStream_t s);
 
 struct AttnArgs {
   const void *q, *k, *v;
@@ -85,6 +93,28 @@ hipError_t launch_attn_bf16(const AttnArgs &a, int d, int tile_m, int tile_n,
                             hipStream_t s);
 hipError_t launch_attn_f32(const AttnArgs &a, int d, int tile_m, int tile_n,
                            hipStream_t s);
+
+struct AttnBwdArgs {
+  const void *q, *k, *v, *out, *dout;
+  const float *lse;
+  float *stats;  // per row: (lse * log2 e, delta), 2 floats
+  void *dq, *dk, *dv;
+  const int32_t *n_full, *full_idx, *n_part, *part_idx;          // per query-tile row
+  const int32_t *n_full_t, *full_idx_t, *n_part_t, *part_idx_t;  // per key-tile column
+  int32_t BH, N, n_qtiles, n_ktiles;
+  float scale, scale_log2;
+  PatternArgs pat;
+};
+
+// Per-row (lse * log2 e, delta = <dout, out>) into a.stats; d in {32, 64}.
+hipError_t launch_bwd_stats(const AttnBwdArgs &a, int d, bool bf16, hipStream_t s);
+
+// Row statistics, then the query gradients (row lists), then the key and value
+// gradients (column lists), all on stream s.
+hipError_t launch_attn_bwd_bf16(const AttnBwdArgs &a, int d, int tile_m, int tile_n,
+                                hipStream_t s);
+hipError_t launch_attn_bwd_f32(const AttnBwdArgs &a, int d, int tile_m, int tile_n,
+                               hipStream_t s);
 
 hipError_t launch_qkv_proj(const void *x, const void *w, void *q, void *k, void *v,
                            int64_t B, int64_t N, int64_t heads, int64_t d,

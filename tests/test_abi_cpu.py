@@ -144,6 +144,56 @@ def test_attn_validation(L):
     assert L.hla_attn_fwd(q, k, v, None, o, None, 2, 4, N, 64, hla.HLA_BF16, 0.1, None) == hla.HLA_ERR_INVALID_ARG
 
 
+def test_build_block_mask_rejects_partial_column_lists(L):
+    m = hla.BlockMaskStruct()
+    m.pat = desc("hilbert_slide", 64, 64, 128)
+    m.tile_m, m.tile_n = 128, 64
+    m.n_full = m.full_idx = m.n_part = m.part_idx = 0x40000
+    m.n_full_t = m.full_idx_t = 0x50000
+    assert L.hla_build_block_mask(ctypes.byref(m), None) == hla.HLA_ERR_INVALID_ARG
+    assert "transposed" in L.hla_last_error().decode()
+    m.n_part_t, m.part_idx_t = 0x50000, 0x50002
+    assert L.hla_build_block_mask(ctypes.byref(m), None) == hla.HLA_ERR_INVALID_ARG
+    assert "part_idx_t" in L.hla_last_error().decode()
+
+
+def test_attn_bwd_validation(L):
+    """Every call here is invalid, so nothing is launched."""
+    vp = ctypes.c_void_p
+    N, B, heads, d = 4096, 2, 4, 64
+    tensor = B * heads * N * d * 2
+    base = [vp(0x10000000 + i * 0x1000000) for i in range(10)]   # 16 MiB apart > tensor
+    assert tensor <= 0x1000000
+    q, k, v, o, g, lse, dq, dk, dv, st = base
+
+    def call(m, **kw):
+        a = dict(q=q, k=k, v=v, out=o, dout=g, lse=lse, dq=dq, dk=dk, dv=dv, stats=st,
+                 d=d, dt=hla.HLA_BF16, scale=0.125, N=N)
+        a.update(kw)
+        return L.hla_attn_bwd(a["q"], a["k"], a["v"], a["out"], a["dout"], a["lse"],
+                              ctypes.byref(m) if m is not None else None, a["dq"], a["dk"],
+                              a["dv"], a["stats"], B, heads, a["N"], a["d"], a["dt"],
+                              a["scale"], None)
+
+    m = fake_mask()
+    assert call(m) == hla.HLA_ERR_INVALID_ARG          # no transposed lists
+    assert "transposed" in L.hla_last_error().decode()
+    m.n_full_t = m.full_idx_t = m.n_part_t = m.part_idx_t = 0x60000
+    assert call(None) == hla.HLA_ERR_INVALID_ARG
+    assert call(m, d=48) == hla.HLA_ERR_UNSUPPORTED
+    assert call(m, N=2048) == hla.HLA_ERR_INVALID_ARG
+    assert call(m, scale=-1.0) == hla.HLA_ERR_INVALID_ARG
+    assert call(m, lse=None) == hla.HLA_ERR_INVALID_ARG
+    assert call(m, stats=None) == hla.HLA_ERR_INVALID_ARG
+    assert call(m, dout=vp(0x10000008)) == hla.HLA_ERR_INVALID_ARG      # misaligned
+    assert call(m, dk=vp(q.value + 4096)) == hla.HLA_ERR_INVALID_ARG     # dk overlaps q
+    assert "overlaps" in L.hla_last_error().decode()
+    assert call(m, dv=vp(dq.value + 64)) == hla.HLA_ERR_INVALID_ARG      # dv overlaps dq
+    assert call(m, stats=vp(dv.value + 256)) == hla.HLA_ERR_INVALID_ARG  # stats overlaps dv
+    assert call(m, stats=vp(lse.value)) == hla.HLA_ERR_INVALID_ARG       # stats overlaps lse
+    assert call(fake_mask(tm=256, tn=64)) == hla.HLA_ERR_UNSUPPORTED
+
+
 def test_proj_validation(L):
     vp = ctypes.c_void_p
     x, w, q, k, v = (vp(0x100000 * i) for i in range(1, 6))

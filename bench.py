@@ -19,6 +19,11 @@ same batch x heads x tokens x head_dim as the paper's headline window row
 (Table 1, I=128x128, W=16x16). The same kernel is then timed on the row-major
 16x16 window mask for the empty-tile comparison, and the CPU oracle is timed
 on a bounded sample of the same step on the host cores.
+
+The backward pass of the same attention workload is timed the same way (a
+graph-replayed step: gather of the upstream gradient, hla_attn_bwd, scatter of
+dq, dk, dv; per-call time of hla_attn_bwd from an eager pass) and reported under
+"backward"; --no-backward skips it.
 """
 from __future__ import annotations
 
@@ -149,6 +154,52 @@ class AttnPipeline:
         w = self.w
         return 2 * w.B * w.heads * w.N * w.d * esize(w.dtype) + 4 * w.N
 
+
+    # backward ------------------------------------------------------------
+    def setup_backward(self):
+        """Buffers of the backward pass for every input set (after the forward has run
+        on every set, so out and lse are valid): an upstream gradient in row-major
+        order and the gradients; the mask with its per-column lists."""
+        hla, w = self.hla, self.w
+        g = torch.Generator(device="cpu")
+        g.manual_seed(w.seed + 1000)
+        dout = torch.randn((w.B, w.heads, w.N, w.d), generator=g).to(tdtype(w.dtype))
+        for s in self.sets:
+            s["dout"] = dout.cuda()
+            for n in ("dq", "dk", "dv"):
+                s[n] = torch.empty_like(s["q"])
+            if self.hilbert:
+                s["douth"] = torch.empty_like(s["q"])
+                for n in ("dqr", "dkr", "dvr"):
+                    s[n] = torch.empty_like(s["q"])
+            s["stats"] = torch.empty((w.B, w.heads, w.N, 2), dtype=torch.float32, device="cuda")
+        self.mask_c = hla.BlockMask(w.pattern, w.tile_m, w.tile_n, columns=True).build()
+        self.timer_bwd = Timer()
+
+    def step_backward(self, i):
+        """Gather the upstream gradient into the forward's order, run the backward,
+        scatter dq, dk, dv back to row-major."""
+        hla, w, s, T = self.hla, self.w, self.sets[i % self.nsets], self.timer_bwd
+        if self.hilbert:
+            with T.stage("gather"):
+                hla.gather(s["dout"], self.order, out=s["douth"])
+            names = ("qh", "kh", "vh", "oh", "douth")
+        else:
+            names = ("q", "k", "v", "o", "dout")
+        with T.stage("attn_bwd"):
+            hla.attn_bwd(*(s[n] for n in names), s["lse"], self.mask_c, w.scale,
+                         dq=s["dq"], dk=s["dk"], dv=s["dv"], stats=s["stats"])
+        if self.hilbert:
+            with T.stage("scatter"):
+                for a, b in (("dq", "dqr"), ("dk", "dkr"), ("dv", "dvr")):
+                    hla.scatter(s[a], self.order, out=s[b])
+
+    def bwd_bytes(self):
+        """Algorithmic HBM bytes of one backward call: q, k, v, out, dout read and dq,
+        dk, dv written once (8 N d s), lse read (4 N), row stats written and read
+        (16 N), per (b, h)."""
+        w = self.w
+        return (8 * w.N * w.d * esize(w.dtype) + 20 * w.N) * w.B * w.heads
 
 # ----------------------------------------------------------------------------
 # layer workload
@@ -283,6 +334,64 @@ def run_timed(pipe, steps, warmup):
     return graph_ms, eager_ms
 
 
+def time_backward(pipe, steps, warmup):
+    """Backward pass of an attention workload: eager pass with stage events, then
+    replays of one captured graph per input set (as for the forward)."""
+    pipe.setup_backward()
+    for i in range(warmup):
+        pipe.step_backward(i)
+    torch.cuda.synchronize()
+    T = pipe.timer_bwd
+    T.active = True
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        pipe.step_backward(i)
+    end.record()
+    torch.cuda.synchronize()
+    T.active = False
+    eager_ms = start.elapsed_time(end) / steps
+    graphs = []
+    for i in range(pipe.nsets):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            pipe.step_backward(i)
+        graphs.append(g)
+    torch.cuda.synchronize()
+    for i in range(min(warmup, len(graphs)) or 1):
+        graphs[i % len(graphs)].replay()
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(steps):
+        graphs[i % len(graphs)].replay()
+    end.record()
+    torch.cuda.synchronize()
+    graph_ms = start.elapsed_time(end) / steps
+    del graphs
+    w = pipe.w
+    tf, tp = pipe.mask.host_totals()
+    tiles = (tf + tp) * w.B * w.heads
+    # five products per non-empty tile (S, dP, dV, dK, dQ), the usual count; the
+    # kernels recompute S and dP once more (seven products executed)
+    flops = 10.0 * w.tile_m * w.tile_n * w.d * tiles
+    bwd_ms = T.mean_ms("attn_bwd")
+    peak = BF16_PEAK_TFLOPS if w.dtype == "bf16" else FP32_PEAK_TFLOPS
+    tflops = flops / (bwd_ms * 1e-3) / 1e12
+    return {
+        "ms_per_step": graph_ms,
+        "ms_per_step_eager": eager_ms,
+        "step": "gather of dout, attention backward, scatter of dq, dk, dv" if pipe.hilbert
+                else "attention backward",
+        "attn_bwd_ms_per_call": bwd_ms,
+        "tile_flops": flops,
+        "tile_flops_executed": 1.4 * flops,
+        "attn_bwd_tflops_nonempty_tiles": tflops,
+        "attn_bwd_pct_peak": 100.0 * tflops / peak,
+        "attn_bwd_algorithmic_gbs": pipe.bwd_bytes() / (bwd_ms * 1e-3) / 1e9,
+        "stages_ms": {n: T.mean_ms(n) for n in T.pairs},
+    }
+
+
 def summarize(pipe, timing):
     ms_step, eager_ms = timing
     T = pipe.timer
@@ -394,6 +503,8 @@ def main():
     ap.add_argument("--all", action="store_true",
                     help="also time every workload and write gpurun_out/bench_all.json")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-backward", action="store_true",
+                    help="skip timing the backward pass of the workload")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="before the steps, time a plain device-to-device copy of this many MiB "
                          "(a kernel of known traffic, to calibrate HBM byte counters)")
@@ -426,6 +537,10 @@ def main():
     ms = timing[0]
     res = summarize(pipe, timing)
     print(f"[bench] {w.name}: {json.dumps(res)}", file=sys.stderr, flush=True)
+    bwd = None
+    if isinstance(w, W.AttnWorkload) and not args.no_backward:
+        bwd = time_backward(pipe, args.steps, args.warmup)
+        print(f"[bench] {w.name} backward: {json.dumps(bwd)}", file=sys.stderr, flush=True)
 
     compare = args.compare
     if compare is None and not args.copy_mib:
@@ -442,6 +557,8 @@ def main():
         for name, wl in W.WORKLOADS.items():
             p = make_pipeline(wl, hla)
             r = summarize(p, run_timed(p, args.steps, args.warmup))
+            if isinstance(wl, W.AttnWorkload) and not args.no_backward:
+                r["backward"] = time_backward(p, args.steps, args.warmup)
             allres[name] = r
             print(f"[bench] {name}: {json.dumps(r)}", file=sys.stderr, flush=True)
             del p
@@ -504,6 +621,8 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    if bwd:
+        line["backward"] = bwd
     if cmp_res:
         line["rowmajor_comparison"] = {
             "workload": cmp_res["workload"], "attn_ms_per_call": cmp_res["attn_ms"],

@@ -84,3 +84,38 @@ def test_layer_step_graph_replays_match_eager():
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(y, ref), r
+
+
+def test_backward_step_graph_replays_match_eager():
+    pat = W.Pattern(W.HILBERT_WINDOW, 32, 32, 64)
+    B, Hh, N, d = 2, 2, 1024, 64
+    q, k, v = (t.cuda() for t in W.attn_inputs(B, Hh, N, d, "bf16", seed=23))
+    g = torch.randn((B, Hh, N, d), generator=torch.Generator().manual_seed(24)).to(torch.bfloat16).cuda()
+    mask = hla.BlockMask(pat, 128, 64, columns=True)
+    out = torch.empty_like(q)
+    lse = torch.empty((B, Hh, N), dtype=torch.float32, device="cuda")
+    grads = [torch.empty_like(q) for _ in range(3)]
+    stats = torch.empty((B, Hh, N, 2), dtype=torch.float32, device="cuda")
+
+    def step():
+        mask.build()
+        hla.attn_fwd(q, k, v, mask, 0.125, out=out, lse=lse)
+        hla.attn_bwd(q, k, v, out, g, lse, mask, 0.125, dq=grads[0], dk=grads[1], dv=grads[2],
+                     stats=stats)
+
+    step()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in grads]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for r in range(3):
+        for t in grads + [out]:
+            t.normal_()
+        stats.fill_(float("nan"))
+        mask.part_idx_t.fill_(-3)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(grads, ref):
+            assert torch.equal(a, b), r

@@ -190,7 +190,7 @@ hla_status hla_attn_fwd(const void *q, const void *k, const void *v,
  * Block-sparse attention backward: the gradients of hla_attn_fwd's out with
  * respect to q, k and v for an upstream gradient dout, over the same tiles as
  * the forward (empty tiles skipped, partial tiles masked; the paper times this
- * pass beside the forward for every pattern, Tables 1-3). With the forward's lse:
+ * pass beside the forward for every pattern, Tables 1, 3, 6, 7, 9, 11). With the forward's lse:
  *   P[i,j]  = exp(scale * <q_i, k_j> - lse_i)  if allowed(i, j), else 0
  *   delta_i = <dout_i, out_i>                  (= sum_j P[i,j] <dout_i, v_j>)
  *   dS[i,j] = P[i,j] * (<dout_i, v_j> - delta_i)

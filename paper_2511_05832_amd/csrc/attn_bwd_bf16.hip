@@ -2,7 +2,7 @@
 // on gfx950 bf16 matrix cores (v_mfma_f32_32x32x16_bf16).
 //
 // What it computes: the gradients of the forward pass (the paper times the
-// backward of every attention it measures, Tables 1-3 and 6-11) over the same
+// backward of every attention it measures, Tables 1, 3, 6, 7, 9, 11) over the same
 // tile structure - empty tiles skipped, full tiles unmasked, partial tiles with
 // the element mask (Sec. 3.1; Eq. 1's per-block cost applies to both passes).
 // With the forward's lse and delta_i = <dout_i, out_i> (row statistics kernel):

@@ -11,7 +11,8 @@
 //
 // Per key tile, per wave:
 //   S^T = K Q^T    (keys x queries): 2 key blocks of 32 x D/16 MFMAs. A = K rows
-//                  from LDS, B = the wave's Q (kept in registers all kernel).
+//                  from LDS, B = the wave's Q (kept in registers all kernel,
+//                  after one pass through LDS at the start).
 //   softmax        lane l owns query l%32; its 32 scores of the tile sit in its
 //                  own accumulators (16 per key block, the other half of the keys
 //                  in lane l^32), so row max / sum need one cross-half exchange.
@@ -31,7 +32,11 @@
 //
 // K/V staging. K and V tiles go from global memory straight into LDS with
 // global_load_lds_dwordx4 (no register round trip), into a ring of kStages
-// stages kept kStages-1 tiles ahead. Both are stored row-major, 16-byte chunks
+// stages kept kStages-1 tiles ahead. The Q tile takes the same path once, into
+// the stage the third key tile fills later. The copies are issued from inline
+// assembly: the compiler's wait insertion would otherwise treat each
+// transposing V read as possibly overlapping a copy in flight and wait for all
+// of them - including the tile prefetched two steps ahead - on every tile. Both are stored row-major, 16-byte chunks
 // XOR-swizzled per row so that the K operand reads (ds_read_b128, eight lanes on
 // eight rows) and the transposing V reads (ds_read_b64_tr_b16, sixteen lanes on
 // four rows) each touch distinct bank groups; the swizzle is applied on the
@@ -41,7 +46,13 @@
 // stage visible to all waves.
 //
 // Tile-list entries are read with scalar loads. Accumulators live in ordinary
-// VGPRs (the library is built with the VGPR form of MFMA).
+// VGPRs (the library is built with the VGPR form of MFMA). Full tiles and
+// partial tiles run separate loop bodies (the lists hold the full tiles first),
+// so the unmasked body carries no mask code.
+//
+// Epilogue. O is normalised and stored straight from the accumulators: one
+// exchange between the two lane halves gives each lane 16 contiguous bytes of
+// its query's row.
 //
 // Masking (partial tiles only). For the 1-D Hilbert patterns each query's
 // allowed keys are one interval [lo, hi] computed once per lane; for the
@@ -54,6 +65,8 @@
 // tiles: neighbouring tiles share key/value tiles (a window is two query tiles;
 // a band overlaps its neighbour almost entirely), and the reuse stays in one
 // XCD's L2.
+#include <type_traits>
+
 #include "attn_common.h"
 
 namespace hla {
@@ -63,8 +76,9 @@ constexpr int BN = 64;
 constexpr float kRescaleSlack = 8.f;  // log2 units the softmax reference may lag the max
 // LDS ring depth. Three 16 KiB stages (d = 64) let three workgroups share a
 // CU's 160 KiB; with the launch bound below that is the occupancy that measured
-// fastest (four stages at two workgroups per CU, and two stages at four per CU,
-// were both slower).
+// fastest. Four stages at two workgroups per CU were slower, also with a
+// software-pipelined body that computes the next tile's scores on the matrix
+// cores during the current tile's softmax; so were two stages at four per CU.
 constexpr int kStages = 3;
 
 // Combine a value of lane l with lane l ^ 32 (the other half of a query's keys).
@@ -83,6 +97,15 @@ __device__ __forceinline__ int swz_v(int r) {
   return 2 * ((r >> 1) & 1);
 }
 
+// Per-row XOR swizzle of the 16-byte chunks of the Q tile in LDS: the operand
+// reads take eight consecutive rows at a time (one chunk each), which this
+// spreads over distinct bank groups.
+template <int D>
+__device__ __forceinline__ int swz_q(int r) {
+  if (D == 64) return r & 7;
+  return (r >> 1) & 3;
+}
+
 // Launch bound (second argument: minimum waves per SIMD): three waves, i.e. at
 // most 168 VGPRs per lane and three 4-wave workgroups per CU.
 template <int D, int NW>
@@ -95,10 +118,13 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
   constexpr int STAGE = 2 * TILE;             // K tile then V tile
   constexpr int CPW = BN * CPR / NT;          // 16-byte copies per thread per tile (K or V)
   constexpr int LPT = 2 * CPW;                // vector memory ops per wave per tile
+  constexpr int LQ = BM * CPR / NT;           // 16-byte copies per thread of the Q tile
   constexpr int NCH = D / 16;                 // MFMA steps over d for S^T
   constexpr int NDB = D / 32;                 // d blocks of O^T
-  static_assert(BN * CPR % NT == 0, "tile copies must split evenly over the workgroup");
-  static_assert((kStages - 2) * LPT < 64, "too many copies in flight for vmcnt");
+  static_assert(BN * CPR % NT == 0 && BM * CPR % NT == 0, "copies must split evenly");
+  static_assert(BM * D * 2 <= STAGE, "the Q tile must fit one stage");
+  static_assert(kStages == 3, "the loop keeps exactly one tile in flight behind the current");
+  static_assert(LPT < 64, "too many copies in flight for vmcnt");
 
   __shared__ __attribute__((aligned(16))) char lds[kStages * STAGE];
 
@@ -109,25 +135,21 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
   const int logical = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = logical / a.n_qtiles;
   const int qt = logical - bh * a.n_qtiles;
-  const int q0 = qt * BM;
   const int64_t slice = (int64_t)bh * a.N * D;
   const __bf16 *Q = static_cast<const __bf16 *>(a.q) + slice;
   const __bf16 *K = static_cast<const __bf16 *>(a.k) + slice;
   const __bf16 *V = static_cast<const __bf16 *>(a.v) + slice;
 
-  // This lane's query and its Q operand (d = half*D/2 + 8c + s for step c).
-  const int qpos = q0 + wave * 32 + col;
-  bf16x8 qop[NCH];
-#pragma unroll
-  for (int c = 0; c < NCH; ++c)
-    qop[c] = *reinterpret_cast<const bf16x8 *>(Q + (int64_t)qpos * D + half * (D / 2) + 8 * c);
+  // This lane's query. Its Q operand (d = half*D/2 + 8c + s for step c) is
+  // staged through LDS below.
+  const int qpos = qt * BM + wave * 32 + col;
 
   // Allowed-key region of this query (used on partial tiles only).
   const PatternArgs &P = a.pat;
   const Region R = region_of<true>(P, qpos);
 
-  // Tile lists, read through the scalar unit.
-  const int nf = sload(a.n_full + qt), np = sload(a.n_part + qt), ntot = nf + np;
+  // Tile lists, read through the scalar unit: the full tiles, then the partial.
+  const int nf = sload(a.n_full + qt), ntot = nf + sload(a.n_part + qt);
   const int32_t *frow = a.full_idx + (int64_t)qt * a.n_ktiles;
   const int32_t *prow = a.part_idx + (int64_t)qt * a.n_ktiles;
   auto tile_of = [&](int i) { return i < nf ? sload(frow + i) : sload(prow + i - nf); };
@@ -148,15 +170,10 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
     const __bf16 *Vt = V + (int64_t)kt * BN * D;
     char *base = lds + stage * STAGE;
 #pragma unroll
-    for (int j = 0; j < CPW; ++j) {
-      char *dk = base + (j * NW + wave) * 1024;
-      lds_dma16(Kt + koff[j], (lds_void *)dk);
-    }
+    for (int j = 0; j < CPW; ++j) lds_dma16(Kt + koff[j], lds_addr(base + (j * NW + wave) * 1024));
 #pragma unroll
-    for (int j = 0; j < CPW; ++j) {
-      char *dv = base + TILE + (j * NW + wave) * 1024;
-      lds_dma16(Vt + voff[j], (lds_void *)dv);
-    }
+    for (int j = 0; j < CPW; ++j)
+      lds_dma16(Vt + voff[j], lds_addr(base + TILE + (j * NW + wave) * 1024));
   };
 
   // LDS byte offsets (within a stage) of this lane's operand reads.
@@ -188,21 +205,51 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
   float l_run = 0.f;               // this lane's partial sum (its half of the keys)
   const float sl2 = a.scale_log2;
 
+  // Prologue: the Q tile goes into stage 2 (which the third key tile fills
+  // later), the first two key tiles into stages 0 and 1. Staging Q through LDS
+  // keeps every global load of the kernel a tracked ring copy: a Q operand
+  // loaded straight into registers would make the compiler wait for all copies
+  // in flight before its first use in the loop.
+  {
+    const __bf16 *Qt = Q + (int64_t)qt * BM * D;
+    char *base = lds + 2 * STAGE;
 #pragma unroll
-  for (int p = 0; p < kStages - 1; ++p)
-    if (p < ntot) issue_tile(tile_of(p), p);
+    for (int j = 0; j < LQ; ++j) {
+      const int p = (j * NW + wave) * 64 + lane;
+      const int r = p / CPR, cs = p % CPR;
+      lds_dma16(Qt + r * D + (cs ^ swz_q<D>(r)) * 8, lds_addr(base + (j * NW + wave) * 1024));
+    }
+  }
+  if (ntot > 0) issue_tile(tile_of(0), 0);
+  if (ntot > 1) issue_tile(tile_of(1), 1);
+  // Q and the first key tile are in; the second may still be in flight.
+  if (ntot > 1) wait_then_barrier<LPT>();
+  else wait_then_barrier<0>();
+  bf16x8 qop[NCH];
+  {
+    const int r = wave * 32 + col;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+      qop[c] = *reinterpret_cast<const bf16x8 *>(lds + 2 * STAGE + r * D * 2 +
+                                                 (((half * NCH + c) ^ swz_q<D>(r)) * 16));
+  }
 
-  for (int it = 0; it < ntot; ++it) {
-    const int stage = it % kStages;
-    // Wait for this wave's copies of tile `it`; copies of the tiles after it
-    // (at most kStages - 2 of them) may stay in flight.
-    wait_tiles_then_barrier<LPT, kStages - 2>(min(ntot - 1 - it, kStages - 2));
+  // One key tile: wait for its copies, refill the ring, then S^T, (mask),
+  // online softmax and O^T += V^T P^T. MASKED is a compile-time flag, so full
+  // and partial tiles run separate loop bodies and the unmasked path carries no
+  // mask code at all.
+  int stage = 0;
+  auto step = [&](int it, auto masked) {
+    // Wait for this wave's copies of tile `it`; the copies of tile it + 1 (the
+    // only one issued after it) may stay in flight.
+    if (it + 1 < ntot) wait_then_barrier<LPT>();
+    else wait_then_barrier<0>();
     // The stage refilled next was last read in iteration it - 1, which every
     // wave has finished (it is behind the barrier above).
-    if (it + kStages - 1 < ntot) issue_tile(tile_of(it + kStages - 1), (it + kStages - 1) % kStages);
-
+    const int nstage = stage == 0 ? 2 : stage - 1;  // (it + 2) % 3
+    if (it + 2 < ntot) issue_tile(tile_of(it + 2), nstage);
     const char *st = lds + stage * STAGE;
-    const int kt = tile_of(it);
+    stage = stage == 2 ? 0 : stage + 1;
 
     // S^T for the two 32-key blocks, independent accumulators interleaved.
     f32x16 s[2] = {f32x16{}, f32x16{}};
@@ -213,21 +260,21 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
         const bf16x8 kop = *reinterpret_cast<const bf16x8 *>(st + kaddr[kb][c]);
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[c], s[kb], 0, 0, 0);
       }
+    if constexpr (decltype(masked)::value) mask_blocks<2>(s, R, P, tile_of(it) * BN + 8 * half);
 
-    if (it >= nf) {  // partial tile: element mask
-      mask_blocks<2>(s, R, P, kt * BN + 8 * half);
+    // Online softmax in the log2 domain with a lazily moved reference: m_run
+    // only moves when a row's tile max exceeds it by more than kRescaleSlack, so
+    // the O / l rescale is rare; weights stay <= 2^kRescaleSlack and O and l
+    // always share the same reference.
+    float mq[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const f32x16 &sv = s[g >> 1];
+      const int o = 8 * (g & 1);
+      mq[g] = fmaxf(fmaxf(fmaxf(sv[o], sv[o + 1]), fmaxf(sv[o + 2], sv[o + 3])),
+                    fmaxf(fmaxf(sv[o + 4], sv[o + 5]), fmaxf(sv[o + 6], sv[o + 7])));
     }
-
-    // Online softmax in the log2 domain with a lazily moved reference: m_run only
-    // moves when a row's tile max exceeds it by more than kRescaleSlack, so the
-    // O / l rescale is rare; weights stay <= 2^kRescaleSlack and O and l always
-    // share the same reference.
-    float mx = s[0][0];
-#pragma unroll
-    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[0][v]);
-#pragma unroll
-    for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[1][v]);
-    mx = xhalf_max(mx);
+    const float mx = xhalf_max(fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3])));
     const float mt = mx * sl2;
     const bool grow = mt > m_run + kRescaleSlack;
     if (__ballot(grow)) {
@@ -240,18 +287,24 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
       m_run = m_new;
     }
     const float m_use = m_run == -__builtin_inff() ? 0.f : m_run;
-    // Row sums in fp32 from the unrounded weights; P goes to the PV product
-    // rounded to bf16.
+    // Row sums in fp32 from the unrounded weights (four partial sums); P goes
+    // to the PV product rounded to bf16.
     bf16x8 pop[4];
+    float lq[4];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int g = 0; g < 4; ++g) {
+      const f32x16 &sv = s[g >> 1];
+      const int o = 8 * (g & 1);
+      float acc = 0.f;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float pv = __builtin_amdgcn_exp2f(s[kb][v] * sl2 - m_use);
-        l_run += pv;
-        pop[kb * 2 + (v >> 3)][v & 7] = (__bf16)pv;
+      for (int e = 0; e < 8; ++e) {
+        const float pv = __builtin_amdgcn_exp2f(sv[o + e] * sl2 - m_use);
+        acc += pv;
+        pop[g][e] = (__bf16)pv;
       }
+      lq[g] = acc;
     }
+    l_run += (lq[0] + lq[1]) + (lq[2] + lq[3]);
 
     // O^T += V^T P^T over four 16-key steps, d blocks interleaved; V^T
     // operands read with the transposing LDS read right before use.
@@ -262,33 +315,37 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
         const bf16x8 vop = lds_read_tr16x2(st + vbase[db] + (16 * t) * D * 2, D * 2);
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[t], oacc[db], 0, 0, 0);
       }
-  }
+  };
+  for (int it = 0; it < nf; ++it) step(it, std::false_type{});
+  for (int it = nf; it < ntot; ++it) step(it, std::true_type{});
 
-  // Epilogue: normalise, stage O through LDS, write rows coalesced.
+  // Epilogue: normalise and store the rows straight from the accumulators. Lane
+  // (col, half) holds, per d block and 8-row group a, the four values
+  // d = 8a + 4half + 0..3 of query col; one exchange with lane col ^ 32 per pair
+  // of groups gives each lane eight consecutive values (16 bytes) to store.
   const float l_tot = xhalf_sum(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  wait_then_barrier<0>();  // no copy in flight; every wave is done reading K/V
-  constexpr int OS = D + 8;
-  __bf16 *Os = reinterpret_cast<__bf16 *>(lds) + wave * 32 * OS;
+  __bf16 *orow = static_cast<__bf16 *>(a.out) + slice + (int64_t)qpos * D;
 #pragma unroll
-  for (int db = 0; db < NDB; ++db) {
+  for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      bf16x4 o4;
+    for (int pr = 0; pr < 2; ++pr) {
+      bf16x4 x0, x1;
 #pragma unroll
-      for (int b = 0; b < 4; ++b) o4[b] = (__bf16)(oacc[db][4 * g + b] * inv);
-      *reinterpret_cast<bf16x4 *>(Os + col * OS + db * 32 + 8 * g + 4 * half) = o4;
+      for (int b = 0; b < 4; ++b) {
+        x0[b] = (__bf16)(oacc[db][8 * pr + b] * inv);
+        x1[b] = (__bf16)(oacc[db][8 * pr + 4 + b] * inv);
+      }
+      const uint2 u0 = __builtin_bit_cast(uint2, x0), u1 = __builtin_bit_cast(uint2, x1);
+      // half 0 keeps group 2pr and receives the partner's part of it; half 1
+      // keeps group 2pr + 1 and receives the partner's part of that.
+      const uint2 send = half ? u0 : u1;
+      uint2 recv;
+      recv.x = __shfl_xor(send.x, 32);
+      recv.y = __shfl_xor(send.y, 32);
+      const uint4 row = half ? uint4{recv.x, recv.y, u1.x, u1.y} : uint4{u0.x, u0.y, recv.x, recv.y};
+      *reinterpret_cast<uint4 *>(orow + db * 32 + 16 * pr + 8 * half) = row;
     }
-  }
-  __syncthreads();
-  __bf16 *O = static_cast<__bf16 *>(a.out) + slice + (int64_t)(q0 + wave * 32) * D;
-  constexpr int OCPR = D / 8;  // 16-byte chunks per row
-#pragma unroll
-  for (int i = lane; i < 32 * OCPR; i += 64) {
-    const int r = i / OCPR, c = i % OCPR;
-    *reinterpret_cast<uint4 *>(O + r * D + c * 8) =
-        *reinterpret_cast<const uint4 *>(Os + r * OS + c * 8);
-  }
   if (a.lse && half == 0) {
     const float ln2 = 0.69314718055994530942f;
     a.lse[(int64_t)bh * a.N + qpos] =

@@ -128,14 +128,6 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
   const __bf16 *G = static_cast<const __bf16 *>(a.dout) + slice;
 
   const int qpos = q0 + wave * 32 + col;
-  bf16x8 qop[NCH], gop[NCH];
-#pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    qop[c] = *reinterpret_cast<const bf16x8 *>(Q + (int64_t)qpos * D + half * (D / 2) + 8 * c);
-    gop[c] = *reinterpret_cast<const bf16x8 *>(G + (int64_t)qpos * D + half * (D / 2) + 8 * c);
-  }
-  const float2 rs = *reinterpret_cast<const float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qpos));
-  const float lse2 = rs.x, delta = rs.y;
 
   const PatternArgs &P = a.pat;
   const Region R = region_of<true>(P, qpos);
@@ -157,10 +149,11 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
     const __bf16 *Vt = V + (int64_t)kt * BN * D;
     char *base = lds + stage * STAGE;
 #pragma unroll
-    for (int j = 0; j < CPW; ++j) lds_dma16(Kt + off[j], (lds_void *)(base + (j * NW + wave) * 1024));
+    for (int j = 0; j < CPW; ++j)
+      lds_dma16(Kt + off[j], lds_addr(base + (j * NW + wave) * 1024));
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
-      lds_dma16(Vt + off[j], (lds_void *)(base + TILE + (j * NW + wave) * 1024));
+      lds_dma16(Vt + off[j], lds_addr(base + TILE + (j * NW + wave) * 1024));
   };
 
   int raddr[2][NCH];
@@ -182,6 +175,18 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
 #pragma unroll
   for (int p = 0; p < kStagesDq - 1; ++p)
     if (p < ntot) issue_tile(tile_of(p), p);
+  // The wave's own q and dout rows and row statistics, loaded after the first
+  // copies so that both latencies overlap; one wait the compiler can see then
+  // covers all of them, so it inserts no wait of its own inside the loop.
+  bf16x8 qop[NCH], gop[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    qop[c] = *reinterpret_cast<const bf16x8 *>(Q + (int64_t)qpos * D + half * (D / 2) + 8 * c);
+    gop[c] = *reinterpret_cast<const bf16x8 *>(G + (int64_t)qpos * D + half * (D / 2) + 8 * c);
+  }
+  const float2 rs = *reinterpret_cast<const float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qpos));
+  const float lse2 = rs.x, delta = rs.y;
+  wait_vmem_all();
 
   for (int it = 0; it < ntot; ++it) {
     const int stage = it % kStagesDq;
@@ -279,12 +284,6 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   const float *S = a.stats + 2 * (int64_t)bh * a.N;
 
   const int kpos = k0 + kb * 32 + col;
-  bf16x8 kop[NCH], vop[NCH];
-#pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    kop[c] = *reinterpret_cast<const bf16x8 *>(K + (int64_t)kpos * D + half * (D / 2) + 8 * c);
-    vop[c] = *reinterpret_cast<const bf16x8 *>(V + (int64_t)kpos * D + half * (D / 2) + 8 * c);
-  }
 
   const PatternArgs &P = a.pat;
   const Region R = region_of<false>(P, kpos);
@@ -306,13 +305,14 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
     const __bf16 *Gt = G + (int64_t)qt * BMQ * D;
     char *base = lds + stage * STAGE;
 #pragma unroll
-    for (int j = 0; j < CPW; ++j) lds_dma16(Qt + off[j], (lds_void *)(base + (j * 4 + wave) * 1024));
+    for (int j = 0; j < CPW; ++j)
+      lds_dma16(Qt + off[j], lds_addr(base + (j * 4 + wave) * 1024));
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
-      lds_dma16(Gt + off[j], (lds_void *)(base + QT + (j * 4 + wave) * 1024));
+      lds_dma16(Gt + off[j], lds_addr(base + QT + (j * 4 + wave) * 1024));
     if (lane < SL)
       lds_dma16(S + 2 * ((int64_t)qt * BMQ) + 4 * (wave * SL + lane),
-                (lds_void *)(base + SOFF + wave * SL * 16));
+                      lds_addr(base + SOFF + wave * SL * 16));
   };
 
   int raddr[QB][NCH];
@@ -335,6 +335,16 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   const float sl2 = a.scale_log2;
 
   if (ntot > 0) issue_tile(tile_of(0), 0);
+  // The wave's own k and v rows, loaded after the first copy so that both
+  // latencies overlap; one wait the compiler can see then covers both, so it
+  // inserts no wait of its own inside the loop.
+  bf16x8 kop[NCH], vop[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    kop[c] = *reinterpret_cast<const bf16x8 *>(K + (int64_t)kpos * D + half * (D / 2) + 8 * c);
+    vop[c] = *reinterpret_cast<const bf16x8 *>(V + (int64_t)kpos * D + half * (D / 2) + 8 * c);
+  }
+  wait_vmem_all();
 
   for (int it = 0; it < ntot; ++it) {
     const int stage = it % kStagesKv;

@@ -164,16 +164,39 @@ __device__ __forceinline__ int row_perm(int i) {
   return 16 * (a >> 1) + 8 * g + 4 * (a & 1) + b;
 }
 
+// LDS byte address of a pointer into __shared__ memory.
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char *)p;
+}
+
 // ---------------------------------------------------------------------------
-// gfx950 LDS DMA (16 bytes per lane; lane l lands at dst + 16 l) and the
-// transposing 64-bit LDS read. Only the device pass may see these builtins:
-// the host pass of the HIP compiler rejects them silently and then emits no
+// gfx950 LDS DMA (16 bytes per lane; lane l lands at dst + 16 l), issued from
+// inline assembly (M0 = the wave's LDS destination, then the load), and the
+// transposing 64-bit LDS read. Only the device pass may see these: the host
+// pass of the HIP compiler rejects the builtins silently and then emits no
 // launch stub for the kernel that calls them.
-__device__ __forceinline__ void lds_dma16(const void *src, lds_void *dst) {
+//
+// The compiler cannot see this copy, so it inserts no wait of
+// its own for it: a kernel that uses it must order every LDS read of the copied
+// data after the copy itself - an explicit vmcnt wait for the wave's own copies
+// followed by a workgroup barrier. In exchange the compiler's wait insertion no
+// longer treats later LDS reads as possibly overlapping a copy in flight (for
+// the transposing read below it would otherwise wait for every outstanding
+// copy, draining a copy ring on every tile). dst must be wave-uniform.
+// M0 is a reserved register, so the compiler does not preserve a value of its
+// own across this statement; nothing else in these kernels uses M0 (the
+// compiler's own LDS DMA builtin would, which is why it is not used here).
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_dma16(const void *src, uint32_t dst) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(dst))
+               : "memory", "m0");
 #endif
 }
+#pragma clang diagnostic pop
 __device__ __forceinline__ i16x4 lds_read_tr16(const char *p) {
 #if defined(__HIP_DEVICE_COMPILE__)
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p);
@@ -186,6 +209,15 @@ __device__ __forceinline__ bf16x8 lds_read_tr16x2(const char *p, int row_bytes) 
   const i16x4 lo4 = lds_read_tr16(p);
   const i16x4 hi4 = lds_read_tr16(p + 4 * row_bytes);
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// Wait for every vector memory operation of this wave, as an instruction the
+// compiler's own wait insertion sees (it then knows its loads have landed). The
+// empty statement in front keeps the compiler from scheduling loads written
+// before this call after the wait.
+__device__ __forceinline__ void wait_vmem_all() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0); expcnt, lgkmcnt unconstrained
 }
 
 // Wait until this wave's LDS reads are done and at most N of its vector memory

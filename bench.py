@@ -259,7 +259,8 @@ class LayerPipeline:
         return 2 * w.B * w.N * w.C * 2 + 4 * w.N
 
 
-ATTN_SOURCES = ("paper_2511_05832_amd/csrc/attn_bf16.hip", "paper_2511_05832_amd/csrc/hla_internal.h")
+ATTN_SOURCES = ("paper_2511_05832_amd/csrc/attn_bf16.hip", "paper_2511_05832_amd/csrc/attn_common.h",
+                "paper_2511_05832_amd/csrc/hla_internal.h")
 
 
 def measured_traffic(workload_name):

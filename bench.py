@@ -95,19 +95,25 @@ class Timer:
 
 
 class AttnPipeline:
-    def __init__(self, w: W.AttnWorkload, hla):
+    """One step of an attention workload. Hilbert patterns either reorder with
+    separate gather and scatter passes around hla_attn_fwd (composed), or hand the
+    grid-ordered tensors and the Hilbert order to hla_attn_fwd_perm, which does the
+    reordering inside its loads and stores (fused)."""
+
+    def __init__(self, w: W.AttnWorkload, hla, fused: bool = False):
         self.w, self.hla = w, hla
         pat = w.pattern
         self.hilbert = pat.hilbert
+        self.fused = fused and self.hilbert
         B, Hh, N, d = w.B, w.heads, w.N, w.d
         tensor_bytes = B * Hh * N * d * esize(w.dtype)
-        set_bytes = tensor_bytes * (7 if self.hilbert else 4)
+        set_bytes = tensor_bytes * (7 if self.hilbert and not self.fused else 4)
         self.nsets = max(2, min(64, math.ceil(3 * MALL_BYTES / set_bytes)))
         q, k, v = W.workload_inputs(w)
         self.sets = []
         for i in range(self.nsets):
             s = {"q": q.cuda(), "k": k.cuda(), "v": v.cuda()}
-            if self.hilbert:
+            if self.hilbert and not self.fused:
                 for n in ("qh", "kh", "vh", "oh"):
                     s[n] = torch.empty_like(s["q"])
             s["o"] = torch.empty_like(s["q"])
@@ -121,6 +127,15 @@ class AttnPipeline:
 
     def step(self, i):
         hla, w, s, T = self.hla, self.w, self.sets[i % self.nsets], self.timer
+        if self.fused:
+            with T.stage("hilbert"):
+                hla.hilbert_perm(w.pattern.H, w.pattern.W, out=(self.order, self.rank))
+            with T.stage("mask"):
+                self.mask.build()
+            with T.stage("attn"):
+                hla.attn_fwd_perm(s["q"], s["k"], s["v"], self.order, self.mask, w.scale,
+                                  out=s["o"], lse=s["lse"])
+            return
         if self.hilbert:
             with T.stage("hilbert"):
                 hla.hilbert_perm(w.pattern.H, w.pattern.W, out=(self.order, self.rank))
@@ -263,11 +278,12 @@ ATTN_SOURCES = ("paper_2511_05832_amd/csrc/attn_bf16.hip", "paper_2511_05832_amd
                 "paper_2511_05832_amd/csrc/hla_internal.h")
 
 
-def measured_traffic(workload_name):
+def measured_traffic(workload_name, kernel="attn_fwd"):
     """HBM bytes per attention dispatch from the committed rocprofv3 counter summary
-    for this workload, or None if there is none or the kernel source changed since."""
+    for this workload and kernel (attn_fwd or attn_fwd_perm), or None if there is
+    none or the kernel source changed since."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"attn_fwd_bf16_{workload_name}_traffic.txt")
+    path = os.path.join(ROOT, "profiles", f"{kernel}_bf16_{workload_name}_traffic.txt")
     if not os.path.exists(path):
         return None
     fields = {}
@@ -286,8 +302,8 @@ def measured_traffic(workload_name):
         return None
 
 
-def make_pipeline(w, hla):
-    return LayerPipeline(w, hla) if isinstance(w, W.LayerWorkload) else AttnPipeline(w, hla)
+def make_pipeline(w, hla, fused=False):
+    return LayerPipeline(w, hla) if isinstance(w, W.LayerWorkload) else AttnPipeline(w, hla, fused)
 
 
 def capture_step_graphs(pipe):
@@ -506,6 +522,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-backward", action="store_true",
                     help="skip timing the backward pass of the workload")
+    ap.add_argument("--step", default="fused", choices=["fused", "composed", "composed-only"],
+                    help="which step of a Hilbert workload the headline value times: the "
+                         "reordering fused into the attention (hla_attn_fwd_perm) or separate "
+                         "gather / attention / scatter calls; the other is reported beside it "
+                         "(composed-only: skip the fused step)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="before the steps, time a plain device-to-device copy of this many MiB "
                          "(a kernel of known traffic, to calibrate HBM byte counters)")
@@ -535,13 +556,26 @@ def main():
     w = W.WORKLOADS[args.workload]
     pipe = make_pipeline(w, hla)
     timing = run_timed(pipe, args.steps, args.warmup)
-    ms = timing[0]
     res = summarize(pipe, timing)
-    print(f"[bench] {w.name}: {json.dumps(res)}", file=sys.stderr, flush=True)
+    print(f"[bench] {w.name} (composed): {json.dumps(res)}", file=sys.stderr, flush=True)
     bwd = None
     if isinstance(w, W.AttnWorkload) and not args.no_backward:
         bwd = time_backward(pipe, args.steps, args.warmup)
         print(f"[bench] {w.name} backward: {json.dumps(bwd)}", file=sys.stderr, flush=True)
+    # The same step with the reordering fused into the attention (Hilbert patterns).
+    res_fused = None
+    if isinstance(w, W.AttnWorkload) and w.pattern.hilbert and args.step != "composed-only":
+        del pipe
+        torch.cuda.empty_cache()
+        fpipe = make_pipeline(w, hla, fused=True)
+        res_fused = summarize(fpipe, run_timed(fpipe, args.steps, args.warmup))
+        print(f"[bench] {w.name} (fused): {json.dumps(res_fused)}", file=sys.stderr, flush=True)
+        pipe = fpipe   # the algorithmic figures below depend on the workload only
+    res_composed = res
+    if args.step == "fused" and res_fused:
+        res = res_fused
+    ms = res["ms_per_step"]
+    attn_kernel = "attn_fwd_perm" if res is res_fused else "attn_fwd"
 
     compare = args.compare
     if compare is None and not args.copy_mib:
@@ -578,16 +612,16 @@ def main():
     if t_hbm >= t_mfma:
         achieved = pipe.attn_bytes() / attn_s / 1e9
         roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(w.name),
-                    "kernel": "attn_fwd",
+                    "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(w.name, attn_kernel),
+                    "kernel": attn_kernel,
                     "algorithmic_bytes": pipe.attn_bytes(),
                     "mfma_frac": res["attn_tile_tflops"] / (BF16_PEAK_TFLOPS if is_bf16 else FP32_PEAK_TFLOPS)}
     else:
         peak = BF16_PEAK_TFLOPS if is_bf16 else FP32_PEAK_TFLOPS
         roofline = {"bound": "mfma", "achieved": res["attn_tile_tflops"], "peak": peak,
                     "unit": "TFLOP/s", "frac": res["attn_tile_tflops"] / peak,
-                    "traffic": measured_traffic(w.name),
-                    "kernel": "attn_fwd", "algorithmic_flops": flops,
+                    "traffic": measured_traffic(w.name, attn_kernel),
+                    "kernel": attn_kernel, "algorithmic_flops": flops,
                     "hbm_frac": pipe.attn_bytes() / attn_s / 1e9 / HBM_PEAK_GBS}
 
     cpu = None
@@ -613,15 +647,28 @@ def main():
         "config": {"workload": w.name, "description": w.description,
                    "B": w.B, "heads": w.heads, "tokens": w.N, "head_dim": w.d,
                    "tile": [w.tile_m, w.tile_n], "parallelism": "single-gpu"},
+        "step": ("Hilbert index, tile lists, attention with the reordering fused in "
+                 "(hla_attn_fwd_perm)" if attn_kernel == "attn_fwd_perm" else
+                 "Hilbert index, gather of q/k/v, tile lists, attention, scatter of out"
+                 if getattr(getattr(w, "pattern", None), "hilbert", False) else
+                 "tile lists, attention" if isinstance(w, W.AttnWorkload) else
+                 "gather, QKV projection, tile lists, attention, output projection, scatter"),
         "attn_ms_per_call": res["attn_ms"],
         "attn_tflops_nonempty_tiles": res["attn_tile_tflops"],
         "attn_pct_bf16_peak": res["attn_pct_peak"],
-        "perm_gbs": {"gather": res.get("gather_gbs"), "scatter": res.get("scatter_gbs")},
+        "perm_gbs": {"gather": res_composed.get("gather_gbs"),
+                     "scatter": res_composed.get("scatter_gbs")},
         "stages_ms": res["stages_ms"],
         "tiles": {"full": res["tiles_full"], "partial": res["tiles_partial"]},
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    other = res_composed if res is res_fused else res_fused
+    if other:
+        line["composed_step" if other is res_composed else "fused_step"] = {
+            "ms_per_step": other["ms_per_step"], "ms_per_step_eager": other["ms_per_step_eager"],
+            "value": flops / (other["ms_per_step"] * 1e-3) / 1e12,
+            "attn_ms_per_call": other["attn_ms"], "stages_ms": other["stages_ms"]}
     if bwd:
         line["backward"] = bwd
     if cmp_res:

@@ -187,6 +187,27 @@ hla_status hla_attn_fwd(const void *q, const void *k, const void *v,
                         hla_dtype dtype, float scale, hla_stream_t stream);
 
 /*
+ * The same attention forward with the reordering fused into its loads and
+ * stores, so that no separate gather or scatter pass is needed (the paper's
+ * "reshape" step, Sec. 4.2, done inside the attention instead of around it).
+ * q, k, v, out are stored in grid order (row-major tokens); sequence position i
+ * (the position the mask's pattern refers to) is row order[i]:
+ *   out[b,h,order[i],:] = hla_attn_fwd's out[b,h,i,:] for
+ *                         q'[b,h,i,:] = q[b,h,order[i],:] (likewise k', v'),
+ *   lse[b,h,order[i]]   = the same row's lse.
+ * The results equal hla_gather -> hla_attn_fwd -> hla_scatter bit for bit.
+ * order: device int32[N], a permutation of [0, N) (not checked; an out-of-range
+ * entry is undefined behaviour), 16-byte aligned, not overlapping any tensor
+ * (typically hla_hilbert_perm's order). Other arguments, support and errors as
+ * hla_attn_fwd.
+ */
+hla_status hla_attn_fwd_perm(const void *q, const void *k, const void *v,
+                             const int32_t *order, const hla_block_mask *mask,
+                             void *out, float *lse, int64_t B, int64_t heads,
+                             int64_t N, int64_t d, hla_dtype dtype, float scale,
+                             hla_stream_t stream);
+
+/*
  * Block-sparse attention backward: the gradients of hla_attn_fwd's out with
  * respect to q, k and v for an upstream gradient dout, over the same tiles as
  * the forward (empty tiles skipped, partial tiles masked; the paper times this

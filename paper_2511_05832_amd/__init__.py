@@ -10,6 +10,7 @@ fallback path.
     mask = build_block_mask(pattern, 128, 64)   # full / partial / empty tile lists
     out, lse = attn_fwd(qh, kh, vh, mask, scale)
     o = scatter(out, order)                     # back to row-major
+    o, lse_rm = attn_fwd_perm(q, k, v, order, mask, scale)   # the same, reordering fused
 
     mask = build_block_mask(pattern, 128, 64, columns=True)   # + per-column lists
     dq, dk, dv = attn_bwd(qh, kh, vh, out, dout, lse, mask, scale)
@@ -27,7 +28,8 @@ from typing import Optional, Tuple
 import torch
 
 __all__ = ["HLAError", "lib", "hilbert_perm", "gather", "scatter", "block_mask_dims",
-           "build_block_mask", "BlockMask", "attn_fwd", "attn_bwd", "qkv_proj", "out_proj",
+           "build_block_mask", "BlockMask", "attn_fwd", "attn_fwd_perm", "attn_bwd", "qkv_proj",
+           "out_proj",
            "PATTERN_IDS", "LIB_PATH", "EXPORTED"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhla.so")
@@ -46,7 +48,8 @@ HLA_OK, HLA_ERR_INVALID_ARG, HLA_ERR_UNSUPPORTED, HLA_ERR_HIP = 0, 1, 2, 3
 HLA_F32, HLA_BF16 = 0, 1
 
 EXPORTED = ("hla_hilbert_perm", "hla_gather", "hla_scatter", "hla_block_mask_dims",
-            "hla_build_block_mask", "hla_attn_fwd", "hla_attn_bwd", "hla_qkv_proj", "hla_out_proj",
+            "hla_build_block_mask", "hla_attn_fwd", "hla_attn_fwd_perm", "hla_attn_bwd",
+            "hla_qkv_proj", "hla_out_proj",
             "hla_last_error", "hla_version")
 
 
@@ -99,6 +102,8 @@ def lib() -> ctypes.CDLL:
             "hla_build_block_mask": [ctypes.POINTER(BlockMaskStruct), vp],
             "hla_attn_fwd": [vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp,
                              i64, i64, i64, i64, ctypes.c_int, f32, vp],
+            "hla_attn_fwd_perm": [vp, vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp,
+                                  i64, i64, i64, i64, ctypes.c_int, f32, vp],
             "hla_attn_bwd": [vp, vp, vp, vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp, vp,
                              vp, i64, i64, i64, i64, ctypes.c_int, f32, vp],
             "hla_qkv_proj": [vp, vp, vp, vp, vp, i64, i64, i64, i64, vp],
@@ -271,10 +276,7 @@ def build_block_mask(pattern, tile_m: int, tile_n: int, device="cuda",
     return BlockMask(pattern, tile_m, tile_n, device, columns).build()
 
 
-def attn_fwd(q, k, v, mask: BlockMask, scale: Optional[float] = None,
-             out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
-             with_lse: bool = True):
-    """Block-sparse attention forward (hla_attn_fwd). Returns (out, lse or None)."""
+def _attn_fwd_args(q, k, v, scale, out, lse, with_lse):
     for t, n in ((q, "q"), (k, "k"), (v, "v")):
         _require(t, n)
     if q.dim() != 4 or k.shape != q.shape or v.shape != q.shape:
@@ -292,8 +294,34 @@ def attn_fwd(q, k, v, mask: BlockMask, scale: Optional[float] = None,
         lse = torch.empty((B, Hh, N), dtype=torch.float32, device=q.device)
     elif lse is not None:
         _require(lse, "lse")
+    return B, Hh, N, d, float(scale), out, lse
+
+
+def attn_fwd(q, k, v, mask: BlockMask, scale: Optional[float] = None,
+             out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+             with_lse: bool = True):
+    """Block-sparse attention forward (hla_attn_fwd). Returns (out, lse or None)."""
+    B, Hh, N, d, scale, out, lse = _attn_fwd_args(q, k, v, scale, out, lse, with_lse)
     _check(lib().hla_attn_fwd(_ptr(q), _ptr(k), _ptr(v), ctypes.byref(mask.struct), _ptr(out),
-                              _ptr(lse), B, Hh, N, d, _dtype_code(q), float(scale), _stream(q)))
+                              _ptr(lse), B, Hh, N, d, _dtype_code(q), scale, _stream(q)))
+    return out, lse
+
+
+def attn_fwd_perm(q, k, v, order, mask: BlockMask, scale: Optional[float] = None,
+                  out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                  with_lse: bool = True):
+    """Attention forward on grid-ordered q, k, v with the reordering fused in
+    (hla_attn_fwd_perm): sequence position i is row order[i]; out and lse come
+    back in grid order. Returns (out, lse or None)."""
+    _require(order, "order")
+    if order.dtype != torch.int32:
+        raise HLAError(HLA_ERR_INVALID_ARG, "order must be int32")
+    B, Hh, N, d, scale, out, lse = _attn_fwd_args(q, k, v, scale, out, lse, with_lse)
+    if order.numel() != N:
+        raise HLAError(HLA_ERR_INVALID_ARG, f"order has {order.numel()} entries, expected N = {N}")
+    _check(lib().hla_attn_fwd_perm(_ptr(q), _ptr(k), _ptr(v), _ptr(order), ctypes.byref(mask.struct),
+                                   _ptr(out), _ptr(lse), B, Hh, N, d, _dtype_code(q), scale,
+                                   _stream(q)))
     return out, lse
 
 

@@ -108,7 +108,14 @@ __device__ __forceinline__ int swz_q(int r) {
 
 // Launch bound (second argument: minimum waves per SIMD): three waves, i.e. at
 // most 168 VGPRs per lane and three 4-wave workgroups per CU.
-template <int D, int NW>
+//
+// GATHER: the tensors are stored in grid (row-major) order and sequence position
+// i lives in row a.order[i] (the reordering fused into the loads and stores).
+// Each key tile's 64 row indices are copied into LDS one step ahead of its K/V
+// copies (by the first wave; issued before that step's K/V copies, so the same
+// vmcnt counts cover them), and the Q tile's indices in the prologue, which also
+// give each lane the row its output goes to.
+template <int D, int NW, bool GATHER>
 __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
     attn_fwd_bf16(AttnArgs a) {
   constexpr int BM = 32 * NW;
@@ -125,8 +132,15 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
   static_assert(BM * D * 2 <= STAGE, "the Q tile must fit one stage");
   static_assert(kStages == 3, "the loop keeps exactly one tile in flight behind the current");
   static_assert(LPT < 64, "too many copies in flight for vmcnt");
+  // Row-index area (GATHER): the Q tile's BM indices, then four slots of BN
+  // indices for key tiles (slot i % 4 holds tile list entry i).
+  constexpr int IDXQ = kStages * STAGE;
+  constexpr int IDXK = IDXQ + BM * 4;
+  constexpr int LDSB = GATHER ? IDXK + 4 * BN * 4 : kStages * STAGE;
 
-  __shared__ __attribute__((aligned(16))) char lds[kStages * STAGE];
+  __shared__ __attribute__((aligned(16))) char lds[LDSB];
+  const int32_t *idx_q = reinterpret_cast<const int32_t *>(lds + IDXQ);
+  auto idx_k = [&](int i) { return reinterpret_cast<const int32_t *>(lds + IDXK + (i & 3) * BN * 4); };
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -157,23 +171,46 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
   // Per-thread source offsets (elements, within a tile) of this thread's K and V
   // chunk copies: LDS slot p = (j*NW + wave)*64 + lane holds row p / CPR, chunk
   // (p % CPR) ^ swizzle(row).
-  int koff[CPW], voff[CPW];
+  // (GATHER: row r of a tile is the row named by its index slot instead.)
+  int krow[CPW], kch[CPW], vch[CPW];
 #pragma unroll
   for (int j = 0; j < CPW; ++j) {
     const int p = (j * NW + wave) * 64 + lane;
     const int r = p / CPR, cs = p % CPR;
-    koff[j] = r * D + (cs ^ swz_k<D>(r)) * 8;
-    voff[j] = r * D + (cs ^ swz_v<D>(r)) * 8;
+    krow[j] = r;
+    kch[j] = (cs ^ swz_k<D>(r)) * 8;
+    vch[j] = (cs ^ swz_v<D>(r)) * 8;
   }
-  auto issue_tile = [&](int kt, int stage) {
-    const __bf16 *Kt = K + (int64_t)kt * BN * D;
-    const __bf16 *Vt = V + (int64_t)kt * BN * D;
+  // Copies of the K/V tile of list entry i into a ring stage.
+  auto issue_tile = [&](int i, int stage) {
     char *base = lds + stage * STAGE;
+    const __bf16 *Kt, *Vt;
+    int64_t roff[CPW];
+    if constexpr (GATHER) {
+      const int32_t *rows = idx_k(i);
+      Kt = K;
+      Vt = V;
 #pragma unroll
-    for (int j = 0; j < CPW; ++j) lds_dma16(Kt + koff[j], lds_addr(base + (j * NW + wave) * 1024));
+      for (int j = 0; j < CPW; ++j) roff[j] = (int64_t)rows[krow[j]] * D;
+    } else {
+      const int kt = tile_of(i);
+      Kt = K + (int64_t)kt * BN * D;
+      Vt = V + (int64_t)kt * BN * D;
+#pragma unroll
+      for (int j = 0; j < CPW; ++j) roff[j] = krow[j] * D;
+    }
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
-      lds_dma16(Vt + voff[j], lds_addr(base + TILE + (j * NW + wave) * 1024));
+      lds_dma16(Kt + roff[j] + kch[j], lds_addr(base + (j * NW + wave) * 1024));
+#pragma unroll
+    for (int j = 0; j < CPW; ++j)
+      lds_dma16(Vt + roff[j] + vch[j], lds_addr(base + TILE + (j * NW + wave) * 1024));
+  };
+  // GATHER: the row indices of list entry i (16 bytes per lane of the first
+  // wave) into its slot.
+  auto issue_idx = [&](int i) {
+    if (wave == 0 && lane < BN / 4)
+      lds_dma16(a.order + (int64_t)tile_of(i) * BN + 4 * lane, lds_addr(lds + IDXK + (i & 3) * BN * 4));
   };
 
   // LDS byte offsets (within a stage) of this lane's operand reads.
@@ -210,18 +247,27 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
   // keeps every global load of the kernel a tracked ring copy: a Q operand
   // loaded straight into registers would make the compiler wait for all copies
   // in flight before its first use in the loop.
+  if constexpr (GATHER) {
+    // Row indices of the Q tile and of the first three key tiles, first.
+    if (wave == 0 && lane < BM / 4)
+      lds_dma16(a.order + (int64_t)qt * BM + 4 * lane, lds_addr(lds + IDXQ));
+#pragma unroll
+    for (int i = 0; i < 3; ++i)
+      if (i < ntot) issue_idx(i);
+    wait_then_barrier<0>();
+  }
   {
-    const __bf16 *Qt = Q + (int64_t)qt * BM * D;
     char *base = lds + 2 * STAGE;
 #pragma unroll
     for (int j = 0; j < LQ; ++j) {
       const int p = (j * NW + wave) * 64 + lane;
       const int r = p / CPR, cs = p % CPR;
-      lds_dma16(Qt + r * D + (cs ^ swz_q<D>(r)) * 8, lds_addr(base + (j * NW + wave) * 1024));
+      const int64_t row = GATHER ? (int64_t)idx_q[r] : (int64_t)qt * BM + r;
+      lds_dma16(Q + row * D + (cs ^ swz_q<D>(r)) * 8, lds_addr(base + (j * NW + wave) * 1024));
     }
   }
-  if (ntot > 0) issue_tile(tile_of(0), 0);
-  if (ntot > 1) issue_tile(tile_of(1), 1);
+  if (ntot > 0) issue_tile(0, 0);
+  if (ntot > 1) issue_tile(1, 1);
   // Q and the first key tile are in; the second may still be in flight.
   if (ntot > 1) wait_then_barrier<LPT>();
   else wait_then_barrier<0>();
@@ -247,7 +293,12 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
     // The stage refilled next was last read in iteration it - 1, which every
     // wave has finished (it is behind the barrier above).
     const int nstage = stage == 0 ? 2 : stage - 1;  // (it + 2) % 3
-    if (it + 2 < ntot) issue_tile(tile_of(it + 2), nstage);
+    // (GATHER: the indices of entry it + 2 arrived with the wait above, those of
+    // it + 3 go out first.)
+    if constexpr (GATHER) {
+      if (it + 3 < ntot) issue_idx(it + 3);
+    }
+    if (it + 2 < ntot) issue_tile(it + 2, nstage);
     const char *st = lds + stage * STAGE;
     stage = stage == 2 ? 0 : stage + 1;
 
@@ -325,7 +376,8 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
   // of groups gives each lane eight consecutive values (16 bytes) to store.
   const float l_tot = xhalf_sum(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  __bf16 *orow = static_cast<__bf16 *>(a.out) + slice + (int64_t)qpos * D;
+  const int64_t out_row = GATHER ? (int64_t)idx_q[wave * 32 + col] : (int64_t)qpos;
+  __bf16 *orow = static_cast<__bf16 *>(a.out) + slice + out_row * D;
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -348,7 +400,7 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
     }
   if (a.lse && half == 0) {
     const float ln2 = 0.69314718055994530942f;
-    a.lse[(int64_t)bh * a.N + qpos] =
+    a.lse[(int64_t)bh * a.N + out_row] =
         l_tot > 0.f ? (m_run + __builtin_amdgcn_logf(l_tot)) * ln2 : -__builtin_inff();
   }
 }
@@ -356,7 +408,10 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
 template <int D, int NW>
 hipError_t launch(const AttnArgs &a, hipStream_t s) {
   const int64_t blocks = (int64_t)a.BH * a.n_qtiles;
-  hipLaunchKernelGGL((attn_fwd_bf16<D, NW>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
+  if (a.order)
+    hipLaunchKernelGGL((attn_fwd_bf16<D, NW, true>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_fwd_bf16<D, NW, false>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
   return hipGetLastError();
 }
 

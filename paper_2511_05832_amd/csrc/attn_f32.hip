@@ -6,7 +6,9 @@
 // fp32 matrix mode, and fp32 vector FMA runs at the same 157 TFLOP/s as fp32
 // MFMA, so each thread owns one query row and does plain FMAs. K and V tiles are
 // staged in LDS and read as broadcasts (every lane of a wave reads the same key
-// row at the same time).
+// row at the same time). GATHER: the tensors are stored in grid order and
+// sequence position i lives in row a.order[i] (reordering fused into the loads
+// and stores).
 #include "attn_common.h"
 
 namespace hla {
@@ -15,7 +17,7 @@ namespace {
 constexpr int BN = 64;
 constexpr int CH = 16;  // keys per online-softmax step
 
-template <int D, int BM>
+template <int D, int BM, bool GATHER>
 __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) float Ks[BN * D];
   __shared__ __attribute__((aligned(16))) float Vs[BN * D];
@@ -30,10 +32,11 @@ __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
   const float *K = static_cast<const float *>(a.k) + slice;
   const float *V = static_cast<const float *>(a.v) + slice;
 
+  const int64_t qrow = GATHER ? (int64_t)a.order[qpos] : (int64_t)qpos;
   float q[D], acc[D];
 #pragma unroll
   for (int i = 0; i < D; i += 4) {
-    const float4 t = *reinterpret_cast<const float4 *>(Q + (int64_t)qpos * D + i);
+    const float4 t = *reinterpret_cast<const float4 *>(Q + qrow * D + i);
     q[i] = t.x; q[i + 1] = t.y; q[i + 2] = t.z; q[i + 3] = t.w;
   }
 #pragma unroll
@@ -52,11 +55,11 @@ __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
     const bool masked = it >= nf;
     const int kt = masked ? prow[it - nf] : frow[it];
     __syncthreads();
-    const float *Kt = K + (int64_t)kt * BN * D;
-    const float *Vt = V + (int64_t)kt * BN * D;
     for (int i = tid; i < BN * D / 4; i += BM) {
-      reinterpret_cast<float4 *>(Ks)[i] = reinterpret_cast<const float4 *>(Kt)[i];
-      reinterpret_cast<float4 *>(Vs)[i] = reinterpret_cast<const float4 *>(Vt)[i];
+      const int r = i / (D / 4), c4 = i % (D / 4);
+      const int64_t row = GATHER ? (int64_t)a.order[kt * BN + r] : (int64_t)kt * BN + r;
+      reinterpret_cast<float4 *>(Ks)[i] = reinterpret_cast<const float4 *>(K + row * D)[c4];
+      reinterpret_cast<float4 *>(Vs)[i] = reinterpret_cast<const float4 *>(V + row * D)[c4];
     }
     __syncthreads();
     for (int j0 = 0; j0 < BN; j0 += CH) {
@@ -94,14 +97,14 @@ __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
   }
 
   const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-  float *O = static_cast<float *>(a.out) + slice + (int64_t)qpos * D;
+  float *O = static_cast<float *>(a.out) + slice + qrow * D;
 #pragma unroll
   for (int i = 0; i < D; i += 4)
     *reinterpret_cast<float4 *>(O + i) =
         make_float4(acc[i] * inv, acc[i + 1] * inv, acc[i + 2] * inv, acc[i + 3] * inv);
   if (a.lse) {
     const float ln2 = 0.69314718055994530942f;
-    a.lse[(int64_t)bh * a.N + qpos] =
+    a.lse[(int64_t)bh * a.N + qrow] =
         l_run > 0.f ? (m_run + __builtin_amdgcn_logf(l_run)) * ln2 : -__builtin_inff();
   }
 }
@@ -109,7 +112,10 @@ __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
 template <int D, int BM>
 hipError_t launch(const AttnArgs &a, hipStream_t s) {
   const int64_t blocks = (int64_t)a.BH * a.n_qtiles;
-  hipLaunchKernelGGL((attn_fwd_f32<D, BM>), dim3((uint32_t)blocks), dim3(BM), 0, s, a);
+  if (a.order)
+    hipLaunchKernelGGL((attn_fwd_f32<D, BM, true>), dim3((uint32_t)blocks), dim3(BM), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_fwd_f32<D, BM, false>), dim3((uint32_t)blocks), dim3(BM), 0, s, a);
   return hipGetLastError();
 }
 

@@ -234,9 +234,10 @@ bool overlaps(const void *a, int64_t na, const void *b, int64_t nb) {
 
 extern "C" {
 
-hla_status hla_attn_fwd(const void *q, const void *k, const void *v, const hla_block_mask *mask,
-                        void *out, float *lse, int64_t B, int64_t heads, int64_t N, int64_t d,
-                        hla_dtype dtype, float scale, hla_stream_t stream) {
+static hla_status attn_fwd(const void *q, const void *k, const void *v, const int32_t *order,
+                           const hla_block_mask *mask, void *out, float *lse, int64_t B,
+                           int64_t heads, int64_t N, int64_t d, hla_dtype dtype, float scale,
+                           hla_stream_t stream, const char *name) {
   hla_status st;
   if ((st = check_tensor_args(q, "q")) != HLA_OK) return st;
   if ((st = check_tensor_args(k, "k")) != HLA_OK) return st;
@@ -256,6 +257,7 @@ hla_status hla_attn_fwd(const void *q, const void *k, const void *v, const hla_b
   a.v = v;
   a.out = out;
   a.lse = lse;
+  a.order = order;
   a.n_full = mask->n_full;
   a.full_idx = mask->full_idx;
   a.n_part = mask->n_part;
@@ -269,7 +271,27 @@ hla_status hla_attn_fwd(const void *q, const void *k, const void *v, const hla_b
   hipError_t e = dtype == HLA_BF16
                      ? hla::launch_attn_bf16(a, (int)d, mask->tile_m, mask->tile_n, (hipStream_t)stream)
                      : hla::launch_attn_f32(a, (int)d, mask->tile_m, mask->tile_n, (hipStream_t)stream);
-  return hip_status(e, "hla_attn_fwd");
+  return hip_status(e, name);
+}
+
+hla_status hla_attn_fwd(const void *q, const void *k, const void *v, const hla_block_mask *mask,
+                        void *out, float *lse, int64_t B, int64_t heads, int64_t N, int64_t d,
+                        hla_dtype dtype, float scale, hla_stream_t stream) {
+  return attn_fwd(q, k, v, nullptr, mask, out, lse, B, heads, N, d, dtype, scale, stream,
+                  "hla_attn_fwd");
+}
+
+hla_status hla_attn_fwd_perm(const void *q, const void *k, const void *v, const int32_t *order,
+                             const hla_block_mask *mask, void *out, float *lse, int64_t B,
+                             int64_t heads, int64_t N, int64_t d, hla_dtype dtype, float scale,
+                             hla_stream_t stream) {
+  if (!order) return fail(HLA_ERR_INVALID_ARG, "order is NULL");
+  if (!aligned(order, 16)) return fail(HLA_ERR_INVALID_ARG, "order is not 16-byte aligned");
+  for (const void *t : {q, k, v, (const void *)out})
+    if (t && overlaps(order, N * 4, t, B * heads * N * d * dtype_size(dtype)))
+      return fail(HLA_ERR_INVALID_ARG, "order overlaps a tensor");
+  return attn_fwd(q, k, v, order, mask, out, lse, B, heads, N, d, dtype, scale, stream,
+                  "hla_attn_fwd_perm");
 }
 
 hla_status hla_attn_bwd(const void *q, const void *k, const void *v, const void *out,

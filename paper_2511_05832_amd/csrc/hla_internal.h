@@ -83,6 +83,7 @@ struct AttnArgs {
   const void *q, *k, *v;
   void *out;
   float *lse;
+  const int32_t *order;  // NULL: tensors in sequence order; else row of position i
   const int32_t *n_full, *full_idx, *n_part, *part_idx;
   int32_t BH, N, n_qtiles, n_ktiles;
   float scale_log2;  // scale * log2(e)

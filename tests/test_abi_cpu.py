@@ -144,6 +144,26 @@ def test_attn_validation(L):
     assert L.hla_attn_fwd(q, k, v, None, o, None, 2, 4, N, 64, hla.HLA_BF16, 0.1, None) == hla.HLA_ERR_INVALID_ARG
 
 
+def test_attn_fwd_perm_validation(L):
+    """The fused-reordering forward checks its order array first, then everything
+    hla_attn_fwd checks; every call here is invalid, so nothing is launched."""
+    vp = ctypes.c_void_p
+    q, k, v, o = vp(0x100000), vp(0x200000), vp(0x300000), vp(0x400000)
+    N = 4096
+
+    def call(order, m=None, d=64, scale=0.125):
+        m = m or fake_mask()
+        return L.hla_attn_fwd_perm(q, k, v, order, ctypes.byref(m), o, None, 2, 4, N, d,
+                                   hla.HLA_BF16, scale, None)
+
+    assert call(None) == hla.HLA_ERR_INVALID_ARG and "order" in L.hla_last_error().decode()
+    assert call(vp(0x800004)) == hla.HLA_ERR_INVALID_ARG and "16-byte" in L.hla_last_error().decode()
+    assert call(vp(0x100000 + 1024)) == hla.HLA_ERR_INVALID_ARG and "overlap" in L.hla_last_error().decode()
+    assert call(vp(0x800000), d=48) == hla.HLA_ERR_UNSUPPORTED
+    assert call(vp(0x800000), scale=0.0) == hla.HLA_ERR_INVALID_ARG
+    assert call(vp(0x800000), m=fake_mask(tm=256, tn=64)) == hla.HLA_ERR_UNSUPPORTED
+
+
 def test_build_block_mask_rejects_partial_column_lists(L):
     m = hla.BlockMaskStruct()
     m.pat = desc("hilbert_slide", 64, 64, 128)

@@ -1,4 +1,4 @@
-"""Hilbert order of a square power-of-two grid, by recursive quadrant construction.
+"""Hilbert order of an H x W token grid, by recursive quadrant construction.
 
 Test infrastructure only (see the package docstring).
 
@@ -20,6 +20,14 @@ text), so this oracle fixes one convention and the library follows it:
 order[d] = row-major id of the d-th cell on the curve; rank = inverse of order.
 Every one of the curve's eight symmetric variants gives the same tile masks for
 the Hilbert patterns, because those depend only on 1-D positions.
+
+Grids that are not a 2^k x 2^k square. The paper measures 56 x 56, 96 x 96,
+160 x 160 and 128 x 256 grids (Tables 1, 3, 6-8) and says only that each size has
+one path, computed once and cached (Sec. 3.2); it does not say how the curve
+covers such a grid. Reading used here: take the curve on the smallest 2^k x 2^k
+square that contains the grid (same convention, grid at its lower-left corner)
+and keep the cells inside the grid, in the curve's order. On a 2^k square this
+is the curve itself.
 """
 from __future__ import annotations
 
@@ -48,10 +56,12 @@ def hilbert_cells(k: int) -> np.ndarray:
 
 def hilbert_order(H: int, W: int) -> np.ndarray:
     """order[d] = row-major id of the d-th token along the curve (int64, length H*W)."""
-    if H != W or not is_pow2(H):
-        raise ValueError("the oracle's Hilbert order is defined on 2^k x 2^k grids")
-    k = H.bit_length() - 1
+    if H < 1 or W < 1:
+        raise ValueError("the grid must have at least one row and one column")
+    k = (max(H, W) - 1).bit_length()          # smallest 2^k >= max(H, W)
     cells = hilbert_cells(k)
+    inside = (cells[:, 0] < W) & (cells[:, 1] < H)
+    cells = cells[inside]
     return cells[:, 1] * W + cells[:, 0]
 
 

@@ -3,7 +3,7 @@
 The paper names the Hilbert curve for its locality (Sec. 1, Sec. 3.1) and caches
 one path per feature-map size (Sec. 3.2); it fixes no orientation. These tests
 pin the oracle to what any Hilbert curve must satisfy, and to the textbook
-iterative index-to-cell algorithm (the quadrant-rotation loop of Hacker's
+iterative index-to-cell algorithm and its inverse (the quadrant-rotation loop of Hacker's
 Delight, ch. 16, also given on Wikipedia's "Hilbert curve" page), written out
 here independently of the oracle's recursion.
 """
@@ -97,8 +97,71 @@ def test_small_orders_by_hand():
                                                    10, 14, 15, 11, 7, 6, 2, 3]
 
 
-def test_rejects_non_power_of_two():
+def textbook_xy2d(side, x, y):
+    """Iterative (x, y) -> d on a side x side curve, the inverse of textbook_d2xy:
+    per level from the coarsest, read the quadrant bits, add its offset, then
+    undo the rotation/reflection of the low bits."""
+    d = 0
+    s = side // 2
+    while s > 0:
+        rx = 1 if x & s else 0
+        ry = 1 if y & s else 0
+        d += s * s * ((3 * rx) ^ ry)
+        if ry == 0:
+            if rx == 1:
+                x, y = s - 1 - (x & (s - 1)), s - 1 - (y & (s - 1))
+            x, y = y, x
+        s //= 2
+    return d
+
+
+def test_textbook_pair_are_inverses():
+    for side in (1, 2, 4, 8, 16):
+        for d in range(side * side):
+            x, y = textbook_d2xy(side, d)
+            assert textbook_xy2d(side, x, y) == d
+
+
+GRIDS = [(1, 1), (1, 7), (7, 1), (3, 5), (5, 3), (6, 6), (7, 13), (17, 9), (24, 24), (32, 48),
+         (48, 32), (56, 56), (64, 128), (128, 64), (96, 96), (100, 37), (160, 160), (128, 256)]
+
+
+@pytest.mark.parametrize("H,W", GRIDS)
+def test_any_grid_is_a_bijection(H, W):
+    order = hilbert.hilbert_order(H, W)
+    assert order.shape == (H * W,)
+    assert np.array_equal(np.sort(order), np.arange(H * W))
+
+
+@pytest.mark.parametrize("H,W", GRIDS)
+def test_any_grid_follows_the_enclosing_curve(H, W):
+    """Every cell of the grid appears, and their positions on the enclosing
+    2^k curve (computed with the textbook inverse, not the oracle) increase."""
+    side = 1
+    while side < max(H, W):
+        side *= 2
+    order = hilbert.hilbert_order(H, W)
+    pos = [textbook_xy2d(side, int(t) % W, int(t) // W) for t in order]
+    assert all(a < b for a, b in zip(pos, pos[1:]))
+    assert len(pos) == H * W
+
+
+@pytest.mark.parametrize("k", range(1, 8))
+def test_two_to_one_rectangles(k):
+    """A 2^k x 2^(k+1) grid (rows x cols) is the lower half of the enclosing square:
+    the path is one 2^k square curve after the other, with a single jump between
+    them; a 2^(k+1) x 2^k grid is the left half and the path never jumps."""
+    s = 1 << k
+    wide = hilbert.hilbert_order(s, 2 * s)
+    x, y = wide % (2 * s), wide // (2 * s)
+    assert (x[: s * s] < s).all() and (x[s * s:] >= s).all()
+    steps = np.abs(np.diff(x)) + np.abs(np.diff(y))
+    assert (steps != 1).sum() == 1 and steps[s * s - 1] != 1
+    tall = hilbert.hilbert_order(2 * s, s)
+    x, y = tall % s, tall // s
+    assert (np.abs(np.diff(x)) + np.abs(np.diff(y)) == 1).all()
+
+
+def test_rejects_empty_grid():
     with pytest.raises(ValueError):
-        hilbert.hilbert_order(96, 96)
-    with pytest.raises(ValueError):
-        hilbert.hilbert_order(64, 128)
+        hilbert.hilbert_order(0, 4)

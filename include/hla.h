@@ -120,8 +120,12 @@ typedef struct {
  * order[d] = row-major id (y*W + x) of the d-th cell on the curve;
  * rank[t]  = position of row-major token t on the curve (rank[order[d]] = d).
  * Curve: starts at cell (x,y) = (0,0), first step to (0,1), ends at (W-1,0).
- * order, rank: device int32[H*W]; either may be NULL to skip it.
- * UNSUPPORTED unless H == W == 2^k with 0 <= k <= 15.
+ * Any other grid (the paper also uses 56x56, 96x96, 160x160 and 128x256
+ * feature maps and does not say how its curve covers them): the curve on the
+ * smallest 2^k x 2^k square holding the grid (grid at its (0,0) corner), with
+ * the cells outside the grid left out, in the curve's order.
+ * order, rank: device int32[H*W]; either may be NULL to skip it; they may not
+ * overlap. INVALID_ARG unless H, W >= 1; UNSUPPORTED if H or W > 32768.
  */
 hla_status hla_hilbert_perm(int32_t H, int32_t W, int32_t *order, int32_t *rank,
                             hla_stream_t stream);

@@ -91,6 +91,11 @@ hla_status check_tensor_args(const void *a, const char *name) {
   return HLA_OK;
 }
 
+bool overlaps(const void *a, int64_t na, const void *b, int64_t nb) {
+  const char *x = static_cast<const char *>(a), *y = static_cast<const char *>(b);
+  return x < y + nb && y < x + na;
+}
+
 }  // namespace
 
 extern "C" {
@@ -101,12 +106,17 @@ const char *hla_version(void) { return "libhla 0.1 (gfx950)"; }
 
 hla_status hla_hilbert_perm(int32_t H, int32_t W, int32_t *order, int32_t *rank,
                             hla_stream_t stream) {
-  if (H != W || !is_pow2(H) || H > (1 << 15))
-    return fail(HLA_ERR_UNSUPPORTED, "Hilbert order needs H == W == 2^k <= 32768 (got %dx%d)", H, W);
+  if (H < 1 || W < 1) return fail(HLA_ERR_INVALID_ARG, "grid %dx%d must be positive", H, W);
+  if (H > (1 << 15) || W > (1 << 15))
+    return fail(HLA_ERR_UNSUPPORTED, "Hilbert order needs H, W <= 32768 (got %dx%d)", H, W);
   if (order && !aligned(order, 4)) return fail(HLA_ERR_INVALID_ARG, "order is not 4-byte aligned");
   if (rank && !aligned(rank, 4)) return fail(HLA_ERR_INVALID_ARG, "rank is not 4-byte aligned");
+  if (order && rank && overlaps(order, (int64_t)H * W * 4, rank, (int64_t)H * W * 4))
+    return fail(HLA_ERR_INVALID_ARG, "order and rank overlap");
   if (!order && !rank) return HLA_OK;
-  return hip_status(hla::launch_hilbert_perm(H, order, rank, (hipStream_t)stream), "hla_hilbert_perm");
+  if (H == W && is_pow2(H))
+    return hip_status(hla::launch_hilbert_perm(H, order, rank, (hipStream_t)stream), "hla_hilbert_perm");
+  return hip_status(hla::launch_hilbert_grid(H, W, order, rank, (hipStream_t)stream), "hla_hilbert_perm");
 }
 
 static hla_status permute(const void *src, void *dst, const int32_t *order, int64_t B,
@@ -223,11 +233,6 @@ hla_status check_attn(const hla_block_mask *mask, int64_t B, int64_t heads, int6
   if (BH * mask->n_qtiles > kMaxI32 || BH * mask->n_ktiles > kMaxI32 || BH * N > kMaxI32)
     return fail(HLA_ERR_UNSUPPORTED, "grid too large");
   return HLA_OK;
-}
-
-bool overlaps(const void *a, int64_t na, const void *b, int64_t nb) {
-  const char *x = static_cast<const char *>(a), *y = static_cast<const char *>(b);
-  return x < y + nb && y < x + na;
 }
 
 }  // namespace

@@ -61,6 +61,9 @@ inline PatternArgs make_pattern_args(const hla_pattern_desc &p) {
 
 hipError_t launch_hilbert_perm(int32_t side, int32_t *order, int32_t *rank,
                                hipStream_t s);
+// Any H x W grid: the enclosing 2^k curve with the cells outside the grid left out.
+hipError_t launch_hilbert_grid(int32_t H, int32_t W, int32_t *order, int32_t *rank,
+                               hipStream_t s);
 
 hipError_t launch_permute(const void *src, void *dst, const int32_t *order,
                           int64_t BH, int64_t N, int64_t row_bytes, bool scatter,

@@ -47,13 +47,19 @@ def status_and_msg(L, st):
     return st, L.hla_last_error().decode()
 
 
-def test_hilbert_rejects_non_power_of_two(L):
-    st, msg = status_and_msg(L, L.hla_hilbert_perm(96, 96, None, None, None))
-    assert st == hla.HLA_ERR_UNSUPPORTED and "2^k" in msg
-    st, _ = status_and_msg(L, L.hla_hilbert_perm(64, 128, None, None, None))
+def test_hilbert_validation(L):
+    """Any H x W grid up to 32768 per side; nothing to write is a no-op."""
+    assert L.hla_hilbert_perm(96, 96, None, None, None) == hla.HLA_OK
+    assert L.hla_hilbert_perm(56, 128, None, None, None) == hla.HLA_OK
+    st, msg = status_and_msg(L, L.hla_hilbert_perm(0, 64, None, None, None))
+    assert st == hla.HLA_ERR_INVALID_ARG and "positive" in msg
+    st, _ = status_and_msg(L, L.hla_hilbert_perm(64, 40000, None, None, None))
     assert st == hla.HLA_ERR_UNSUPPORTED
     st, _ = status_and_msg(L, L.hla_hilbert_perm(64, 64, ctypes.c_void_p(2), None, None))
     assert st == hla.HLA_ERR_INVALID_ARG
+    st, msg = status_and_msg(L, L.hla_hilbert_perm(8, 8, ctypes.c_void_p(0x1000),
+                                                   ctypes.c_void_p(0x1000 + 64), None))
+    assert st == hla.HLA_ERR_INVALID_ARG and "overlap" in msg
 
 
 def test_permute_validation(L):

@@ -45,6 +45,24 @@ def test_full_size_workloads_sampled_rows(w):
     check(w.pattern, q, k, v, w.tile_m, w.tile_n, w.scale, w.dtype, rows=rows)
 
 
+# Feature maps of the paper whose side is not a power of two (Tables 1, 3, 6-8),
+# through the library's Hilbert order for any grid: (pattern, B, heads, tile_m, rows)
+PAPER_GRIDS = [
+    (Pat("hilbert_slide", 56, 56, 24), 2, 2, 64, None),           # I=56, K=7 -> h=24
+    (Pat("hilbert_neighborhood", 56, 56, 49), 1, 2, 64, None),    # HNA, I=56, K=7
+    (Pat("hilbert_window", 96, 96, 144), 1, 2, 128, None),        # I=96, W=12x12
+    (Pat("hilbert_window", 160, 160, 400), 1, 2, 128, "sample"),  # I=160, W=20x20
+    (Pat("hilbert_window", 128, 256, 256), 1, 2, 128, "sample"),  # I=128x256, W=16x16
+]
+
+
+@pytest.mark.parametrize("pat,B,Hh,tm,rows", PAPER_GRIDS, ids=lambda x: str(x) if isinstance(x, Pat) else None)
+def test_paper_grids_that_are_not_powers_of_two(pat, B, Hh, tm, rows):
+    q, k, v = W.attn_inputs(B, Hh, pat.N, 64, "bf16", 900 + pat.H)
+    rows = sample_rows(pat.N, tm, pat.H, n_random=96) if rows == "sample" else None
+    check(pat, q, k, v, tm, 64, 0.125, "bf16", rows=rows)
+
+
 def random_cases(n):
     rng = np.random.default_rng(77)
     kinds = list(hla.PATTERN_IDS)

@@ -19,6 +19,31 @@ def test_hilbert_perm_bit_exact(k):
     np.testing.assert_array_equal(rank.cpu().numpy(), o_hil.inverse_permutation(ref))
 
 
+# Grids that are not 2^k squares: the paper's 56^2, 96^2, 160^2 and 128 x 256 feature
+# maps, 2:1 rectangles both ways, single rows and columns, and odd sizes.
+GRIDS = [(56, 56), (96, 96), (160, 160), (128, 256), (256, 128), (1, 1), (1, 1000), (1000, 1),
+         (7, 13), (33, 65), (100, 37), (3, 5), (640, 480)]
+
+
+@pytest.mark.parametrize("H,W", GRIDS)
+def test_hilbert_perm_any_grid_bit_exact(H, W):
+    order, rank = hla.hilbert_perm(H, W)
+    ref = o_hil.hilbert_order(H, W)
+    np.testing.assert_array_equal(order.cpu().numpy(), ref)
+    np.testing.assert_array_equal(rank.cpu().numpy(), o_hil.inverse_permutation(ref))
+
+
+def test_hilbert_perm_order_only_and_rank_only():
+    ref = o_hil.hilbert_order(96, 96)
+    order = torch.full((96 * 96,), -1, dtype=torch.int32, device="cuda")
+    rank = torch.full((96 * 96,), -1, dtype=torch.int32, device="cuda")
+    hla.lib().hla_hilbert_perm(96, 96, order.data_ptr(), None, None)
+    hla.lib().hla_hilbert_perm(96, 96, None, rank.data_ptr(), None)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(order.cpu().numpy(), ref)
+    np.testing.assert_array_equal(rank.cpu().numpy(), o_hil.inverse_permutation(ref))
+
+
 def _bits(t: torch.Tensor) -> np.ndarray:
     t = t.cpu().contiguous()
     return t.view(torch.int16).numpy() if t.element_size() == 2 else t.view(torch.int32).numpy()

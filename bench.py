@@ -122,7 +122,7 @@ class AttnPipeline:
         del q, k, v
         self.order = torch.empty(N, dtype=torch.int32, device="cuda")
         self.rank = torch.empty(N, dtype=torch.int32, device="cuda")
-        self.mask = hla.BlockMask(pat, w.tile_m, w.tile_n)
+        self.mask = hla.BlockMask(pat, w.tile_m, w.tile_n, totals=False)
         self.timer = Timer()
 
     def step(self, i):
@@ -240,7 +240,7 @@ class LayerPipeline:
             self.sets.append(s)
         self.order = torch.empty(N, dtype=torch.int32, device="cuda")
         self.rank = torch.empty(N, dtype=torch.int32, device="cuda")
-        self.mask = hla.BlockMask(w.pattern, w.tile_m, w.tile_n)
+        self.mask = hla.BlockMask(w.pattern, w.tile_m, w.tile_n, totals=False)
         self.timer = Timer()
 
     def step(self, i):

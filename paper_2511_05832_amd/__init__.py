@@ -228,7 +228,8 @@ class BlockMask:
     ``columns=True`` also allocates and builds the per-key-tile-column lists
     that the backward pass walks."""
 
-    def __init__(self, pattern, tile_m: int, tile_n: int, device="cuda", columns: bool = False):
+    def __init__(self, pattern, tile_m: int, tile_n: int, device="cuda", columns: bool = False,
+                 totals: bool = True):
         nq, nk = block_mask_dims(pattern, tile_m, tile_n)
         self.pattern = pattern
         self.tile_m, self.tile_n, self.n_qtiles, self.n_ktiles = tile_m, tile_n, nq, nk
@@ -244,7 +245,10 @@ class BlockMask:
         self.struct.full_idx = self.full_idx.data_ptr()
         self.struct.n_part = self.n_part.data_ptr()
         self.struct.part_idx = self.part_idx.data_ptr()
-        self.struct.totals = self.totals.data_ptr()
+        # totals=False: the build writes only the lists (the attention reads nothing
+        # else); host_totals() then sums the per-row counts itself
+        self.with_totals = totals
+        self.struct.totals = self.totals.data_ptr() if totals else 0
         self.columns = columns
         if columns:
             self.n_full_t = torch.empty(nk, dtype=torch.int32, device=device)
@@ -265,6 +269,8 @@ class BlockMask:
         return self.struct.N
 
     def host_totals(self) -> Tuple[int, int]:
+        if not self.with_totals:
+            return int(self.n_full.sum().item()), int(self.n_part.sum().item())
         t = self.totals.cpu()
         return int(t[0]), int(t[1])
 

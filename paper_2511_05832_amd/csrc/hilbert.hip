@@ -2,7 +2,7 @@
 // Hilbert curve; the path depends only on (H, W) and is computed once and
 // cached).
 //
-// Both kernels are one thread per output element and write coalesced:
+// One launch, one thread per output element, both outputs written coalesced:
 //   hilbert_d2xy: thread d walks the curve index two bits per level, from the
 //                 finest quadrant up, and writes order[d] = y*W + x;
 //   hilbert_xy2d: thread t = y*W + x walks the cell's coordinate bits from the
@@ -25,10 +25,8 @@
 namespace hla {
 namespace {
 
-__global__ void __launch_bounds__(256) hilbert_d2xy(int32_t side, int32_t n,
-                                                    int32_t *__restrict__ order) {
-  const int32_t d = blockIdx.x * 256 + threadIdx.x;
-  if (d >= n) return;
+__device__ __forceinline__ void hilbert_d2xy(int32_t side, int32_t d,
+                                             int32_t *__restrict__ order) {
   uint32_t x = 0, y = 0, t = (uint32_t)d;
   for (uint32_t s = 1; s < (uint32_t)side; s <<= 1) {
     // quadrant at this level: 0 lower-left, 1 upper-left, 2 upper-right, 3 lower-right
@@ -50,10 +48,8 @@ __global__ void __launch_bounds__(256) hilbert_d2xy(int32_t side, int32_t n,
   order[d] = (int32_t)(y * (uint32_t)side + x);
 }
 
-__global__ void __launch_bounds__(256) hilbert_xy2d(int32_t side, int32_t n,
-                                                    int32_t *__restrict__ rank) {
-  const int32_t id = blockIdx.x * 256 + threadIdx.x;
-  if (id >= n) return;
+__device__ __forceinline__ void hilbert_xy2d(int32_t side, int32_t id,
+                                             int32_t *__restrict__ rank) {
   uint32_t x = (uint32_t)id % (uint32_t)side;
   uint32_t y = (uint32_t)id / (uint32_t)side;
   uint32_t d = 0;
@@ -72,6 +68,20 @@ __global__ void __launch_bounds__(256) hilbert_xy2d(int32_t side, int32_t n,
     }
   }
   rank[id] = (int32_t)d;
+}
+
+// One launch for both directions: the first `blocks_order` workgroups write order,
+// the rest write rank (either part may be absent).
+__global__ void __launch_bounds__(256) hilbert_square(int32_t side, int32_t n, int32_t blocks_order,
+                                                      int32_t *__restrict__ order,
+                                                      int32_t *__restrict__ rank) {
+  if ((int32_t)blockIdx.x < blocks_order) {
+    const int32_t d = blockIdx.x * 256 + threadIdx.x;
+    if (d < n) hilbert_d2xy(side, d, order);
+  } else {
+    const int32_t id = (blockIdx.x - blocks_order) * 256 + threadIdx.x;
+    if (id < n) hilbert_xy2d(side, id, rank);
+  }
 }
 
 // Cells of the grid [0, W) x [0, H) inside the axis-aligned square spanned by the
@@ -162,17 +172,10 @@ hipError_t launch_hilbert_perm(int32_t side, int32_t *order, int32_t *rank,
                                hipStream_t s) {
   const int32_t n = side * side;
   const int32_t blocks = (n + 255) / 256;
-  if (order) {
-    hipLaunchKernelGGL(hilbert_d2xy, dim3(blocks), dim3(256), 0, s, side, n, order);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  if (rank) {
-    hipLaunchKernelGGL(hilbert_xy2d, dim3(blocks), dim3(256), 0, s, side, n, rank);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
+  const int32_t bo = order ? blocks : 0, br = rank ? blocks : 0;
+  if (bo + br == 0) return hipSuccess;
+  hipLaunchKernelGGL(hilbert_square, dim3(bo + br), dim3(256), 0, s, side, n, bo, order, rank);
+  return hipGetLastError();
 }
 
 }  // namespace hla

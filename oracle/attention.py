@@ -23,6 +23,19 @@ positions refer to; they are upcast to float64 exactly. ``positions`` maps an
 index on the token axis to the pattern position of that token (default:
 identity); with positions = Hilbert rank this evaluates a Hilbert pattern on
 row-major tensors. ``rows`` restricts the output to those query indices.
+
+Global relative position bias (the score modification of the Hilbert Window
+Transformer, Sec. 3.2, and part of the per-block work in Eq. 1): with
+``rpb = (table, grid_rows)``, table[h] of shape [2H-1, 2W-1] and grid_rows[i] the
+row-major grid id of the token at index i,
+
+  S_ij = scale * <q_i, k_j> + table[h, r_i - r_j + H - 1, c_i - c_j + W - 1]
+
+before the mask, with (r, c) = (grid_rows // W, grid_rows % W). The bias is the
+same for every batch element. The paper enlarges the Swin-style window bias to
+the whole feature map (its windows have irregular shapes); it gives no table
+layout, so the Swin one - offsets shifted to be non-negative, rows then columns
+- is used.
 """
 from __future__ import annotations
 
@@ -31,8 +44,22 @@ import numpy as np
 from . import masks
 
 
+def rpb_bias(table, grid_rows_q, grid_rows_k, H: int, W: int) -> np.ndarray:
+    """Bias [heads, len(q), len(k)] of the global relative position bias: for
+    query token at grid id a and key token at grid id b,
+    table[h, a//W - b//W + H - 1, a%W - b%W + W - 1]."""
+    table = np.asarray(table, dtype=np.float64)
+    if table.ndim != 3 or table.shape[1:] != (2 * H - 1, 2 * W - 1):
+        raise ValueError(f"table must be [heads, {2 * H - 1}, {2 * W - 1}]")
+    a = np.asarray(grid_rows_q, dtype=np.int64)
+    b = np.asarray(grid_rows_k, dtype=np.int64)
+    dr = a[:, None] // W - b[None, :] // W + H - 1
+    dc = a[:, None] % W - b[None, :] % W + W - 1
+    return table[:, dr, dc]
+
+
 def attention(q, k, v, pattern, scale: float, rows=None, positions=None,
-              chunk: int = 256):
+              chunk: int = 256, rpb=None):
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
@@ -48,9 +75,16 @@ def attention(q, k, v, pattern, scale: float, rows=None, positions=None,
         r = rows[c0:c0 + chunk]
         allow = masks.allowed(pattern, pos[r][:, None], pos[None, :])   # [R, N]
         any_allowed = allow.any(axis=1)
+        bias = None
+        if rpb is not None:
+            table, grid_rows = rpb
+            grid_rows = np.asarray(grid_rows, dtype=np.int64)
+            bias = rpb_bias(table, grid_rows[r], grid_rows, pattern.H, pattern.W)  # [heads, R, N]
         for b in range(B):
             for h in range(Hh):
                 s = scale * (q[b, h, r] @ k[b, h].T)                      # [R, N]
+                if bias is not None:
+                    s = s + bias[h]
                 s = np.where(allow, s, -np.inf)
                 m = s.max(axis=1)
                 m_safe = np.where(any_allowed, m, 0.0)
@@ -66,8 +100,8 @@ def attention_backward(q, k, v, dout, pattern, scale: float, rows=None, key_rows
                        positions=None, chunk: int = 256):
     """Gradients of ``attention`` for an upstream gradient ``dout``, in float64.
 
-    The paper times the backward pass of every attention it measures (Tables 1-3
-    and 6-11, Backward columns) but writes no formula for it; the gradients are
+    The paper times the backward pass of every attention it measures (Tables 1,
+    3, 6, 7, 9, 11, Backward columns) but writes no formula for it; the gradients are
     those of the forward definition above. Per (b, h), with P_ij the softmax
     weights (0 where masked) and out_i = sum_j P_ij v_j:
 

@@ -23,7 +23,9 @@ on a bounded sample of the same step on the host cores.
 The backward pass of the same attention workload is timed the same way (a
 graph-replayed step: gather of the upstream gradient, hla_attn_bwd, scatter of
 dq, dk, dv; per-call time of hla_attn_bwd from an eager pass) and reported under
-"backward"; --no-backward skips it.
+"backward"; --no-backward skips it. The attention with the global relative
+position bias (hla_attn_fwd_rpb) is timed per call on the same inputs and
+reported under "rpb"; --no-rpb skips it.
 """
 from __future__ import annotations
 
@@ -409,6 +411,43 @@ def time_backward(pipe, steps, warmup):
     }
 
 
+def time_rpb(pipe, steps, warmup):
+    """The attention with the global relative position bias (hla_attn_fwd_rpb) on the
+    workload's resident inputs taken as sequence-ordered, with the Hilbert order
+    (identity for row-major patterns) and a seeded float32 table [heads, 2H-1, 2W-1];
+    eager calls with an event pair around each."""
+    hla, w = pipe.hla, pipe.w
+    pat = w.pattern
+    g = torch.Generator(device="cpu")
+    g.manual_seed(w.seed + 2000)
+    table = torch.randn((w.heads, 2 * pat.H - 1, 2 * pat.W - 1), generator=g).cuda()
+    if pat.hilbert:
+        order = hla.hilbert_perm(pat.H, pat.W)[0]
+    else:
+        order = torch.arange(w.N, dtype=torch.int32, device="cuda")
+    mask = hla.BlockMask(pat, w.tile_m, w.tile_n, totals=False).build()
+    T = Timer()
+
+    def call(i):
+        s = pipe.sets[i % pipe.nsets]
+        with T.stage("attn_rpb"):
+            hla.attn_fwd_rpb(s["q"], s["k"], s["v"], order, table, mask, w.scale,
+                             out=s["o"], lse=s["lse"])
+    for i in range(warmup):
+        call(i)
+    torch.cuda.synchronize()
+    T.active = True
+    for i in range(steps):
+        call(warmup + i)
+    torch.cuda.synchronize()
+    ms = T.mean_ms("attn_rpb")
+    flops = pipe.tile_flops()[0]
+    peak = BF16_PEAK_TFLOPS if w.dtype == "bf16" else FP32_PEAK_TFLOPS
+    return {"attn_rpb_ms_per_call": ms,
+            "attn_rpb_tflops_nonempty_tiles": flops / (ms * 1e-3) / 1e12,
+            "attn_rpb_pct_peak": 100.0 * flops / (ms * 1e-3) / 1e12 / peak}
+
+
 def summarize(pipe, timing):
     ms_step, eager_ms = timing
     T = pipe.timer
@@ -522,6 +561,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-backward", action="store_true",
                     help="skip timing the backward pass of the workload")
+    ap.add_argument("--no-rpb", action="store_true",
+                    help="skip timing the attention with the relative position bias")
     ap.add_argument("--step", default="fused", choices=["fused", "composed", "composed-only"],
                     help="which step of a Hilbert workload the headline value times: the "
                          "reordering fused into the attention (hla_attn_fwd_perm) or separate "
@@ -571,6 +612,10 @@ def main():
         res_fused = summarize(fpipe, run_timed(fpipe, args.steps, args.warmup))
         print(f"[bench] {w.name} (fused): {json.dumps(res_fused)}", file=sys.stderr, flush=True)
         pipe = fpipe   # the algorithmic figures below depend on the workload only
+    rpb = None
+    if isinstance(w, W.AttnWorkload) and not args.no_rpb:
+        rpb = time_rpb(pipe, args.steps, args.warmup)
+        print(f"[bench] {w.name} with the position bias: {json.dumps(rpb)}", file=sys.stderr, flush=True)
     res_composed = res
     if args.step == "fused" and res_fused:
         res = res_fused
@@ -671,6 +716,8 @@ def main():
             "attn_ms_per_call": other["attn_ms"], "stages_ms": other["stages_ms"]}
     if bwd:
         line["backward"] = bwd
+    if rpb:
+        line["rpb"] = rpb
     if cmp_res:
         line["rowmajor_comparison"] = {
             "workload": cmp_res["workload"], "attn_ms_per_call": cmp_res["attn_ms"],

@@ -212,6 +212,28 @@ hla_status hla_attn_fwd_perm(const void *q, const void *k, const void *v,
                              hla_stream_t stream);
 
 /*
+ * The attention forward with the global relative position bias of the Hilbert
+ * Window Transformer (Sec. 3.2: the Swin window bias enlarged to the whole
+ * feature map, because Hilbert windows have irregular shapes; Eq. 1 counts such
+ * a score modification in the per-block work):
+ *   S_ij = scale * <q_i, k_j> + rpb[h, r_i - r_j + H - 1, c_i - c_j + W - 1]
+ * where (r_i, c_i) = (order[i] / W, order[i] % W) is the grid cell of sequence
+ * position i, and H, W are the mask's grid. q, k, v, out, lse in sequence order
+ * as for hla_attn_fwd.
+ * order: device int32[N], the grid (row-major) id of each sequence position
+ * (hla_hilbert_perm's order for the Hilbert patterns; 0, 1, ..., N-1 for the
+ * row-major ones), 16-byte aligned, entries in [0, N) (not checked).
+ * rpb: device float32 [heads, 2H-1, 2W-1], the same for every batch element.
+ * Neither may overlap a tensor. Other arguments, support and errors as
+ * hla_attn_fwd.
+ */
+hla_status hla_attn_fwd_rpb(const void *q, const void *k, const void *v,
+                            const int32_t *order, const float *rpb,
+                            const hla_block_mask *mask, void *out, float *lse,
+                            int64_t B, int64_t heads, int64_t N, int64_t d,
+                            hla_dtype dtype, float scale, hla_stream_t stream);
+
+/*
  * Block-sparse attention backward: the gradients of hla_attn_fwd's out with
  * respect to q, k and v for an upstream gradient dout, over the same tiles as
  * the forward (empty tiles skipped, partial tiles masked; the paper times this

@@ -28,8 +28,8 @@ from typing import Optional, Tuple
 import torch
 
 __all__ = ["HLAError", "lib", "hilbert_perm", "gather", "scatter", "block_mask_dims",
-           "build_block_mask", "BlockMask", "attn_fwd", "attn_fwd_perm", "attn_bwd", "qkv_proj",
-           "out_proj",
+           "build_block_mask", "BlockMask", "attn_fwd", "attn_fwd_perm", "attn_fwd_rpb", "attn_bwd",
+           "qkv_proj", "out_proj",
            "PATTERN_IDS", "LIB_PATH", "EXPORTED"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhla.so")
@@ -48,7 +48,8 @@ HLA_OK, HLA_ERR_INVALID_ARG, HLA_ERR_UNSUPPORTED, HLA_ERR_HIP = 0, 1, 2, 3
 HLA_F32, HLA_BF16 = 0, 1
 
 EXPORTED = ("hla_hilbert_perm", "hla_gather", "hla_scatter", "hla_block_mask_dims",
-            "hla_build_block_mask", "hla_attn_fwd", "hla_attn_fwd_perm", "hla_attn_bwd",
+            "hla_build_block_mask", "hla_attn_fwd", "hla_attn_fwd_perm", "hla_attn_fwd_rpb",
+            "hla_attn_bwd",
             "hla_qkv_proj", "hla_out_proj",
             "hla_last_error", "hla_version")
 
@@ -104,6 +105,8 @@ def lib() -> ctypes.CDLL:
                              i64, i64, i64, i64, ctypes.c_int, f32, vp],
             "hla_attn_fwd_perm": [vp, vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp,
                                   i64, i64, i64, i64, ctypes.c_int, f32, vp],
+            "hla_attn_fwd_rpb": [vp, vp, vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp,
+                                 i64, i64, i64, i64, ctypes.c_int, f32, vp],
             "hla_attn_bwd": [vp, vp, vp, vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp, vp,
                              vp, i64, i64, i64, i64, ctypes.c_int, f32, vp],
             "hla_qkv_proj": [vp, vp, vp, vp, vp, i64, i64, i64, i64, vp],
@@ -328,6 +331,29 @@ def attn_fwd_perm(q, k, v, order, mask: BlockMask, scale: Optional[float] = None
     _check(lib().hla_attn_fwd_perm(_ptr(q), _ptr(k), _ptr(v), _ptr(order), ctypes.byref(mask.struct),
                                    _ptr(out), _ptr(lse), B, Hh, N, d, _dtype_code(q), scale,
                                    _stream(q)))
+    return out, lse
+
+
+def attn_fwd_rpb(q, k, v, order, rpb, mask: BlockMask, scale: Optional[float] = None,
+                 out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                 with_lse: bool = True):
+    """Attention forward with the global relative position bias (hla_attn_fwd_rpb):
+    q, k, v in sequence order; order[i] = grid (row-major) id of sequence position i
+    (None: the identity, for row-major patterns); rpb = float32 [heads, 2H-1, 2W-1].
+    Returns (out, lse or None)."""
+    B, Hh, N, d, scale, out, lse = _attn_fwd_args(q, k, v, scale, out, lse, with_lse)
+    if order is None:
+        order = torch.arange(N, dtype=torch.int32, device=q.device)
+    _require(order, "order")
+    _require(rpb, "rpb")
+    if order.dtype != torch.int32 or order.numel() != N:
+        raise HLAError(HLA_ERR_INVALID_ARG, f"order must be int32 with N = {N} entries")
+    H, W = mask.struct.pat.H, mask.struct.pat.W
+    if rpb.dtype != torch.float32 or tuple(rpb.shape) != (Hh, 2 * H - 1, 2 * W - 1):
+        raise HLAError(HLA_ERR_INVALID_ARG, f"rpb must be float32 [{Hh}, {2 * H - 1}, {2 * W - 1}]")
+    _check(lib().hla_attn_fwd_rpb(_ptr(q), _ptr(k), _ptr(v), _ptr(order), _ptr(rpb),
+                                  ctypes.byref(mask.struct), _ptr(out), _ptr(lse), B, Hh, N, d,
+                                  _dtype_code(q), scale, _stream(q)))
     return out, lse
 
 

@@ -109,15 +109,29 @@ __device__ __forceinline__ int swz_q(int r) {
 // Launch bound (second argument: minimum waves per SIMD): three waves, i.e. at
 // most 168 VGPRs per lane and three 4-wave workgroups per CU.
 //
-// GATHER: the tensors are stored in grid (row-major) order and sequence position
-// i lives in row a.order[i] (the reordering fused into the loads and stores).
-// Each key tile's 64 row indices are copied into LDS one step ahead of its K/V
-// copies (by the first wave; issued before that step's K/V copies, so the same
-// vmcnt counts cover them), and the Q tile's indices in the prologue, which also
-// give each lane the row its output goes to.
-template <int D, int NW, bool GATHER>
-__global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
+// MODE ATTN_GATHER: the tensors are stored in grid (row-major) order and
+// sequence position i lives in row a.order[i] (the reordering fused into the
+// loads and stores). Each key tile's 64 row indices are copied into LDS one step
+// ahead of its K/V copies (by the first wave; issued before that step's K/V
+// copies, so the same vmcnt counts cover them), and the Q tile's indices in the
+// prologue, which also give each lane the row its output goes to.
+//
+// MODE ATTN_RPB: tensors in sequence order, and every score gets the global
+// relative position bias table[h][r_i - r_j + H - 1][c_i - c_j + W - 1] of the
+// grid cells (r, c) of order[i], order[j]. With off(g) = g + (W - 1) * (g / W)
+// for a grid id g, that entry is table[h][C + off(q) - off(k)], C = (H - 1)(2W - 1)
+// + W - 1. Each wave copies a quarter of a key tile's grid ids into LDS with the
+// tile's K/V copies; each lane reads its 32 keys' ids from there and loads the
+// 32 bias values (ordinary loads: the compiler waits for them - and, the vmcnt
+// counter being in order, for the copies issued before them - before the
+// softmax, so this mode issues each tile's copies at the end of the step two
+// tiles earlier rather than at its start).
+template <int D, int NW, int MODE>
+__global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2)
     attn_fwd_bf16(AttnArgs a) {
+  constexpr bool GATHER = MODE == ATTN_GATHER;
+  constexpr bool RPB = MODE == ATTN_RPB;
+  constexpr bool IDX = GATHER || RPB;
   constexpr int BM = 32 * NW;
   constexpr int NT = 64 * NW;
   constexpr int CPR = D / 8;                  // 16-byte chunks per K/V row
@@ -132,11 +146,12 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
   static_assert(BM * D * 2 <= STAGE, "the Q tile must fit one stage");
   static_assert(kStages == 3, "the loop keeps exactly one tile in flight behind the current");
   static_assert(LPT < 64, "too many copies in flight for vmcnt");
+  constexpr int LPTR = RPB ? LPT + 1 : LPT;   // + the wave's share of the tile's grid ids
   // Row-index area (GATHER): the Q tile's BM indices, then four slots of BN
   // indices for key tiles (slot i % 4 holds tile list entry i).
   constexpr int IDXQ = kStages * STAGE;
   constexpr int IDXK = IDXQ + BM * 4;
-  constexpr int LDSB = GATHER ? IDXK + 4 * BN * 4 : kStages * STAGE;
+  constexpr int LDSB = IDX ? IDXK + 4 * BN * 4 : kStages * STAGE;
 
   __shared__ __attribute__((aligned(16))) char lds[LDSB];
   const int32_t *idx_q = reinterpret_cast<const int32_t *>(lds + IDXQ);
@@ -207,10 +222,17 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
       lds_dma16(Vt + roff[j] + vch[j], lds_addr(base + TILE + (j * NW + wave) * 1024));
   };
   // GATHER: the row indices of list entry i (16 bytes per lane of the first
-  // wave) into its slot.
+  // wave) into its slot. RPB: every wave copies BN / NW of them.
   auto issue_idx = [&](int i) {
-    if (wave == 0 && lane < BN / 4)
-      lds_dma16(a.order + (int64_t)tile_of(i) * BN + 4 * lane, lds_addr(lds + IDXK + (i & 3) * BN * 4));
+    if constexpr (GATHER) {
+      if (wave == 0 && lane < BN / 4)
+        lds_dma16(a.order + (int64_t)tile_of(i) * BN + 4 * lane, lds_addr(lds + IDXK + (i & 3) * BN * 4));
+    } else {
+      constexpr int PER = BN / NW;   // ids per wave
+      if (lane < PER / 4)
+        lds_dma16(a.order + (int64_t)tile_of(i) * BN + wave * PER + 4 * lane,
+                  lds_addr(lds + IDXK + (i & 3) * BN * 4 + wave * PER * 4));
+    }
   };
 
   // LDS byte offsets (within a stage) of this lane's operand reads.
@@ -240,7 +262,8 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
   for (int db = 0; db < NDB; ++db) oacc[db] = f32x16{};
   float m_run = -__builtin_inff();  // running reference, in units of log2
   float l_run = 0.f;               // this lane's partial sum (its half of the keys)
-  const float sl2 = a.scale_log2;
+  // scores are multiplied by smul to reach log2 units (RPB: already scaled)
+  const float smul = RPB ? 1.44269504088896340736f : a.scale_log2;
 
   // Prologue: the Q tile goes into stage 2 (which the third key tile fills
   // later), the first two key tiles into stages 0 and 1. Staging Q through LDS
@@ -266,11 +289,30 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
       lds_dma16(Q + row * D + (cs ^ swz_q<D>(r)) * 8, lds_addr(base + (j * NW + wave) * 1024));
     }
   }
+  if constexpr (RPB) {
+    if (ntot > 0) issue_idx(0);
+  }
   if (ntot > 0) issue_tile(0, 0);
+  if constexpr (RPB) {
+    if (ntot > 1) issue_idx(1);
+  }
   if (ntot > 1) issue_tile(1, 1);
-  // Q and the first key tile are in; the second may still be in flight.
-  if (ntot > 1) wait_then_barrier<LPT>();
-  else wait_then_barrier<0>();
+  // RPB: this lane's bias base C + off(q), loaded after the copies; one wait
+  // the compiler sees then covers it and them.
+  int32_t rpb_base = 0;
+  const float *rpb_h = nullptr;
+  if constexpr (RPB) {
+    const int32_t g = a.order[qpos];
+    const int32_t Wg = P.W;
+    rpb_base = (P.H - 1) * (2 * Wg - 1) + (Wg - 1) + g + (Wg - 1) * (int32_t)fdiv((uint32_t)g, P.wdiv);
+    rpb_h = a.rpb + (int64_t)(bh % a.heads) * (2 * P.H - 1) * (2 * Wg - 1);
+    wait_vmem_all();
+    wait_then_barrier<0>();
+  } else {
+    // Q and the first key tile are in; the second may still be in flight.
+    if (ntot > 1) wait_then_barrier<LPT>();
+    else wait_then_barrier<0>();
+  }
   bf16x8 qop[NCH];
   {
     const int r = wave * 32 + col;
@@ -288,7 +330,7 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
   auto step = [&](int it, auto masked) {
     // Wait for this wave's copies of tile `it`; the copies of tile it + 1 (the
     // only one issued after it) may stay in flight.
-    if (it + 1 < ntot) wait_then_barrier<LPT>();
+    if (it + 1 < ntot) wait_then_barrier<LPTR>();
     else wait_then_barrier<0>();
     // The stage refilled next was last read in iteration it - 1, which every
     // wave has finished (it is behind the barrier above).
@@ -298,7 +340,9 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
     if constexpr (GATHER) {
       if (it + 3 < ntot) issue_idx(it + 3);
     }
-    if (it + 2 < ntot) issue_tile(it + 2, nstage);
+    if constexpr (!RPB) {
+      if (it + 2 < ntot) issue_tile(it + 2, nstage);
+    }
     const char *st = lds + stage * STAGE;
     stage = stage == 2 ? 0 : stage + 1;
 
@@ -311,6 +355,30 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
         const bf16x8 kop = *reinterpret_cast<const bf16x8 *>(st + kaddr[kb][c]);
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[c], s[kb], 0, 0, 0);
       }
+    // RPB: scores in natural units plus the bias, s = scale * <q, k> + bias.
+    if constexpr (RPB) {
+      // all 32 bias loads first, so that they are in flight together
+      const int32_t *kid = idx_k(it);
+      const int32_t Wm1 = P.W - 1;
+      float bias[2][16];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+          const int4 *ids = reinterpret_cast<const int4 *>(kid + kb * 32 + 16 * g + 8 * half);
+          const int4 lo = ids[0], hi = ids[1];
+          const int32_t gk[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int32_t koff = gk[e] + Wm1 * (int32_t)fdiv((uint32_t)gk[e], P.wdiv);
+            bias[kb][8 * g + e] = rpb_h[rpb_base - koff];
+          }
+        }
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) s[kb][v] = __builtin_fmaf(s[kb][v], a.scale, bias[kb][v]);
+    }
     if constexpr (decltype(masked)::value) mask_blocks<2>(s, R, P, tile_of(it) * BN + 8 * half);
 
     // Online softmax in the log2 domain with a lazily moved reference: m_run
@@ -326,7 +394,7 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
                     fmaxf(fmaxf(sv[o + 4], sv[o + 5]), fmaxf(sv[o + 6], sv[o + 7])));
     }
     const float mx = xhalf_max(fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3])));
-    const float mt = mx * sl2;
+    const float mt = mx * smul;
     const bool grow = mt > m_run + kRescaleSlack;
     if (__ballot(grow)) {
       const float m_new = grow ? mt : m_run;
@@ -349,7 +417,7 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
       float acc = 0.f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float pv = __builtin_amdgcn_exp2f(sv[o + e] * sl2 - m_use);
+        const float pv = __builtin_amdgcn_exp2f(sv[o + e] * smul - m_use);
         acc += pv;
         pop[g][e] = (__bf16)pv;
       }
@@ -366,6 +434,14 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
         const bf16x8 vop = lds_read_tr16x2(st + vbase[db] + (16 * t) * D * 2, D * 2);
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[t], oacc[db], 0, 0, 0);
       }
+    // RPB: refill the ring at the end of the step (stage (it + 2) % 3 held tile
+    // it - 1, which every wave finished before this step's barrier).
+    if constexpr (RPB) {
+      if (it + 2 < ntot) {
+        issue_idx(it + 2);
+        issue_tile(it + 2, nstage);
+      }
+    }
   };
   for (int it = 0; it < nf; ++it) step(it, std::false_type{});
   for (int it = nf; it < ntot; ++it) step(it, std::true_type{});
@@ -408,10 +484,12 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2)
 template <int D, int NW>
 hipError_t launch(const AttnArgs &a, hipStream_t s) {
   const int64_t blocks = (int64_t)a.BH * a.n_qtiles;
-  if (a.order)
-    hipLaunchKernelGGL((attn_fwd_bf16<D, NW, true>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
+  if (a.mode == ATTN_GATHER)
+    hipLaunchKernelGGL((attn_fwd_bf16<D, NW, ATTN_GATHER>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
+  else if (a.mode == ATTN_RPB)
+    hipLaunchKernelGGL((attn_fwd_bf16<D, NW, ATTN_RPB>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
   else
-    hipLaunchKernelGGL((attn_fwd_bf16<D, NW, false>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
+    hipLaunchKernelGGL((attn_fwd_bf16<D, NW, ATTN_PLAIN>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
   return hipGetLastError();
 }
 

@@ -6,9 +6,10 @@
 // fp32 matrix mode, and fp32 vector FMA runs at the same 157 TFLOP/s as fp32
 // MFMA, so each thread owns one query row and does plain FMAs. K and V tiles are
 // staged in LDS and read as broadcasts (every lane of a wave reads the same key
-// row at the same time). GATHER: the tensors are stored in grid order and
-// sequence position i lives in row a.order[i] (reordering fused into the loads
-// and stores).
+// row at the same time). MODE ATTN_GATHER: the tensors are stored in grid
+// order and sequence position i lives in row a.order[i] (reordering fused into
+// the loads and stores). MODE ATTN_RPB: every score gets the global relative
+// position bias of the grid cells order[i], order[j] (see the bf16 kernel).
 #include "attn_common.h"
 
 namespace hla {
@@ -17,8 +18,10 @@ namespace {
 constexpr int BN = 64;
 constexpr int CH = 16;  // keys per online-softmax step
 
-template <int D, int BM, bool GATHER>
+template <int D, int BM, int MODE>
 __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
+  constexpr bool GATHER = MODE == ATTN_GATHER;
+  constexpr bool RPB = MODE == ATTN_RPB;
   __shared__ __attribute__((aligned(16))) float Ks[BN * D];
   __shared__ __attribute__((aligned(16))) float Vs[BN * D];
 
@@ -48,8 +51,16 @@ __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
   const int nf = a.n_full[qt], np = a.n_part[qt], ntot = nf + np;
   const int32_t *frow = a.full_idx + (int64_t)qt * a.n_ktiles;
   const int32_t *prow = a.part_idx + (int64_t)qt * a.n_ktiles;
-  const float sl2 = a.scale_log2;
+  // scores are multiplied by smul to reach log2 units (RPB: already scaled)
+  const float sl2 = RPB ? 1.44269504088896340736f : a.scale_log2;
   float m_run = -__builtin_inff(), l_run = 0.f;
+  int32_t rpb_base = 0;
+  const float *rpb_h = nullptr;
+  if constexpr (RPB) {
+    const int32_t g = a.order[qpos];
+    rpb_base = (P.H - 1) * (2 * P.W - 1) + (P.W - 1) + g + (P.W - 1) * (int32_t)fdiv((uint32_t)g, P.wdiv);
+    rpb_h = a.rpb + (int64_t)(bh % a.heads) * (2 * P.H - 1) * (2 * P.W - 1);
+  }
 
   for (int it = 0; it < ntot; ++it) {
     const bool masked = it >= nf;
@@ -70,6 +81,11 @@ __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
 #pragma unroll
         for (int i = 0; i < D; ++i) dot = __builtin_fmaf(q[i], Ks[(j0 + j) * D + i], dot);
         s[j] = dot;
+        if constexpr (RPB) {
+          const int32_t gk = a.order[kt * BN + j0 + j];
+          const int32_t koff = gk + (P.W - 1) * (int32_t)fdiv((uint32_t)gk, P.wdiv);
+          s[j] = __builtin_fmaf(dot, a.scale, rpb_h[rpb_base - koff]);
+        }
       }
       if (masked) {
 #pragma unroll
@@ -112,10 +128,12 @@ __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
 template <int D, int BM>
 hipError_t launch(const AttnArgs &a, hipStream_t s) {
   const int64_t blocks = (int64_t)a.BH * a.n_qtiles;
-  if (a.order)
-    hipLaunchKernelGGL((attn_fwd_f32<D, BM, true>), dim3((uint32_t)blocks), dim3(BM), 0, s, a);
+  if (a.mode == ATTN_GATHER)
+    hipLaunchKernelGGL((attn_fwd_f32<D, BM, ATTN_GATHER>), dim3((uint32_t)blocks), dim3(BM), 0, s, a);
+  else if (a.mode == ATTN_RPB)
+    hipLaunchKernelGGL((attn_fwd_f32<D, BM, ATTN_RPB>), dim3((uint32_t)blocks), dim3(BM), 0, s, a);
   else
-    hipLaunchKernelGGL((attn_fwd_f32<D, BM, false>), dim3((uint32_t)blocks), dim3(BM), 0, s, a);
+    hipLaunchKernelGGL((attn_fwd_f32<D, BM, ATTN_PLAIN>), dim3((uint32_t)blocks), dim3(BM), 0, s, a);
   return hipGetLastError();
 }
 

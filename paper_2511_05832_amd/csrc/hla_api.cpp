@@ -240,9 +240,9 @@ hla_status check_attn(const hla_block_mask *mask, int64_t B, int64_t heads, int6
 extern "C" {
 
 static hla_status attn_fwd(const void *q, const void *k, const void *v, const int32_t *order,
-                           const hla_block_mask *mask, void *out, float *lse, int64_t B,
-                           int64_t heads, int64_t N, int64_t d, hla_dtype dtype, float scale,
-                           hla_stream_t stream, const char *name) {
+                           const float *rpb, int mode, const hla_block_mask *mask, void *out,
+                           float *lse, int64_t B, int64_t heads, int64_t N, int64_t d,
+                           hla_dtype dtype, float scale, hla_stream_t stream, const char *name) {
   hla_status st;
   if ((st = check_tensor_args(q, "q")) != HLA_OK) return st;
   if ((st = check_tensor_args(k, "k")) != HLA_OK) return st;
@@ -263,14 +263,18 @@ static hla_status attn_fwd(const void *q, const void *k, const void *v, const in
   a.out = out;
   a.lse = lse;
   a.order = order;
+  a.rpb = rpb;
+  a.mode = mode;
   a.n_full = mask->n_full;
   a.full_idx = mask->full_idx;
   a.n_part = mask->n_part;
   a.part_idx = mask->part_idx;
   a.BH = (int32_t)BH;
+  a.heads = (int32_t)heads;
   a.N = (int32_t)N;
   a.n_qtiles = mask->n_qtiles;
   a.n_ktiles = mask->n_ktiles;
+  a.scale = scale;
   a.scale_log2 = (float)((double)scale * 1.4426950408889634074);
   a.pat = hla::make_pattern_args(mask->pat);
   hipError_t e = dtype == HLA_BF16
@@ -282,8 +286,8 @@ static hla_status attn_fwd(const void *q, const void *k, const void *v, const in
 hla_status hla_attn_fwd(const void *q, const void *k, const void *v, const hla_block_mask *mask,
                         void *out, float *lse, int64_t B, int64_t heads, int64_t N, int64_t d,
                         hla_dtype dtype, float scale, hla_stream_t stream) {
-  return attn_fwd(q, k, v, nullptr, mask, out, lse, B, heads, N, d, dtype, scale, stream,
-                  "hla_attn_fwd");
+  return attn_fwd(q, k, v, nullptr, nullptr, hla::ATTN_PLAIN, mask, out, lse, B, heads, N, d,
+                  dtype, scale, stream, "hla_attn_fwd");
 }
 
 hla_status hla_attn_fwd_perm(const void *q, const void *k, const void *v, const int32_t *order,
@@ -295,8 +299,32 @@ hla_status hla_attn_fwd_perm(const void *q, const void *k, const void *v, const 
   for (const void *t : {q, k, v, (const void *)out})
     if (t && overlaps(order, N * 4, t, B * heads * N * d * dtype_size(dtype)))
       return fail(HLA_ERR_INVALID_ARG, "order overlaps a tensor");
-  return attn_fwd(q, k, v, order, mask, out, lse, B, heads, N, d, dtype, scale, stream,
-                  "hla_attn_fwd_perm");
+  return attn_fwd(q, k, v, order, nullptr, hla::ATTN_GATHER, mask, out, lse, B, heads, N, d,
+                  dtype, scale, stream, "hla_attn_fwd_perm");
+}
+
+hla_status hla_attn_fwd_rpb(const void *q, const void *k, const void *v, const int32_t *order,
+                            const float *rpb, const hla_block_mask *mask, void *out, float *lse,
+                            int64_t B, int64_t heads, int64_t N, int64_t d, hla_dtype dtype,
+                            float scale, hla_stream_t stream) {
+  if (!order) return fail(HLA_ERR_INVALID_ARG, "order is NULL");
+  if (!aligned(order, 16)) return fail(HLA_ERR_INVALID_ARG, "order is not 16-byte aligned");
+  if (!rpb) return fail(HLA_ERR_INVALID_ARG, "rpb is NULL");
+  if (!aligned(rpb, 4)) return fail(HLA_ERR_INVALID_ARG, "rpb is not 4-byte aligned");
+  if (!mask) return fail(HLA_ERR_INVALID_ARG, "mask is NULL");
+  if (heads <= 0 || heads > (1 << 20)) return fail(HLA_ERR_INVALID_ARG, "heads must be in [1, 2^20]");
+  const int64_t tab = (2LL * mask->pat.H - 1) * (2LL * mask->pat.W - 1);
+  if (mask->pat.H <= 0 || mask->pat.W <= 0 || tab * heads > kMaxI32)
+    return fail(HLA_ERR_UNSUPPORTED, "bias table of %lld entries per head is too large", (long long)tab);
+  const int64_t tbytes = B * heads * N * d * dtype_size(dtype);
+  for (const void *t : {q, k, v, (const void *)out}) {
+    if (t && overlaps(order, N * 4, t, tbytes)) return fail(HLA_ERR_INVALID_ARG, "order overlaps a tensor");
+    if (t && overlaps(rpb, tab * heads * 4, t, tbytes)) return fail(HLA_ERR_INVALID_ARG, "rpb overlaps a tensor");
+  }
+  if (lse && overlaps(rpb, tab * heads * 4, lse, B * heads * N * 4))
+    return fail(HLA_ERR_INVALID_ARG, "rpb overlaps lse");
+  return attn_fwd(q, k, v, order, rpb, hla::ATTN_RPB, mask, out, lse, B, heads, N, d, dtype, scale,
+                  stream, "hla_attn_fwd_rpb");
 }
 
 hla_status hla_attn_bwd(const void *q, const void *k, const void *v, const void *out,

@@ -82,14 +82,21 @@ hipError_t launch_block_mask(const PatternArgs &pat, int32_t tile_m,
                              const BlockLists &rows, const BlockLists *cols,
                              int32_t *totals, hipStream_t s);
 
+// Forward modes: plain (tensors in sequence order), gather (tensors in grid
+// order, sequence position i is row order[i]), rpb (tensors in sequence order,
+// plus the global relative position bias looked up from the grid cells order[i]).
+enum AttnMode { ATTN_PLAIN = 0, ATTN_GATHER = 1, ATTN_RPB = 2 };
+
 struct AttnArgs {
   const void *q, *k, *v;
   void *out;
   float *lse;
-  const int32_t *order;  // NULL: tensors in sequence order; else row of position i
+  const int32_t *order;  // grid row of each sequence position (gather, rpb), else NULL
+  const float *rpb;      // rpb: [heads, 2H-1, 2W-1] bias table, else NULL
+  int32_t mode;          // AttnMode
   const int32_t *n_full, *full_idx, *n_part, *part_idx;
-  int32_t BH, N, n_qtiles, n_ktiles;
-  float scale_log2;  // scale * log2(e)
+  int32_t BH, heads, N, n_qtiles, n_ktiles;
+  float scale, scale_log2;  // scale, scale * log2(e)
   PatternArgs pat;
 };
 

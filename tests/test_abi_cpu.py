@@ -170,6 +170,26 @@ def test_attn_fwd_perm_validation(L):
     assert call(vp(0x800000), m=fake_mask(tm=256, tn=64)) == hla.HLA_ERR_UNSUPPORTED
 
 
+def test_attn_fwd_rpb_validation(L):
+    """Every call here is invalid, so nothing is launched."""
+    vp = ctypes.c_void_p
+    q, k, v, o = vp(0x100000), vp(0x200000), vp(0x300000), vp(0x400000)
+    N = 4096
+
+    def call(order, rpb, m=None, d=64):
+        m = m or fake_mask()
+        return L.hla_attn_fwd_rpb(q, k, v, order, rpb, ctypes.byref(m), o, None, 2, 4, N, d,
+                                  hla.HLA_BF16, 0.125, None)
+
+    good_o, good_t = vp(0x800000), vp(0x900000)
+    assert call(None, good_t) == hla.HLA_ERR_INVALID_ARG and "order" in L.hla_last_error().decode()
+    assert call(vp(0x800004), good_t) == hla.HLA_ERR_INVALID_ARG
+    assert call(good_o, None) == hla.HLA_ERR_INVALID_ARG and "rpb" in L.hla_last_error().decode()
+    assert call(good_o, vp(0x900002)) == hla.HLA_ERR_INVALID_ARG
+    assert call(good_o, vp(0x100000 + 64)) == hla.HLA_ERR_INVALID_ARG and "overlap" in L.hla_last_error().decode()
+    assert call(good_o, good_t, d=48) == hla.HLA_ERR_UNSUPPORTED
+
+
 def test_build_block_mask_rejects_partial_column_lists(L):
     m = hla.BlockMaskStruct()
     m.pat = desc("hilbert_slide", 64, 64, 128)

@@ -10,9 +10,14 @@ skipped, full tiles run unmasked, partial tiles need the element mask.
 The per-query-tile-row lists hold the key-tile indices of the full and of the
 partial tiles in ascending order, padded with -1 to n_ktiles entries.
 
-Tile sizes must divide N (the paper's ragged grids do not reproduce its
-printed sparsity under ceil-tiling, so no convention for ragged tiles is
-assumed).
+Ragged tiles (N not a multiple of a tile size; the paper's 56 x 56 grid at
+block 128, Tables 3 and 6, is one). The paper does not say how it cuts the
+ragged edge. Reading used here: the tile grid is ceil(N / tile_m) x
+ceil(N / tile_n), and the sequence is padded to whole tiles with positions that
+attend nothing and that nothing attends. A tile is full only when all of its
+tile_m * tile_n slots are real and allowed, so a tile reaching past N is never
+full; it is empty when none of its slots is allowed. With this reading the
+printed sparsity of every 56 x 56 row reproduces (see block_sparsity).
 """
 from __future__ import annotations
 
@@ -49,15 +54,16 @@ class BlockMask:
 def tile_counts(pattern, tile_m: int, tile_n: int, qtiles=None) -> np.ndarray:
     """Number of allowed elements in every tile of the requested query-tile rows."""
     N = int(pattern.H) * int(pattern.W)
-    if N % tile_m or N % tile_n:
-        raise ValueError("tile sizes must divide N")
-    nq, nk = N // tile_m, N // tile_n
+    if tile_m < 1 or tile_n < 1:
+        raise ValueError("tile sizes must be positive")
+    nq, nk = -(-N // tile_m), -(-N // tile_n)
     rows = range(nq) if qtiles is None else list(qtiles)
     cols = np.arange(N, dtype=np.int64)
     out = np.zeros((len(rows), nk), dtype=np.int64)
     for r, qt in enumerate(rows):
-        qi = np.arange(qt * tile_m, (qt + 1) * tile_m, dtype=np.int64)
-        m = masks.allowed(pattern, qi[:, None], cols[None, :])
+        qi = np.arange(qt * tile_m, min(N, (qt + 1) * tile_m), dtype=np.int64)
+        m = np.zeros((tile_m, nk * tile_n), dtype=bool)      # padded slots stay False
+        m[:len(qi), :N] = masks.allowed(pattern, qi[:, None], cols[None, :])
         out[r] = m.reshape(tile_m, nk, tile_n).sum(axis=(0, 2))
     return out
 
@@ -93,6 +99,18 @@ def build(pattern, tile_m: int, tile_n: int, qtiles=None) -> BlockMask:
 
 def empty_fraction(pattern, tile_m: int, tile_n: int) -> float:
     return float((classify(pattern, tile_m, tile_n) == EMPTY).mean())
+
+
+def block_sparsity(pattern, block: int) -> float:
+    """The tables' "Sparsity" at block size b: the share of the N x N score matrix
+    outside the non-empty b x b blocks, each block counted at its full area b^2,
+    i.e. 1 - (non-empty blocks) * b^2 / N^2. When b divides N this is the share of
+    empty blocks; on a ragged grid (56 x 56 at b = 128) the padded part of the edge
+    blocks is counted too, which is how the printed values come out."""
+    N = int(pattern.H) * int(pattern.W)
+    cls = classify(pattern, block, block)
+    nonempty = int((cls != EMPTY).sum())
+    return 1.0 - nonempty * block * block / float(N * N)
 
 
 def column_lists(cls: np.ndarray) -> BlockMask:

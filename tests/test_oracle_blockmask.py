@@ -20,8 +20,10 @@ def test_paper_sparsity(row):
     (kind, H, W, p0, p1, block, printed), source = row
     pat = Pat(kind, H, W, p0, p1)
     b = int(block)
-    pct = 100.0 * blockmask.empty_fraction(pat, b, b)
+    pct = 100.0 * blockmask.block_sparsity(pat, b)
     assert round(pct, 2) == pytest.approx(float(printed), abs=1e-9), (source, pct)
+    if (pat.H * pat.W) % b == 0:   # whole tiles: the same number as the share of empty tiles
+        assert pct == pytest.approx(100.0 * blockmask.empty_fraction(pat, b, b), abs=1e-9)
 
 
 @pytest.mark.parametrize("row", FIG3, ids=[s for _, s in FIG3])
@@ -93,16 +95,19 @@ def test_band_counts_for_the_slide_workload():
 
 
 def brute_force_tiny(pat, bm, bn):
-    """Literal element-by-element loop (tiny grids only)."""
+    """Literal element-by-element loop (tiny grids only). Slots past N (ragged edge
+    tiles) are never allowed."""
     N = pat.H * pat.W
     m = masks.dense(pat)
-    cls = np.zeros((N // bm, N // bn), dtype=np.int8)
-    for qt in range(N // bm):
-        for kt in range(N // bn):
+    nq, nk = (N + bm - 1) // bm, (N + bn - 1) // bn
+    cls = np.zeros((nq, nk), dtype=np.int8)
+    for qt in range(nq):
+        for kt in range(nk):
             c = 0
             for i in range(qt * bm, qt * bm + bm):
                 for j in range(kt * bn, kt * bn + bn):
-                    c += int(m[i, j])
+                    if i < N and j < N:
+                        c += int(m[i, j])
             cls[qt, kt] = 0 if c == 0 else (2 if c == bm * bn else 1)
     return cls
 
@@ -118,6 +123,47 @@ def brute_force_tiny(pat, bm, bn):
 ])
 def test_classifier_matches_literal_loop(pat, bm, bn):
     assert np.array_equal(blockmask.classify(pat, bm, bn), brute_force_tiny(pat, bm, bn))
+
+
+@pytest.mark.parametrize("pat,bm,bn", [
+    (Pat("rowmajor_window", 7, 7, 3, 2), 8, 4),
+    (Pat("rowmajor_slide", 5, 9, 1, 2), 16, 8),
+    (Pat("hilbert_window", 7, 7, 8), 4, 16),
+    (Pat("hilbert_slide", 6, 5, 3), 8, 8),
+    (Pat("hilbert_neighborhood", 7, 6, 9), 16, 4),
+    (Pat("rowmajor_neighborhood", 7, 7, 3, 3), 8, 16),
+    (Pat("hilbert_shifted_window", 9, 7, 8, 3), 8, 8),
+])
+def test_ragged_classifier_matches_literal_loop(pat, bm, bn):
+    """N not a multiple of the tiles: ceil(N / b) tiles per axis, padded slots never allowed."""
+    cls = blockmask.classify(pat, bm, bn)
+    assert np.array_equal(cls, brute_force_tiny(pat, bm, bn))
+    N = pat.H * pat.W
+    assert cls.shape == ((N + bm - 1) // bm, (N + bn - 1) // bn)
+    if N % bn:
+        assert (cls[:, -1] != blockmask.FULL).all()     # an edge tile is never full
+    if N % bm:
+        assert (cls[-1, :] != blockmask.FULL).all()
+
+
+@pytest.mark.parametrize("H,W,h,bm,bn", [(56, 56, 24, 128, 64), (56, 56, 512, 128, 128),
+                                         (10, 10, 7, 64, 16), (7, 9, 0, 16, 32)])
+def test_ragged_band_interval_bounds(H, W, h, bm, bn):
+    """Band on a ragged tiling: the tile's real index ranges are intervals clipped at N - 1;
+    empty iff their closest pair is farther than h, full iff the tile is whole and its
+    farthest pair is within h."""
+    N = H * W
+    cls = blockmask.classify(Pat("hilbert_slide", H, W, h), bm, bn)
+    for qt in range((N + bm - 1) // bm):
+        i0, i1 = qt * bm, min(N, qt * bm + bm) - 1
+        for kt in range((N + bn - 1) // bn):
+            j0, j1 = kt * bn, min(N, kt * bn + bn) - 1
+            whole = i1 - i0 + 1 == bm and j1 - j0 + 1 == bn
+            dmin = max(0, j0 - i1, i0 - j1)
+            dmax = max(abs(i0 - j1), abs(i1 - j0))
+            want = (blockmask.EMPTY if dmin > h else
+                    blockmask.FULL if whole and dmax <= h else blockmask.PARTIAL)
+            assert cls[qt, kt] == want
 
 
 def test_lists_are_ascending_and_padded():

@@ -87,7 +87,10 @@ typedef struct {
  * Block-sparse metadata (Sec. 3.1: full / partial / empty blocks; the paper's
  * engine keeps only this lightweight block metadata, Sec. 4.2).
  * The N x N score matrix is cut into tiles of tile_m query rows by tile_n key
- * columns. For query-tile row q:
+ * columns: n_qtiles = ceil(N / tile_m), n_ktiles = ceil(N / tile_n). When a tile
+ * size does not divide N (the paper's 56x56 grid at block 128, Tables 3 and 6)
+ * the last tiles reach past N; their padded slots are never allowed, so such a
+ * tile is partial or empty, never full. For query-tile row q:
  *   n_full[q]            number of full tiles
  *   full_idx[q*n_ktiles + t], t < n_full[q]: key-tile indices, ascending
  *   n_part[q], part_idx  the same for partial tiles
@@ -152,8 +155,9 @@ hla_status hla_scatter(const void *src, void *dst, const int32_t *order,
 
 /*
  * Host-only: tile-grid sizes for a pattern and tile, so the caller can size the
- * block-mask arrays. N = H*W must be a multiple of tile_m and of tile_n; tile
- * sizes are powers of two in [16, 1024]. Pattern parameters must be >= 1
+ * block-mask arrays: n_qtiles = ceil(N / tile_m), n_ktiles = ceil(N / tile_n),
+ * N = H*W (any N; tiles may be ragged). Tile sizes are powers of two in
+ * [16, 1024]. Pattern parameters must be >= 1
  * (slide radii and half-widths >= 0; neighbourhood kernels <= the grid extent).
  */
 hla_status hla_block_mask_dims(const hla_pattern_desc *pat, int32_t tile_m,
@@ -182,8 +186,8 @@ hla_status hla_build_block_mask(hla_block_mask *mask, hla_stream_t stream);
  * out may not alias q, k or v. The mask must have been built for this N.
  * bf16: products on bf16 matrix cores, fp32 accumulation and softmax, out
  * rounded to bf16. f32: fp32 arithmetic throughout.
- * Supported: d in {32, 64}; tile_m in {64, 128}; tile_n == 64;
- * otherwise UNSUPPORTED.
+ * Supported: d in {32, 64}; tile_m in {64, 128}; tile_n == 64 (any N: on a
+ * ragged tiling only rows < N are read or written); otherwise UNSUPPORTED.
  */
 hla_status hla_attn_fwd(const void *q, const void *k, const void *v,
                         const hla_block_mask *mask, void *out, float *lse,

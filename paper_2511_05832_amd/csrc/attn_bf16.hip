@@ -60,6 +60,12 @@
 // -inf before the row max; a query with no allowed key so far keeps m = -inf and
 // contributes exactly zero.
 //
+// Ragged tilings (N not a multiple of the tile): a key tile reaching past the
+// end of the sequence is always in the partial list, its rows past N - 1 are
+// copied from row N - 1 and the mask (every allowed region is clipped at N - 1)
+// drops them; query rows past N - 1 load row N - 1 and store nothing. Every
+// global access stays inside the tensors.
+//
 // Grid: one workgroup per (b*h, query tile), remapped so each XCD (workgroups
 // are dealt round-robin to the 8 XCDs) receives a contiguous range of query
 // tiles: neighbouring tiles share key/value tiles (a window is two query tiles;
@@ -208,11 +214,13 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2
 #pragma unroll
       for (int j = 0; j < CPW; ++j) roff[j] = (int64_t)rows[krow[j]] * D;
     } else {
-      const int kt = tile_of(i);
-      Kt = K + (int64_t)kt * BN * D;
-      Vt = V + (int64_t)kt * BN * D;
+      // rows past the end of the sequence (ragged last key tile) read row N - 1;
+      // the mask of that (always partial) tile drops them
+      const int k0 = tile_of(i) * BN;
+      Kt = K;
+      Vt = V;
 #pragma unroll
-      for (int j = 0; j < CPW; ++j) roff[j] = krow[j] * D;
+      for (int j = 0; j < CPW; ++j) roff[j] = (int64_t)min(k0 + krow[j], a.N - 1) * D;
     }
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
@@ -221,17 +229,18 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2
     for (int j = 0; j < CPW; ++j)
       lds_dma16(Vt + roff[j] + vch[j], lds_addr(base + TILE + (j * NW + wave) * 1024));
   };
-  // GATHER: the row indices of list entry i (16 bytes per lane of the first
-  // wave) into its slot. RPB: every wave copies BN / NW of them.
+  // GATHER: the row indices of list entry i (one per lane of the first wave)
+  // into its slot. RPB: every wave copies BN / NW of them. Positions past the end
+  // of the sequence read entry N - 1.
   auto issue_idx = [&](int i) {
     if constexpr (GATHER) {
-      if (wave == 0 && lane < BN / 4)
-        lds_dma16(a.order + (int64_t)tile_of(i) * BN + 4 * lane, lds_addr(lds + IDXK + (i & 3) * BN * 4));
+      if (wave == 0)
+        lds_dma4(a.order + min(tile_of(i) * BN + lane, a.N - 1), lds_addr(lds + IDXK + (i & 3) * BN * 4));
     } else {
       constexpr int PER = BN / NW;   // ids per wave
-      if (lane < PER / 4)
-        lds_dma16(a.order + (int64_t)tile_of(i) * BN + wave * PER + 4 * lane,
-                  lds_addr(lds + IDXK + (i & 3) * BN * 4 + wave * PER * 4));
+      if (lane < PER)
+        lds_dma4(a.order + min(tile_of(i) * BN + wave * PER + lane, a.N - 1),
+                 lds_addr(lds + IDXK + (i & 3) * BN * 4 + wave * PER * 4));
     }
   };
 
@@ -272,8 +281,11 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2
   // in flight before its first use in the loop.
   if constexpr (GATHER) {
     // Row indices of the Q tile and of the first three key tiles, first.
-    if (wave == 0 && lane < BM / 4)
-      lds_dma16(a.order + (int64_t)qt * BM + 4 * lane, lds_addr(lds + IDXQ));
+    if (wave == 0) {
+#pragma unroll
+      for (int c = 0; c < BM / 64; ++c)
+        lds_dma4(a.order + min(qt * BM + 64 * c + lane, a.N - 1), lds_addr(lds + IDXQ + 256 * c));
+    }
 #pragma unroll
     for (int i = 0; i < 3; ++i)
       if (i < ntot) issue_idx(i);
@@ -285,7 +297,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2
     for (int j = 0; j < LQ; ++j) {
       const int p = (j * NW + wave) * 64 + lane;
       const int r = p / CPR, cs = p % CPR;
-      const int64_t row = GATHER ? (int64_t)idx_q[r] : (int64_t)qt * BM + r;
+      const int64_t row = GATHER ? (int64_t)idx_q[r] : (int64_t)min(qt * BM + r, a.N - 1);
       lds_dma16(Q + row * D + (cs ^ swz_q<D>(r)) * 8, lds_addr(base + (j * NW + wave) * 1024));
     }
   }
@@ -302,7 +314,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2
   int32_t rpb_base = 0;
   const float *rpb_h = nullptr;
   if constexpr (RPB) {
-    const int32_t g = a.order[qpos];
+    const int32_t g = a.order[min(qpos, a.N - 1)];
     const int32_t Wg = P.W;
     rpb_base = (P.H - 1) * (2 * Wg - 1) + (Wg - 1) + g + (Wg - 1) * (int32_t)fdiv((uint32_t)g, P.wdiv);
     rpb_h = a.rpb + (int64_t)(bh % a.heads) * (2 * P.H - 1) * (2 * Wg - 1);
@@ -452,6 +464,9 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2
   // of groups gives each lane eight consecutive values (16 bytes) to store.
   const float l_tot = xhalf_sum(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  // (queries past the end of the sequence, in a ragged last query tile, take part
+  // in the exchanges but store nothing)
+  const bool live = qpos < a.N;
   const int64_t out_row = GATHER ? (int64_t)idx_q[wave * 32 + col] : (int64_t)qpos;
   __bf16 *orow = static_cast<__bf16 *>(a.out) + slice + out_row * D;
 #pragma unroll
@@ -472,9 +487,9 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2
       recv.x = __shfl_xor(send.x, 32);
       recv.y = __shfl_xor(send.y, 32);
       const uint4 row = half ? uint4{recv.x, recv.y, u1.x, u1.y} : uint4{u0.x, u0.y, recv.x, recv.y};
-      *reinterpret_cast<uint4 *>(orow + db * 32 + 16 * pr + 8 * half) = row;
+      if (live) *reinterpret_cast<uint4 *>(orow + db * 32 + 16 * pr + 8 * half) = row;
     }
-  if (a.lse && half == 0) {
+  if (a.lse && half == 0 && live) {
     const float ln2 = 0.69314718055994530942f;
     a.lse[(int64_t)bh * a.N + out_row] =
         l_tot > 0.f ? (m_run + __builtin_amdgcn_logf(l_tot)) * ln2 : -__builtin_inff();

@@ -77,14 +77,17 @@ __device__ __forceinline__ void stage_rows(const f32x16 *acc, float mul, __bf16 
       *reinterpret_cast<bf16x4 *>(Os + col * OS + db * 32 + 8 * g + 4 * half) = o4;
     }
 }
+// Only the first `nrows` rows are written (rows past the end of the sequence in
+// a ragged last tile are not).
 template <int D>
-__device__ __forceinline__ void write_rows(const __bf16 *Os, __bf16 *dst, int lane) {
+__device__ __forceinline__ void write_rows(const __bf16 *Os, __bf16 *dst, int lane, int nrows) {
   constexpr int OS = D + 8, CPR = D / 8;
 #pragma unroll
   for (int i = lane; i < 32 * CPR; i += 64) {
     const int r = i / CPR, c = i % CPR;
-    *reinterpret_cast<uint4 *>(dst + r * D + c * 8) =
-        *reinterpret_cast<const uint4 *>(Os + r * OS + c * 8);
+    if (r < nrows)
+      *reinterpret_cast<uint4 *>(dst + r * D + c * 8) =
+          *reinterpret_cast<const uint4 *>(Os + r * OS + c * 8);
   }
 }
 
@@ -137,23 +140,28 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
   const int32_t *prow = a.part_idx + (int64_t)qt * a.n_ktiles;
   auto tile_of = [&](int i) { return i < nf ? sload(frow + i) : sload(prow + i - nf); };
 
-  int off[CPW];
+  // Row within the tile and chunk offset of this thread's copies. Rows past the
+  // end of the sequence (ragged last key tile, always partial) read row N - 1
+  // and are masked.
+  int offr[CPW], offc[CPW];
 #pragma unroll
   for (int j = 0; j < CPW; ++j) {
     const int p = (j * NW + wave) * 64 + lane;
     const int r = p / CPR, cs = p % CPR;
-    off[j] = r * D + (cs ^ swz<D>(r)) * 8;
+    offr[j] = r;
+    offc[j] = (cs ^ swz<D>(r)) * 8;
   }
   auto issue_tile = [&](int kt, int stage) {
-    const __bf16 *Kt = K + (int64_t)kt * BN * D;
-    const __bf16 *Vt = V + (int64_t)kt * BN * D;
     char *base = lds + stage * STAGE;
+    int64_t roff[CPW];
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) roff[j] = (int64_t)min(kt * BN + offr[j], a.N - 1) * D + offc[j];
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
-      lds_dma16(Kt + off[j], lds_addr(base + (j * NW + wave) * 1024));
+      lds_dma16(K + roff[j], lds_addr(base + (j * NW + wave) * 1024));
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
-      lds_dma16(Vt + off[j], lds_addr(base + TILE + (j * NW + wave) * 1024));
+      lds_dma16(V + roff[j], lds_addr(base + TILE + (j * NW + wave) * 1024));
   };
 
   int raddr[2][NCH];
@@ -178,13 +186,15 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
   // The wave's own q and dout rows and row statistics, loaded after the first
   // copies so that both latencies overlap; one wait the compiler can see then
   // covers all of them, so it inserts no wait of its own inside the loop.
+  // (a query row past the end of the sequence reads row N - 1 and stores nothing)
+  const int qc = min(qpos, a.N - 1);
   bf16x8 qop[NCH], gop[NCH];
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
-    qop[c] = *reinterpret_cast<const bf16x8 *>(Q + (int64_t)qpos * D + half * (D / 2) + 8 * c);
-    gop[c] = *reinterpret_cast<const bf16x8 *>(G + (int64_t)qpos * D + half * (D / 2) + 8 * c);
+    qop[c] = *reinterpret_cast<const bf16x8 *>(Q + (int64_t)qc * D + half * (D / 2) + 8 * c);
+    gop[c] = *reinterpret_cast<const bf16x8 *>(G + (int64_t)qc * D + half * (D / 2) + 8 * c);
   }
-  const float2 rs = *reinterpret_cast<const float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qpos));
+  const float2 rs = *reinterpret_cast<const float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qc));
   const float lse2 = rs.x, delta = rs.y;
   wait_vmem_all();
 
@@ -230,7 +240,8 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
   __bf16 *Os = reinterpret_cast<__bf16 *>(lds) + wave * 32 * (D + 8);
   stage_rows<D>(acc, a.scale, Os, col, half);
   __syncthreads();
-  write_rows<D>(Os, static_cast<__bf16 *>(a.dq) + slice + (int64_t)(q0 + wave * 32) * D, lane);
+  write_rows<D>(Os, static_cast<__bf16 *>(a.dq) + slice + (int64_t)(q0 + wave * 32) * D, lane,
+                a.N - (q0 + wave * 32));
 }
 
 // ---------------------------------------------------------------------------
@@ -253,7 +264,7 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   constexpr int SOFF = 2 * QT;          // stats pairs after Q and dout
   constexpr int STAGE = 2 * QT + BMQ * 8;
   constexpr int CPW = BMQ * CPR / NT;   // 16-byte copies per thread per tile (Q or dout)
-  constexpr int SL = BMQ / 8;           // stats copies per wave (16 bytes = 2 rows each)
+  constexpr int SL = BMQ / 2;           // stats values copied per wave (4 bytes each)
   constexpr int LPT = 2 * CPW + 1;
   constexpr int QB = BMQ / 64;
   constexpr int HALF = BMQ / 2;
@@ -264,6 +275,7 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   constexpr int LDSB = kStagesKv * STAGE > EPI ? kStagesKv * STAGE : EPI;
   static_assert(CPW >= 1 && BMQ * CPR % NT == 0, "tile copies must split evenly");
   static_assert(SL <= 64, "stats copies exceed a wave");
+  static_assert(4 * SL * 4 == BMQ * 8, "the waves' stats copies cover the tile's rows");
 
   __shared__ __attribute__((aligned(16))) char lds[LDSB];
 
@@ -293,26 +305,33 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   const int32_t *pcol = a.part_idx_t + (int64_t)kt * a.n_qtiles;
   auto tile_of = [&](int i) { return i < nf ? sload(fcol + i) : sload(pcol + i - nf); };
 
-  int off[CPW];
+  // Query rows past the end of the sequence (ragged last query tile, always
+  // partial) read row N - 1 and are masked.
+  int offr[CPW], offc[CPW];
 #pragma unroll
   for (int j = 0; j < CPW; ++j) {
     const int p = (j * 4 + wave) * 64 + lane;
     const int r = p / CPR, cs = p % CPR;
-    off[j] = r * D + (cs ^ swz<D>(r)) * 8;
+    offr[j] = r;
+    offc[j] = (cs ^ swz<D>(r)) * 8;
   }
   auto issue_tile = [&](int qt, int stage) {
-    const __bf16 *Qt = Q + (int64_t)qt * BMQ * D;
-    const __bf16 *Gt = G + (int64_t)qt * BMQ * D;
     char *base = lds + stage * STAGE;
+    int64_t roff[CPW];
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) roff[j] = (int64_t)min(qt * BMQ + offr[j], a.N - 1) * D + offc[j];
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
-      lds_dma16(Qt + off[j], lds_addr(base + (j * 4 + wave) * 1024));
+      lds_dma16(Q + roff[j], lds_addr(base + (j * 4 + wave) * 1024));
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
-      lds_dma16(Gt + off[j], lds_addr(base + QT + (j * 4 + wave) * 1024));
-    if (lane < SL)
-      lds_dma16(S + 2 * ((int64_t)qt * BMQ) + 4 * (wave * SL + lane),
-                      lds_addr(base + SOFF + wave * SL * 16));
+      lds_dma16(G + roff[j], lds_addr(base + QT + (j * 4 + wave) * 1024));
+    // stats value f of the tile = component f % 2 of row f / 2
+    if (lane < SL) {
+      const int f = wave * SL + lane;
+      lds_dma4(S + 2 * (int64_t)min(qt * BMQ + f / 2, a.N - 1) + (f & 1),
+               lds_addr(base + SOFF + wave * SL * 4));
+    }
   };
 
   int raddr[QB][NCH];
@@ -338,11 +357,13 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   // The wave's own k and v rows, loaded after the first copy so that both
   // latencies overlap; one wait the compiler can see then covers both, so it
   // inserts no wait of its own inside the loop.
+  // (a key row past the end of the sequence reads row N - 1 and stores nothing)
+  const int kc = min(kpos, a.N - 1);
   bf16x8 kop[NCH], vop[NCH];
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
-    kop[c] = *reinterpret_cast<const bf16x8 *>(K + (int64_t)kpos * D + half * (D / 2) + 8 * c);
-    vop[c] = *reinterpret_cast<const bf16x8 *>(V + (int64_t)kpos * D + half * (D / 2) + 8 * c);
+    kop[c] = *reinterpret_cast<const bf16x8 *>(K + (int64_t)kc * D + half * (D / 2) + 8 * c);
+    vop[c] = *reinterpret_cast<const bf16x8 *>(V + (int64_t)kc * D + half * (D / 2) + 8 * c);
   }
   wait_vmem_all();
 
@@ -430,7 +451,7 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   stage_rows<D>(res, qh == 0 ? a.scale : 1.f, Os, col, half);
   __syncthreads();
   __bf16 *dst = static_cast<__bf16 *>(qh == 0 ? a.dk : a.dv) + slice + (int64_t)(k0 + kb * 32) * D;
-  write_rows<D>(Os, dst, lane);
+  write_rows<D>(Os, dst, lane, a.N - (k0 + kb * 32));
 }
 
 template <int D, int NW>

@@ -92,6 +92,10 @@ __device__ __forceinline__ Region region_of(const PatternArgs &P, int x) {
       neigh_bwd(c, P.p1, P.W, R.clo, R.chi);
     }
   }
+  // Clip at the end of the sequence: on a ragged tiling the edge tiles hold
+  // padded positions >= N (grid rows >= H), which pair with nothing.
+  R.hi = min(R.hi, P.N - 1);
+  R.rhi = min(R.rhi, P.H - 1);
   return R;
 }
 
@@ -191,6 +195,17 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p) {
 __device__ __forceinline__ void lds_dma16(const void *src, uint32_t dst) {
 #if defined(__HIP_DEVICE_COMPILE__)
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(dst))
+               : "memory", "m0");
+#endif
+}
+// The same copy with 4 bytes per lane (lane l lands at dst + 4 l; lanes that are
+// switched off write nothing): row indices, where each lane clamps its own source
+// position at the end of the sequence.
+__device__ __forceinline__ void lds_dma4(const void *src, uint32_t dst) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
                :
                : "v"(src), "s"(__builtin_amdgcn_readfirstlane(dst))
                : "memory", "m0");

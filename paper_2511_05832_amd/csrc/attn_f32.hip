@@ -35,7 +35,12 @@ __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
   const float *K = static_cast<const float *>(a.k) + slice;
   const float *V = static_cast<const float *>(a.v) + slice;
 
-  const int64_t qrow = GATHER ? (int64_t)a.order[qpos] : (int64_t)qpos;
+  // A query row past the end of the sequence (ragged last query tile) reads row
+  // N - 1 and stores nothing; key rows past it read row N - 1 and are masked
+  // (such a tile is always partial and every allowed region ends at N - 1).
+  const bool live = qpos < a.N;
+  const int qc = min(qpos, a.N - 1);
+  const int64_t qrow = GATHER ? (int64_t)a.order[qc] : (int64_t)qc;
   float q[D], acc[D];
 #pragma unroll
   for (int i = 0; i < D; i += 4) {
@@ -57,7 +62,7 @@ __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
   int32_t rpb_base = 0;
   const float *rpb_h = nullptr;
   if constexpr (RPB) {
-    const int32_t g = a.order[qpos];
+    const int32_t g = a.order[qc];
     rpb_base = (P.H - 1) * (2 * P.W - 1) + (P.W - 1) + g + (P.W - 1) * (int32_t)fdiv((uint32_t)g, P.wdiv);
     rpb_h = a.rpb + (int64_t)(bh % a.heads) * (2 * P.H - 1) * (2 * P.W - 1);
   }
@@ -68,7 +73,8 @@ __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
     __syncthreads();
     for (int i = tid; i < BN * D / 4; i += BM) {
       const int r = i / (D / 4), c4 = i % (D / 4);
-      const int64_t row = GATHER ? (int64_t)a.order[kt * BN + r] : (int64_t)kt * BN + r;
+      const int pos = min(kt * BN + r, a.N - 1);
+      const int64_t row = GATHER ? (int64_t)a.order[pos] : (int64_t)pos;
       reinterpret_cast<float4 *>(Ks)[i] = reinterpret_cast<const float4 *>(K + row * D)[c4];
       reinterpret_cast<float4 *>(Vs)[i] = reinterpret_cast<const float4 *>(V + row * D)[c4];
     }
@@ -82,7 +88,7 @@ __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
         for (int i = 0; i < D; ++i) dot = __builtin_fmaf(q[i], Ks[(j0 + j) * D + i], dot);
         s[j] = dot;
         if constexpr (RPB) {
-          const int32_t gk = a.order[kt * BN + j0 + j];
+          const int32_t gk = a.order[min(kt * BN + j0 + j, a.N - 1)];
           const int32_t koff = gk + (P.W - 1) * (int32_t)fdiv((uint32_t)gk, P.wdiv);
           s[j] = __builtin_fmaf(dot, a.scale, rpb_h[rpb_base - koff]);
         }
@@ -112,6 +118,7 @@ __global__ void __launch_bounds__(BM) attn_fwd_f32(AttnArgs a) {
     }
   }
 
+  if (!live) return;
   const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
   float *O = static_cast<float *>(a.out) + slice + qrow * D;
 #pragma unroll

@@ -12,6 +12,10 @@
 // condition and a column condition, so each rectangle pair is decided per axis
 // and the tile is non-empty if any pair is, full if every pair is.
 //
+// Ragged tilings (N not a multiple of a tile): the last tile row / column covers
+// the positions up to N - 1 and padded slots past them, which are never allowed;
+// such a tile is classified on its real positions and is never full.
+//
 // Layout: one workgroup per line walks the tiles of that line in chunks of 256,
 // compacts full and partial indices with wave ballots into ascending lists,
 // then pads the rest of both lists with -1. A line is a query-tile row (the
@@ -142,8 +146,11 @@ __global__ void __launch_bounds__(kThreads)
     int cls = 0;
     if (e < n_entries) {
       const int qt = COLS ? e : line, kt = COLS ? line : e;
-      cls = classify_tile(p, qt * tile_m, qt * tile_m + tile_m - 1, kt * tile_n,
-                          kt * tile_n + tile_n - 1);
+      // Ragged edge: the tile's real positions end at N - 1; the padded slots are
+      // never allowed, so a tile reaching past N is never full.
+      const int i1 = qt * tile_m + tile_m - 1, j1 = kt * tile_n + tile_n - 1;
+      cls = classify_tile(p, qt * tile_m, min(i1, p.N - 1), kt * tile_n, min(j1, p.N - 1));
+      if (cls == 2 && (i1 >= p.N || j1 >= p.N)) cls = 1;
     }
     const uint64_t bf = __ballot(cls == 2);
     const uint64_t bp = __ballot(cls == 1);

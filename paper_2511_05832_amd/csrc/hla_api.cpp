@@ -74,14 +74,10 @@ hla_status check_pattern(const hla_pattern_desc *p) {
   return HLA_OK;
 }
 
-hla_status check_tiles(const hla_pattern_desc *p, int32_t tile_m, int32_t tile_n) {
+hla_status check_tiles(int32_t tile_m, int32_t tile_n) {
   if (!is_pow2(tile_m) || !is_pow2(tile_n) || tile_m < 16 || tile_n < 16 || tile_m > 1024 ||
       tile_n > 1024)
     return fail(HLA_ERR_UNSUPPORTED, "tiles %dx%d must be powers of two in [16, 1024]", tile_m, tile_n);
-  const int64_t N = (int64_t)p->H * p->W;
-  if (N % tile_m || N % tile_n)
-    return fail(HLA_ERR_UNSUPPORTED, "N = %lld is not a multiple of the tiles %dx%d",
-                (long long)N, tile_m, tile_n);
   return HLA_OK;
 }
 
@@ -161,10 +157,10 @@ hla_status hla_block_mask_dims(const hla_pattern_desc *pat, int32_t tile_m, int3
                                int32_t *n_qtiles, int32_t *n_ktiles) {
   hla_status st;
   if ((st = check_pattern(pat)) != HLA_OK) return st;
-  if ((st = check_tiles(pat, tile_m, tile_n)) != HLA_OK) return st;
+  if ((st = check_tiles(tile_m, tile_n)) != HLA_OK) return st;
   const int64_t N = (int64_t)pat->H * pat->W;
-  if (n_qtiles) *n_qtiles = (int32_t)(N / tile_m);
-  if (n_ktiles) *n_ktiles = (int32_t)(N / tile_n);
+  if (n_qtiles) *n_qtiles = (int32_t)((N + tile_m - 1) / tile_m);
+  if (n_ktiles) *n_ktiles = (int32_t)((N + tile_n - 1) / tile_n);
   return HLA_OK;
 }
 
@@ -218,10 +214,10 @@ hla_status check_attn(const hla_block_mask *mask, int64_t B, int64_t heads, int6
     return fail(HLA_ERR_INVALID_ARG, "sizes must be positive");
   if (!(scale > 0.f) || scale > 1e30f) return fail(HLA_ERR_INVALID_ARG, "scale must be positive and finite");
   if ((st = check_pattern(&mask->pat)) != HLA_OK) return st;
-  if ((st = check_tiles(&mask->pat, mask->tile_m, mask->tile_n)) != HLA_OK) return st;
+  if ((st = check_tiles(mask->tile_m, mask->tile_n)) != HLA_OK) return st;
   const int64_t mN = (int64_t)mask->pat.H * mask->pat.W;
-  if (mask->N != mN || N != mN || mask->n_qtiles != mN / mask->tile_m ||
-      mask->n_ktiles != mN / mask->tile_n)
+  if (mask->N != mN || N != mN || mask->n_qtiles != (mN + mask->tile_m - 1) / mask->tile_m ||
+      mask->n_ktiles != (mN + mask->tile_n - 1) / mask->tile_n)
     return fail(HLA_ERR_INVALID_ARG, "mask was built for N = %d, attention has N = %lld",
                 mask->N, (long long)N);
   if (dtype != HLA_F32 && dtype != HLA_BF16) return fail(HLA_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);

@@ -89,9 +89,13 @@ def test_block_mask_dims(L):
     d = desc("hilbert_slide", 256, 256, 512)
     assert L.hla_block_mask_dims(ctypes.byref(d), 128, 64, ctypes.byref(nq), ctypes.byref(nk)) == 0
     assert (nq.value, nk.value) == (512, 1024)
+    # ragged tilings: ceil(N / tile) per axis (3136 = 24.5 * 128 = 49 * 64; 63 < 64)
+    for dd, tm, tn, want in [(desc("hilbert_slide", 56, 56, 24), 128, 64, (25, 49)),
+                             (desc("rowmajor_slide", 7, 9, 1, 1), 64, 16, (1, 4))]:
+        assert L.hla_block_mask_dims(ctypes.byref(dd), tm, tn, ctypes.byref(nq), ctypes.byref(nk)) == 0
+        assert (nq.value, nk.value) == want
     bad = [
         (desc("hilbert_slide", 64, 64, 128), 96, 64, hla.HLA_ERR_UNSUPPORTED),     # not pow2
-        (desc("hilbert_slide", 56, 56, 24), 128, 128, hla.HLA_ERR_UNSUPPORTED),    # 128 does not divide 3136
         (desc("hilbert_slide", 64, 64, -1), 128, 64, hla.HLA_ERR_INVALID_ARG),
         (desc("hilbert_window", 64, 64, 0), 128, 64, hla.HLA_ERR_INVALID_ARG),
         (desc("hilbert_shifted_window", 64, 64, 16, 16), 128, 64, hla.HLA_ERR_INVALID_ARG),

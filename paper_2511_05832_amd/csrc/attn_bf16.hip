@@ -80,6 +80,9 @@ namespace {
 
 constexpr int BN = 64;
 constexpr float kRescaleSlack = 8.f;  // log2 units the softmax reference may lag the max
+// Largest weight sum per lane and tile the max-free softmax step accepts
+// against a stale reference (2^32: far from fp32 overflow in O and l).
+constexpr float kFastBound = 4294967296.f;
 // LDS ring depth. Three 16 KiB stages (d = 64) let three workgroups share a
 // CU's 160 KiB; with the launch bound below that is the occupancy that measured
 // fastest. Four stages at two workgroups per CU were slower, also with a
@@ -271,6 +274,7 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2
   for (int db = 0; db < NDB; ++db) oacc[db] = f32x16{};
   float m_run = -__builtin_inff();  // running reference, in units of log2
   float l_run = 0.f;               // this lane's partial sum (its half of the keys)
+  bool primed = false;             // every lane's m_run is finite (wave-uniform)
   // scores are multiplied by smul to reach log2 units (RPB: already scaled)
   const float smul = RPB ? 1.44269504088896340736f : a.scale_log2;
 
@@ -358,84 +362,120 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2
     const char *st = lds + stage * STAGE;
     stage = stage == 2 ? 0 : stage + 1;
 
-    // S^T for the two 32-key blocks, independent accumulators interleaved.
-    f32x16 s[2] = {f32x16{}, f32x16{}};
+    // S^T for the two 32-key blocks (independent accumulators interleaved), the
+    // RPB bias and the mask: the tile's scores, this lane's 32 of them.
+    auto scores = [&](f32x16 (&s)[2]) {
+      s[0] = f32x16{};
+      s[1] = f32x16{};
 #pragma unroll
-    for (int c = 0; c < NCH; ++c)
+      for (int c = 0; c < NCH; ++c)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const bf16x8 kop = *reinterpret_cast<const bf16x8 *>(st + kaddr[kb][c]);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[c], s[kb], 0, 0, 0);
-      }
-    // RPB: scores in natural units plus the bias, s = scale * <q, k> + bias.
-    if constexpr (RPB) {
-      // all 32 bias loads first, so that they are in flight together
-      const int32_t *kid = idx_k(it);
-      const int32_t Wm1 = P.W - 1;
-      float bias[2][16];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int g = 0; g < 2; ++g) {
-          const int4 *ids = reinterpret_cast<const int4 *>(kid + kb * 32 + 16 * g + 8 * half);
-          const int4 lo = ids[0], hi = ids[1];
-          const int32_t gk[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int32_t koff = gk[e] + Wm1 * (int32_t)fdiv((uint32_t)gk[e], P.wdiv);
-            bias[kb][8 * g + e] = rpb_h[rpb_base - koff];
-          }
+        for (int kb = 0; kb < 2; ++kb) {
+          const bf16x8 kop = *reinterpret_cast<const bf16x8 *>(st + kaddr[kb][c]);
+          s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[c], s[kb], 0, 0, 0);
         }
+      // RPB: scores in natural units plus the bias, s = scale * <q, k> + bias.
+      if constexpr (RPB) {
+        // all 32 bias loads first, so that they are in flight together
+        const int32_t *kid = idx_k(it);
+        const int32_t Wm1 = P.W - 1;
+        float bias[2][16];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) s[kb][v] = __builtin_fmaf(s[kb][v], a.scale, bias[kb][v]);
-    }
-    if constexpr (decltype(masked)::value) mask_blocks<2>(s, R, P, tile_of(it) * BN + 8 * half);
-
-    // Online softmax in the log2 domain with a lazily moved reference: m_run
-    // only moves when a row's tile max exceeds it by more than kRescaleSlack, so
-    // the O / l rescale is rare; weights stay <= 2^kRescaleSlack and O and l
-    // always share the same reference.
-    float mq[4];
+          for (int g = 0; g < 2; ++g) {
+            const int4 *ids = reinterpret_cast<const int4 *>(kid + kb * 32 + 16 * g + 8 * half);
+            const int4 lo = ids[0], hi = ids[1];
+            const int32_t gk[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x16 &sv = s[g >> 1];
-      const int o = 8 * (g & 1);
-      mq[g] = fmaxf(fmaxf(fmaxf(sv[o], sv[o + 1]), fmaxf(sv[o + 2], sv[o + 3])),
-                    fmaxf(fmaxf(sv[o + 4], sv[o + 5]), fmaxf(sv[o + 6], sv[o + 7])));
-    }
-    const float mx = xhalf_max(fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3])));
-    const float mt = mx * smul;
-    const bool grow = mt > m_run + kRescaleSlack;
-    if (__ballot(grow)) {
-      const float m_new = grow ? mt : m_run;
-      // 1 where unchanged; a row with no allowed key yet has nothing to rescale
-      const float alpha = m_new == -__builtin_inff() ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
+            for (int e = 0; e < 8; ++e) {
+              const int32_t koff = gk[e] + Wm1 * (int32_t)fdiv((uint32_t)gk[e], P.wdiv);
+              bias[kb][8 * g + e] = rpb_h[rpb_base - koff];
+            }
+          }
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
-      m_run = m_new;
-    }
-    const float m_use = m_run == -__builtin_inff() ? 0.f : m_run;
-    // Row sums in fp32 from the unrounded weights (four partial sums); P goes
-    // to the PV product rounded to bf16.
-    bf16x8 pop[4];
-    float lq[4];
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x16 &sv = s[g >> 1];
-      const int o = 8 * (g & 1);
-      float acc = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float pv = __builtin_amdgcn_exp2f(sv[o + e] * smul - m_use);
-        acc += pv;
-        pop[g][e] = (__bf16)pv;
+          for (int v = 0; v < 16; ++v) s[kb][v] = __builtin_fmaf(s[kb][v], a.scale, bias[kb][v]);
       }
-      lq[g] = acc;
+      if constexpr (decltype(masked)::value) mask_blocks<2>(s, R, P, tile_of(it) * BN + 8 * half);
+    };
+    // Weights p = 2^(s * smul - m) in place of the scores, and this lane's sum.
+    auto weights = [&](f32x16 (&s)[2], float m) {
+      float lq[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int o = 8 * (g & 1);
+        float acc = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s[g >> 1][o + e], smul, -m));
+          acc += pv;
+          s[g >> 1][o + e] = pv;
+        }
+        lq[g] = acc;
+      }
+      return (lq[0] + lq[1]) + (lq[2] + lq[3]);
+    };
+
+    // Online softmax in the log2 domain with a lazily moved reference m_run
+    // (O and l always share it). Once every row of the wave has a finite
+    // reference, a tile first takes its weights against the reference as it
+    // stands, with no row max at all: weights up to 2^kFastLog2 are harmless
+    // (fp32 accumulators, bf16 operands), and since they are >= 0 their sum
+    // bounds each of them, so one compare of the sum (which is needed anyway;
+    // NaN and inf fail it too) validates the tile. Only when some row's sum
+    // fails does the tile fall back: its scores are recomputed from LDS and it
+    // takes the max path below.
+    f32x16 s[2];
+    bool fast = primed;
+    for (;;) {
+      // (keeps the compiler from hoisting the K operand reads out of this loop
+      // and holding them in registers across it)
+      asm volatile("" ::: "memory");
+      scores(s);
+      float m_ref = m_run;
+      if (!fast) {
+        // Max path: the reference moves only when a row's tile max exceeds it by
+        // more than kRescaleSlack, so the O / l rescale stays rare.
+        float mq[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x16 &sv = s[g >> 1];
+          const int o = 8 * (g & 1);
+          mq[g] = fmaxf(fmaxf(fmaxf(sv[o], sv[o + 1]), fmaxf(sv[o + 2], sv[o + 3])),
+                        fmaxf(fmaxf(sv[o + 4], sv[o + 5]), fmaxf(sv[o + 6], sv[o + 7])));
+        }
+        const float mx = xhalf_max(fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3])));
+        const float mt = mx * smul;
+        const bool grow = mt > m_run + kRescaleSlack;
+        if (__ballot(grow)) {
+          const float m_new = grow ? mt : m_run;
+          // 1 where unchanged; a row with no allowed key yet has nothing to rescale
+          const float alpha = m_new == -__builtin_inff() ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+          l_run *= alpha;
+#pragma unroll
+          for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
+          m_run = m_new;
+        }
+        m_ref = m_run == -__builtin_inff() ? 0.f : m_run;
+      }
+      const float lt = weights(s, m_ref);
+      if (fast && __ballot(!(lt <= kFastBound))) {
+        fast = false;  // recompute the scores and take the max path
+        continue;
+      }
+      l_run += lt;
+      if (!fast) primed = !__ballot(m_run == -__builtin_inff());
+      break;
     }
-    l_run += (lq[0] + lq[1]) + (lq[2] + lq[3]);
+    // Row sums above are fp32 sums of the unrounded weights; P goes to the PV
+    // product rounded to bf16.
+    bf16x8 pop[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pop[g][e] = (__bf16)s[g >> 1][8 * (g & 1) + e];
 
     // O^T += V^T P^T over four 16-key steps, d blocks interleaved; V^T
     // operands read with the transposing LDS read right before use.

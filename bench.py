@@ -88,6 +88,10 @@ class Timer:
         ps = self.pairs.get(name, [])
         return sum(a.elapsed_time(b) for a, b in ps) / len(ps) if ps else float("nan")
 
+    def median_ms(self, name):
+        ts = sorted(a.elapsed_time(b) for a, b in self.pairs.get(name, []))
+        return ts[len(ts) // 2] if ts else float("nan")
+
     def count(self, name):
         return len(self.pairs.get(name, []))
 
@@ -393,7 +397,9 @@ def time_backward(pipe, steps, warmup):
     # five products per non-empty tile (S, dP, dV, dK, dQ), the usual count; the
     # kernels recompute S and dP once more (seven products executed)
     flops = 10.0 * w.tile_m * w.tile_n * w.d * tiles
-    bwd_ms = T.mean_ms("attn_bwd")
+    # median per call: host stalls of the eager loop (up to milliseconds on some
+    # boxes) land inside whichever event bracket is open and would skew a mean
+    bwd_ms = T.median_ms("attn_bwd")
     peak = BF16_PEAK_TFLOPS if w.dtype == "bf16" else FP32_PEAK_TFLOPS
     tflops = flops / (bwd_ms * 1e-3) / 1e12
     return {
@@ -402,6 +408,7 @@ def time_backward(pipe, steps, warmup):
         "step": "gather of dout, attention backward, scatter of dq, dk, dv" if pipe.hilbert
                 else "attention backward",
         "attn_bwd_ms_per_call": bwd_ms,
+        "attn_bwd_ms_per_call_mean": T.mean_ms("attn_bwd"),
         "tile_flops": flops,
         "tile_flops_executed": 1.4 * flops,
         "attn_bwd_tflops_nonempty_tiles": tflops,

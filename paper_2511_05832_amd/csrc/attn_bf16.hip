@@ -94,6 +94,25 @@ constexpr int kStages = 3;
 __device__ __forceinline__ float xhalf_max(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
 __device__ __forceinline__ float xhalf_sum(float x) { return x + __shfl_xor(x, 32); }
 
+// RPB: table entries a staged bias window may hold (per buffer).
+constexpr int kWinCap = 1024;
+
+// Bounding box {r_min, r_max, c_min, c_max} of the 64 lanes' grid cells (r, c <
+// 2^15), in every lane: both coordinates' min and max at once, as packed 16-bit
+// pairs. All 64 lanes must be active.
+__device__ __forceinline__ int4 wave_box(int32_t r, int32_t c) {
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  u16x2 lo = {(unsigned short)r, (unsigned short)c}, hi = lo;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const u16x2 l2 = __builtin_bit_cast(u16x2, __shfl_xor(__builtin_bit_cast(int, lo), o));
+    const u16x2 h2 = __builtin_bit_cast(u16x2, __shfl_xor(__builtin_bit_cast(int, hi), o));
+    lo = __builtin_elementwise_min(lo, l2);
+    hi = __builtin_elementwise_max(hi, h2);
+  }
+  return int4{lo.x, hi.x, lo.y, hi.y};
+}
+
 // Per-row XOR swizzle of the 16-byte chunks of a K / V tile row in LDS.
 template <int D>
 __device__ __forceinline__ int swz_k(int r) {
@@ -155,12 +174,18 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2
   static_assert(BM * D * 2 <= STAGE, "the Q tile must fit one stage");
   static_assert(kStages == 3, "the loop keeps exactly one tile in flight behind the current");
   static_assert(LPT < 64, "too many copies in flight for vmcnt");
-  constexpr int LPTR = RPB ? LPT + 1 : LPT;   // + the wave's share of the tile's grid ids
   // Row-index area (GATHER): the Q tile's BM indices, then four slots of BN
   // indices for key tiles (slot i % 4 holds tile list entry i).
   constexpr int IDXQ = kStages * STAGE;
   constexpr int IDXK = IDXQ + BM * 4;
-  constexpr int LDSB = IDX ? IDXK + 4 * BN * 4 : kStages * STAGE;
+  // RPB: parameters {dr0, dc0, wc, n} of four tiles' bias windows, each key's
+  // window term for them (four slots of BN), the waves' query boxes, and two
+  // window buffers of kWinCap table entries.
+  constexpr int WINP = IDXK + 4 * BN * 4;
+  constexpr int WINB = WINP + 4 * 16;
+  constexpr int QBOX = WINB + 4 * BN * 4;
+  constexpr int WIN = QBOX + NW * 16;
+  constexpr int LDSB = RPB ? WIN + 2 * kWinCap * 4 : IDX ? IDXK + 4 * BN * 4 : kStages * STAGE;
 
   __shared__ __attribute__((aligned(16))) char lds[LDSB];
   const int32_t *idx_q = reinterpret_cast<const int32_t *>(lds + IDXQ);
@@ -307,23 +332,38 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2
   }
   if constexpr (RPB) {
     if (ntot > 0) issue_idx(0);
-  }
-  if (ntot > 0) issue_tile(0, 0);
-  if constexpr (RPB) {
     if (ntot > 1) issue_idx(1);
   }
+  if (ntot > 0) issue_tile(0, 0);
   if (ntot > 1) issue_tile(1, 1);
-  // RPB: this lane's bias base C + off(q), loaded after the copies; one wait
-  // the compiler sees then covers it and them.
-  int32_t rpb_base = 0;
+  if constexpr (RPB) {
+    if (ntot > 2) issue_idx(2);
+  }
+  // RPB: this lane's query cell (rq, cq) and bias base C + off(q), loaded after
+  // the copies; one wait the compiler sees then covers it and them. Then the
+  // workgroup's query box: each wave's, combined through LDS.
+  int32_t rpb_base = 0, rq = 0, cq = 0, qr0 = 0, qr1 = 0, qc0 = 0, qc1 = 0;
   const float *rpb_h = nullptr;
   if constexpr (RPB) {
     const int32_t g = a.order[min(qpos, a.N - 1)];
     const int32_t Wg = P.W;
-    rpb_base = (P.H - 1) * (2 * Wg - 1) + (Wg - 1) + g + (Wg - 1) * (int32_t)fdiv((uint32_t)g, P.wdiv);
+    rq = (int32_t)fdiv((uint32_t)g, P.wdiv);
+    cq = g - rq * Wg;
+    rpb_base = (P.H - 1) * (2 * Wg - 1) + (Wg - 1) + g + (Wg - 1) * rq;
     rpb_h = a.rpb + (int64_t)(bh % a.heads) * (2 * P.H - 1) * (2 * Wg - 1);
     wait_vmem_all();
+    int4 box = wave_box(rq, cq);
+    if (lane == 0) reinterpret_cast<int4 *>(lds + QBOX)[wave] = box;
     wait_then_barrier<0>();
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const int4 b = reinterpret_cast<const int4 *>(lds + QBOX)[w];
+      box = int4{min(box.x, b.x), max(box.y, b.y), min(box.z, b.z), max(box.w, b.w)};
+    }
+    qr0 = __builtin_amdgcn_readfirstlane(box.x);
+    qr1 = __builtin_amdgcn_readfirstlane(box.y);
+    qc0 = __builtin_amdgcn_readfirstlane(box.z);
+    qc1 = __builtin_amdgcn_readfirstlane(box.w);
   } else {
     // Q and the first key tile are in; the second may still be in flight.
     if (ntot > 1) wait_then_barrier<LPT>();
@@ -338,6 +378,49 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2
                                                  (((half * NCH + c) ^ swz_q<D>(r)) * 16));
   }
 
+  // RPB: the bias window of list entry j, issued by one wave: the table entries
+  // that this workgroup's queries and entry j's keys can address - the rectangle
+  // of cell offsets spanned by the query box and the key tile's box - copied
+  // into window buffer j % 2, its parameters {dr0, dc0, wc, n} into slot j % 4,
+  // and each key's term rk * wc + ck (one key per lane) into that slot's terms.
+  // A tile whose window exceeds kWinCap entries gets n = 0 and reads the table
+  // directly. Every table index copied lies in the table: both boxes are inside
+  // the grid.
+  auto issue_window = [&](int j) {
+    const int32_t id = idx_k(j)[lane];
+    const int32_t rk = (int32_t)fdiv((uint32_t)id, P.wdiv);
+    const int4 kbox = wave_box(rk, id - rk * P.W);
+    const int32_t kr0 = __builtin_amdgcn_readfirstlane(kbox.x);
+    const int32_t kr1 = __builtin_amdgcn_readfirstlane(kbox.y);
+    const int32_t kc0 = __builtin_amdgcn_readfirstlane(kbox.z);
+    const int32_t kc1 = __builtin_amdgcn_readfirstlane(kbox.w);
+    const int32_t dr0 = qr0 - kr1, dc0 = qc0 - kc1;
+    const int32_t wc = qc1 - kc0 - dc0 + 1, n = (qr1 - kr0 - dr0 + 1) * wc;
+    const bool fits = n <= kWinCap;
+    if (lane == 0) *reinterpret_cast<int4 *>(lds + WINP + (j & 3) * 16) = int4{dr0, dc0, wc, fits ? n : 0};
+    if (fits) {
+      reinterpret_cast<int32_t *>(lds + WINB + (j & 3) * BN * 4)[lane] = id + rk * (wc - P.W);
+      // entry f of the window is offset row f / wc, column f % wc (the row from
+      // a float quotient: exact, as f < 2^10 puts the fraction >= 2^-11 away
+      // from an integer)
+      const float inv = 1.f / (float)wc;
+      const int32_t pitch = 2 * P.W - 1, last = (2 * P.H - 1) * pitch - 1;
+      for (int c = 0; c * 64 < n; ++c) {
+        const int32_t f = min(64 * c + lane, n - 1);
+        const int32_t i = (int32_t)(((float)f + 0.5f) * inv);
+        const int32_t jj = f - i * wc;
+        // (clamped as a guard: the boxes already keep it inside the table)
+        const int32_t e = min(max((dr0 + i + P.H - 1) * pitch + (dc0 + jj + P.W - 1), 0), last);
+        lds_dma4(rpb_h + e, lds_addr(lds + WIN + (j & 1) * kWinCap * 4 + 256 * c));
+      }
+    }
+  };
+  if constexpr (RPB) {
+    // entry 0's window, complete and visible before the loop
+    if (ntot > 0 && wave == 0) issue_window(0);
+    wait_then_barrier<0>();
+  }
+
   // One key tile: wait for its copies, refill the ring, then S^T, (mask),
   // online softmax and O^T += V^T P^T. MASKED is a compile-time flag, so full
   // and partial tiles run separate loop bodies and the unmasked path carries no
@@ -346,7 +429,10 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2
   auto step = [&](int it, auto masked) {
     // Wait for this wave's copies of tile `it`; the copies of tile it + 1 (the
     // only one issued after it) may stay in flight.
-    if (it + 1 < ntot) wait_then_barrier<LPTR>();
+    // RPB: after tile it's window come tile it + 1's copies and entry it + 2's
+    // indices.
+    if (RPB && it + 2 < ntot) wait_then_barrier<LPT + 1>();
+    else if (it + 1 < ntot) wait_then_barrier<LPT>();
     else wait_then_barrier<0>();
     // The stage refilled next was last read in iteration it - 1, which every
     // wave has finished (it is behind the barrier above).
@@ -374,25 +460,48 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2
           const bf16x8 kop = *reinterpret_cast<const bf16x8 *>(st + kaddr[kb][c]);
           s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[c], s[kb], 0, 0, 0);
         }
-      // RPB: scores in natural units plus the bias, s = scale * <q, k> + bias.
+      // RPB: scores in natural units plus the bias, s = scale * <q, k> + bias,
+      // from the tile's staged window (entry (rq - rk - dr0) * wc + (cq - ck -
+      // dc0)) or, for a tile whose window did not fit, from the table.
       if constexpr (RPB) {
-        // all 32 bias loads first, so that they are in flight together
         const int32_t *kid = idx_k(it);
-        const int32_t Wm1 = P.W - 1;
+        const int4 pw = *reinterpret_cast<const int4 *>(lds + WINP + (it & 3) * 16);
+        const int32_t w_dr0 = __builtin_amdgcn_readfirstlane(pw.x);
+        const int32_t w_dc0 = __builtin_amdgcn_readfirstlane(pw.y);
+        const int32_t w_wc = __builtin_amdgcn_readfirstlane(pw.z);
+        const int32_t w_n = __builtin_amdgcn_readfirstlane(pw.w);
         float bias[2][16];
+        if (w_n != 0) {
+          const float *win = reinterpret_cast<const float *>(lds + WIN + (it & 1) * kWinCap * 4);
+          const int32_t *term = reinterpret_cast<const int32_t *>(lds + WINB + (it & 3) * BN * 4);
+          const int32_t aq = (rq - w_dr0) * w_wc + (cq - w_dc0);
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+          for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int g = 0; g < 2; ++g) {
-            const int4 *ids = reinterpret_cast<const int4 *>(kid + kb * 32 + 16 * g + 8 * half);
-            const int4 lo = ids[0], hi = ids[1];
-            const int32_t gk[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+            for (int g = 0; g < 2; ++g) {
+              const int4 *tk = reinterpret_cast<const int4 *>(term + kb * 32 + 16 * g + 8 * half);
+              const int4 lo = tk[0], hi = tk[1];
+              const int32_t bk[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const int32_t koff = gk[e] + Wm1 * (int32_t)fdiv((uint32_t)gk[e], P.wdiv);
-              bias[kb][8 * g + e] = rpb_h[rpb_base - koff];
+              for (int e = 0; e < 8; ++e) bias[kb][8 * g + e] = win[aq - bk[e]];
             }
-          }
+        } else {
+          // all 32 bias loads first, so that they are in flight together
+          const int32_t Wm1 = P.W - 1;
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int g = 0; g < 2; ++g) {
+              const int4 *ids = reinterpret_cast<const int4 *>(kid + kb * 32 + 16 * g + 8 * half);
+              const int4 lo = ids[0], hi = ids[1];
+              const int32_t gk[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                const int32_t koff = gk[e] + Wm1 * (int32_t)fdiv((uint32_t)gk[e], P.wdiv);
+                bias[kb][8 * g + e] = rpb_h[rpb_base - koff];
+              }
+            }
+        }
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -486,13 +595,14 @@ __global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2
         const bf16x8 vop = lds_read_tr16x2(st + vbase[db] + (16 * t) * D * 2, D * 2);
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[t], oacc[db], 0, 0, 0);
       }
-    // RPB: refill the ring at the end of the step (stage (it + 2) % 3 held tile
-    // it - 1, which every wave finished before this step's barrier).
+    // RPB: at the end of the step, entry it + 1's window (its indices arrived
+    // before this step's barrier), then the ring refill (stage (it + 2) % 3 held
+    // tile it - 1, which every wave finished before this step's barrier), then
+    // entry it + 3's indices (slot (it + 3) % 4 last held entry it - 1's).
     if constexpr (RPB) {
-      if (it + 2 < ntot) {
-        issue_idx(it + 2);
-        issue_tile(it + 2, nstage);
-      }
+      if (it + 1 < ntot && wave == (it + 1) % NW) issue_window(it + 1);
+      if (it + 2 < ntot) issue_tile(it + 2, nstage);
+      if (it + 3 < ntot) issue_idx(it + 3);
     }
   };
   for (int it = 0; it < nf; ++it) step(it, std::false_type{});

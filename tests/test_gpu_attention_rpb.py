@@ -100,3 +100,26 @@ def test_rejects_wrong_table_shape():
     mask = hla.build_block_mask(pat, 64, 64)
     with pytest.raises(hla.HLAError):
         hla.attn_fwd_rpb(q, k, v, None, torch.zeros((2, 31, 30), device=DEV), mask)
+
+
+@pytest.mark.parametrize("H,Wd,dtype", [(32, 32, "bf16"), (8, 8, "bf16"), (16, 24, "f32")], ids=str)
+def test_arbitrary_order(H, Wd, dtype):
+    """Any order, not just the Hilbert path: with a random permutation the cells of a
+    tile scatter over the grid, so a 32 x 32 grid's tile windows (up to 63 x 63
+    entries) exceed the staged capacity and the kernel reads the table directly,
+    while an 8 x 8 grid keeps staged windows of irregular boxes."""
+    pat = Pat("hilbert_slide", H, Wd, 40)
+    B, Hh, d = 1, 2, 64
+    q, k, v = W.attn_inputs(B, Hh, pat.N, d, dtype, 91)
+    g = torch.Generator().manual_seed(H * Wd)
+    order = torch.randperm(pat.N, generator=g).to(torch.int32)
+    table = torch.randn((Hh, 2 * H - 1, 2 * Wd - 1), generator=g)
+    mask = hla.build_block_mask(pat, 128 if pat.N % 128 == 0 else 64, 64)
+    scale = 1.0 / d ** 0.5
+    out, lse = hla.attn_fwd_rpb(q.to(DEV), k.to(DEV), v.to(DEV), order.to(DEV), table.to(DEV), mask, scale)
+    torch.cuda.synchronize()
+    ref_out, ref_lse = o_attn.attention(np64(q), np64(k), np64(v), pat, scale,
+                                        rpb=(table.double().numpy(), order.numpy().astype(np.int64)))
+    e_out, e_lse = max_abs(np64(out), ref_out), max_abs(np64(lse), ref_lse)
+    print(f"{H}x{Wd} {dtype}: out err {e_out:.3e}, lse err {e_lse:.3e}")
+    assert e_out <= TOL_OUT[dtype] and e_lse <= TOL_LSE, (e_out, e_lse)

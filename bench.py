@@ -23,7 +23,8 @@ on a bounded sample of the same step on the host cores.
 The backward pass of the same attention workload is timed the same way (a
 graph-replayed step: gather of the upstream gradient, hla_attn_bwd, scatter of
 dq, dk, dv; per-call time of hla_attn_bwd from an eager pass) and reported under
-"backward"; --no-backward skips it. The attention with the global relative
+"backward"; with the reordering fused in (hla_attn_bwd_perm on the grid-ordered
+tensors) under "backward_fused"; --no-backward skips both. The attention with the global relative
 position bias (hla_attn_fwd_rpb) is timed per call on the same inputs and
 reported under "rpb"; --no-rpb skips it.
 """
@@ -189,7 +190,7 @@ class AttnPipeline:
             s["dout"] = dout.cuda()
             for n in ("dq", "dk", "dv"):
                 s[n] = torch.empty_like(s["q"])
-            if self.hilbert:
+            if self.hilbert and not self.fused:
                 s["douth"] = torch.empty_like(s["q"])
                 for n in ("dqr", "dkr", "dvr"):
                     s[n] = torch.empty_like(s["q"])
@@ -199,8 +200,15 @@ class AttnPipeline:
 
     def step_backward(self, i):
         """Gather the upstream gradient into the forward's order, run the backward,
-        scatter dq, dk, dv back to row-major."""
+        scatter dq, dk, dv back to row-major (fused: hla_attn_bwd_perm on the
+        grid-ordered tensors, no gather or scatter)."""
         hla, w, s, T = self.hla, self.w, self.sets[i % self.nsets], self.timer_bwd
+        if self.fused:
+            with T.stage("attn_bwd"):
+                hla.attn_bwd_perm(s["q"], s["k"], s["v"], s["o"], s["dout"], s["lse"], self.order,
+                                  self.mask_c, w.scale, dq=s["dq"], dk=s["dk"], dv=s["dv"],
+                                  stats=s["stats"])
+            return
         if self.hilbert:
             with T.stage("gather"):
                 hla.gather(s["dout"], self.order, out=s["douth"])
@@ -405,8 +413,9 @@ def time_backward(pipe, steps, warmup):
     return {
         "ms_per_step": graph_ms,
         "ms_per_step_eager": eager_ms,
-        "step": "gather of dout, attention backward, scatter of dq, dk, dv" if pipe.hilbert
-                else "attention backward",
+        "step": ("attention backward with the reordering fused in (hla_attn_bwd_perm)" if pipe.fused
+                 else "gather of dout, attention backward, scatter of dq, dk, dv" if pipe.hilbert
+                 else "attention backward"),
         "attn_bwd_ms_per_call": bwd_ms,
         "attn_bwd_ms_per_call_mean": T.mean_ms("attn_bwd"),
         "tile_flops": flops,
@@ -611,13 +620,16 @@ def main():
         bwd = time_backward(pipe, args.steps, args.warmup)
         print(f"[bench] {w.name} backward: {json.dumps(bwd)}", file=sys.stderr, flush=True)
     # The same step with the reordering fused into the attention (Hilbert patterns).
-    res_fused = None
+    res_fused = bwd_fused = None
     if isinstance(w, W.AttnWorkload) and w.pattern.hilbert and args.step != "composed-only":
         del pipe
         torch.cuda.empty_cache()
         fpipe = make_pipeline(w, hla, fused=True)
         res_fused = summarize(fpipe, run_timed(fpipe, args.steps, args.warmup))
         print(f"[bench] {w.name} (fused): {json.dumps(res_fused)}", file=sys.stderr, flush=True)
+        if not args.no_backward:
+            bwd_fused = time_backward(fpipe, args.steps, args.warmup)
+            print(f"[bench] {w.name} backward (fused): {json.dumps(bwd_fused)}", file=sys.stderr, flush=True)
         pipe = fpipe   # the algorithmic figures below depend on the workload only
     rpb = None
     if isinstance(w, W.AttnWorkload) and not args.no_rpb:
@@ -723,6 +735,8 @@ def main():
             "attn_ms_per_call": other["attn_ms"], "stages_ms": other["stages_ms"]}
     if bwd:
         line["backward"] = bwd
+    if bwd_fused:
+        line["backward_fused"] = bwd_fused
     if rpb:
         line["rpb"] = rpb
     if cmp_res:

@@ -270,6 +270,26 @@ hla_status hla_attn_bwd(const void *q, const void *k, const void *v, const void 
                         hla_stream_t stream);
 
 /*
+ * The same backward pass with the reordering fused into its loads and stores,
+ * the counterpart of hla_attn_fwd_perm for training: q, k, v, out, dout, lse,
+ * dq, dk, dv and stats are all stored in grid (row-major) order, and sequence
+ * position i (the position the mask's pattern refers to) is row order[i]:
+ *   dq[b,h,order[i],:] = hla_attn_bwd's dq[b,h,i,:] for the inputs taken in
+ *   sequence order (q'[b,h,i,:] = q[b,h,order[i],:], likewise k, v, out, dout,
+ *   lse), and the same for dk, dv.
+ * out and lse are hla_attn_fwd_perm's results for these q, k, v, order, mask and
+ * scale. order: device int32[N], a permutation of [0, N) (not checked),
+ * 16-byte aligned, not overlapping an output or stats. The results equal
+ * gather -> hla_attn_bwd -> scatter bit for bit. Other arguments, support and
+ * errors as hla_attn_bwd.
+ */
+hla_status hla_attn_bwd_perm(const void *q, const void *k, const void *v, const void *out,
+                             const void *dout, const float *lse, const int32_t *order,
+                             const hla_block_mask *mask, void *dq, void *dk, void *dv,
+                             float *stats, int64_t B, int64_t heads, int64_t N, int64_t d,
+                             hla_dtype dtype, float scale, hla_stream_t stream);
+
+/*
  * QKV projection with head split (Sec. 4.2, input processing: the Linear layer
  * that produces Q, K, V from the token features):
  *   y = x W_qkv^T,  x [B, N, C],  W_qkv [3C, C] (row f is output feature f),

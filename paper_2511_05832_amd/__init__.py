@@ -29,6 +29,7 @@ import torch
 
 __all__ = ["HLAError", "lib", "hilbert_perm", "gather", "scatter", "block_mask_dims",
            "build_block_mask", "BlockMask", "attn_fwd", "attn_fwd_perm", "attn_fwd_rpb", "attn_bwd",
+           "attn_bwd_perm",
            "qkv_proj", "out_proj",
            "PATTERN_IDS", "LIB_PATH", "EXPORTED"]
 
@@ -49,7 +50,7 @@ HLA_F32, HLA_BF16 = 0, 1
 
 EXPORTED = ("hla_hilbert_perm", "hla_gather", "hla_scatter", "hla_block_mask_dims",
             "hla_build_block_mask", "hla_attn_fwd", "hla_attn_fwd_perm", "hla_attn_fwd_rpb",
-            "hla_attn_bwd",
+            "hla_attn_bwd", "hla_attn_bwd_perm",
             "hla_qkv_proj", "hla_out_proj",
             "hla_last_error", "hla_version")
 
@@ -109,6 +110,8 @@ def lib() -> ctypes.CDLL:
                                  i64, i64, i64, i64, ctypes.c_int, f32, vp],
             "hla_attn_bwd": [vp, vp, vp, vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp, vp,
                              vp, i64, i64, i64, i64, ctypes.c_int, f32, vp],
+            "hla_attn_bwd_perm": [vp, vp, vp, vp, vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp,
+                                  vp, vp, i64, i64, i64, i64, ctypes.c_int, f32, vp],
             "hla_qkv_proj": [vp, vp, vp, vp, vp, i64, i64, i64, i64, vp],
             "hla_out_proj": [vp, vp, vp, i64, i64, i64, i64, i64, vp],
         }
@@ -357,12 +360,7 @@ def attn_fwd_rpb(q, k, v, order, rpb, mask: BlockMask, scale: Optional[float] = 
     return out, lse
 
 
-def attn_bwd(q, k, v, out, dout, lse, mask: BlockMask, scale: Optional[float] = None,
-             dq: Optional[torch.Tensor] = None, dk: Optional[torch.Tensor] = None,
-             dv: Optional[torch.Tensor] = None, stats: Optional[torch.Tensor] = None):
-    """Block-sparse attention backward (hla_attn_bwd). ``out`` and ``lse`` are the
-    forward's results for these q, k, v, mask and scale. Returns (dq, dk, dv).
-    ``stats`` is the float32 [B, heads, N, 2] workspace (allocated if None)."""
+def _attn_bwd_args(q, k, v, out, dout, lse, scale, dq, dk, dv, stats):
     for t, n in ((q, "q"), (k, "k"), (v, "v"), (out, "out"), (dout, "dout"), (lse, "lse")):
         _require(t, n)
     if q.dim() != 4 or any(t.shape != q.shape for t in (k, v, out, dout)):
@@ -381,9 +379,38 @@ def attn_bwd(q, k, v, out, dout, lse, mask: BlockMask, scale: Optional[float] = 
         stats = torch.empty((B, Hh, N, 2), dtype=torch.float32, device=q.device)
     for t, n in ((dq, "dq"), (dk, "dk"), (dv, "dv"), (stats, "stats")):
         _require(t, n)
+    return B, Hh, N, d, float(scale), dq, dk, dv, stats
+
+
+def attn_bwd(q, k, v, out, dout, lse, mask: BlockMask, scale: Optional[float] = None,
+             dq: Optional[torch.Tensor] = None, dk: Optional[torch.Tensor] = None,
+             dv: Optional[torch.Tensor] = None, stats: Optional[torch.Tensor] = None):
+    """Block-sparse attention backward (hla_attn_bwd). ``out`` and ``lse`` are the
+    forward's results for these q, k, v, mask and scale. Returns (dq, dk, dv).
+    ``stats`` is the float32 [B, heads, N, 2] workspace (allocated if None)."""
+    B, Hh, N, d, scale, dq, dk, dv, stats = _attn_bwd_args(q, k, v, out, dout, lse, scale,
+                                                           dq, dk, dv, stats)
     _check(lib().hla_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse),
                               ctypes.byref(mask.struct), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(stats),
-                              B, Hh, N, d, _dtype_code(q), float(scale), _stream(q)))
+                              B, Hh, N, d, _dtype_code(q), scale, _stream(q)))
+    return dq, dk, dv
+
+
+def attn_bwd_perm(q, k, v, out, dout, lse, order, mask: BlockMask, scale: Optional[float] = None,
+                  dq: Optional[torch.Tensor] = None, dk: Optional[torch.Tensor] = None,
+                  dv: Optional[torch.Tensor] = None, stats: Optional[torch.Tensor] = None):
+    """Backward with the reordering fused in (hla_attn_bwd_perm): every tensor in grid
+    order, sequence position i is row order[i]; ``out`` and ``lse`` are attn_fwd_perm's
+    results. Returns (dq, dk, dv) in grid order."""
+    B, Hh, N, d, scale, dq, dk, dv, stats = _attn_bwd_args(q, k, v, out, dout, lse, scale,
+                                                           dq, dk, dv, stats)
+    _require(order, "order")
+    if order.dtype != torch.int32 or order.numel() != N:
+        raise HLAError(HLA_ERR_INVALID_ARG, f"order must be int32 with N = {N} entries")
+    _check(lib().hla_attn_bwd_perm(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse),
+                                   _ptr(order), ctypes.byref(mask.struct), _ptr(dq), _ptr(dk),
+                                   _ptr(dv), _ptr(stats), B, Hh, N, d, _dtype_code(q), scale,
+                                   _stream(q)))
     return dq, dk, dv
 
 

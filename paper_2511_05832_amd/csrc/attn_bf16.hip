@@ -155,7 +155,9 @@ __device__ __forceinline__ int swz_q(int r) {
 // softmax, so this mode issues each tile's copies at the end of the step two
 // tiles earlier rather than at its start).
 template <int D, int NW, int MODE>
-__global__ void __launch_bounds__(64 * NW, (NW == 4 && MODE != ATTN_RPB) ? 3 : 2)
+// (waves per SIMD the launch bound asks for: what the registers and LDS allow -
+// the RPB mode's windows leave room for two workgroups per CU)
+__global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) : (NW == 4 ? 3 : 2))
     attn_fwd_bf16(AttnArgs a) {
   constexpr bool GATHER = MODE == ATTN_GATHER;
   constexpr bool RPB = MODE == ATTN_RPB;

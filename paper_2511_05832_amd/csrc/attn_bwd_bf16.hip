@@ -78,16 +78,20 @@ __device__ __forceinline__ void stage_rows(const f32x16 *acc, float mul, __bf16 
     }
 }
 // Only the first `nrows` rows are written (rows past the end of the sequence in
-// a ragged last tile are not).
+// a ragged last tile are not). Row r goes to dst row r, or to dst row rows[r]
+// when a row map is given (the fused reordering).
 template <int D>
-__device__ __forceinline__ void write_rows(const __bf16 *Os, __bf16 *dst, int lane, int nrows) {
+__device__ __forceinline__ void write_rows(const __bf16 *Os, __bf16 *dst, int lane, int nrows,
+                                           const int32_t *rows = nullptr) {
   constexpr int OS = D + 8, CPR = D / 8;
 #pragma unroll
   for (int i = lane; i < 32 * CPR; i += 64) {
     const int r = i / CPR, c = i % CPR;
-    if (r < nrows)
-      *reinterpret_cast<uint4 *>(dst + r * D + c * 8) =
+    if (r < nrows) {
+      const int64_t row = rows ? (int64_t)rows[r] : (int64_t)r;
+      *reinterpret_cast<uint4 *>(dst + row * D + c * 8) =
           *reinterpret_cast<const uint4 *>(Os + r * OS + c * 8);
+    }
   }
 }
 
@@ -100,7 +104,7 @@ __device__ __forceinline__ void write_rows(const __bf16 *Os, __bf16 *dst, int la
 //   dq^T += K^T dS^T  A = K^T (transposing LDS reads), B = dS^T (registers)
 constexpr int kStagesDq = 3;
 
-template <int D, int NW>
+template <int D, int NW, bool GATHER>
 __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
   constexpr int BM = 32 * NW;
   constexpr int NT = 64 * NW;
@@ -113,8 +117,15 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
   constexpr int NDB = D / 32;
   static_assert(BN * CPR % NT == 0, "tile copies must split evenly over the workgroup");
   static_assert((kStagesDq - 2) * LPT < 64, "too many copies in flight for vmcnt");
+  // GATHER: the query tile's BM row indices, then four slots of BN indices for
+  // key tiles (slot i % 4 holds tile list entry i).
+  constexpr int IDXQ = kStagesDq * STAGE;
+  constexpr int IDXK = IDXQ + BM * 4;
+  constexpr int LDSB = GATHER ? IDXK + 4 * BN * 4 : kStagesDq * STAGE;
 
-  __shared__ __attribute__((aligned(16))) char lds[kStagesDq * STAGE];
+  __shared__ __attribute__((aligned(16))) char lds[LDSB];
+  const int32_t *idx_q = reinterpret_cast<const int32_t *>(lds + IDXQ);
+  auto idx_k = [&](int i) { return reinterpret_cast<const int32_t *>(lds + IDXK + (i & 3) * BN * 4); };
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -151,17 +162,32 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
     offr[j] = r;
     offc[j] = (cs ^ swz<D>(r)) * 8;
   }
-  auto issue_tile = [&](int kt, int stage) {
+  // Copies of the K/V tile of list entry i (GATHER: row r of the tile is the
+  // row its index slot names).
+  auto issue_tile = [&](int i, int stage) {
     char *base = lds + stage * STAGE;
     int64_t roff[CPW];
+    if constexpr (GATHER) {
+      const int32_t *rows = idx_k(i);
 #pragma unroll
-    for (int j = 0; j < CPW; ++j) roff[j] = (int64_t)min(kt * BN + offr[j], a.N - 1) * D + offc[j];
+      for (int j = 0; j < CPW; ++j) roff[j] = (int64_t)rows[offr[j]] * D + offc[j];
+    } else {
+      const int kt = tile_of(i);
+#pragma unroll
+      for (int j = 0; j < CPW; ++j) roff[j] = (int64_t)min(kt * BN + offr[j], a.N - 1) * D + offc[j];
+    }
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
       lds_dma16(K + roff[j], lds_addr(base + (j * NW + wave) * 1024));
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
       lds_dma16(V + roff[j], lds_addr(base + TILE + (j * NW + wave) * 1024));
+  };
+  // GATHER: the row indices of list entry i (one per lane of the first wave)
+  // into its slot; positions past the end of the sequence read entry N - 1.
+  auto issue_idx = [&](int i) {
+    if (wave == 0)
+      lds_dma4(a.order + min(tile_of(i) * BN + lane, a.N - 1), lds_addr(lds + IDXK + (i & 3) * BN * 4));
   };
 
   int raddr[2][NCH];
@@ -180,29 +206,46 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
   for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
   const float sl2 = a.scale_log2;
 
+  if constexpr (GATHER) {
+    // Row indices of the query tile and of the first three key tiles, first.
+    if (wave == 0) {
+#pragma unroll
+      for (int c = 0; c < BM / 64; ++c)
+        lds_dma4(a.order + min(q0 + 64 * c + lane, a.N - 1), lds_addr(lds + IDXQ + 256 * c));
+    }
+#pragma unroll
+    for (int i = 0; i < 3; ++i)
+      if (i < ntot) issue_idx(i);
+    wait_then_barrier<0>();
+  }
 #pragma unroll
   for (int p = 0; p < kStagesDq - 1; ++p)
-    if (p < ntot) issue_tile(tile_of(p), p);
+    if (p < ntot) issue_tile(p, p);
   // The wave's own q and dout rows and row statistics, loaded after the first
   // copies so that both latencies overlap; one wait the compiler can see then
   // covers all of them, so it inserts no wait of its own inside the loop.
   // (a query row past the end of the sequence reads row N - 1 and stores nothing)
-  const int qc = min(qpos, a.N - 1);
+  const int64_t qrow = GATHER ? (int64_t)idx_q[wave * 32 + col] : (int64_t)min(qpos, a.N - 1);
   bf16x8 qop[NCH], gop[NCH];
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
-    qop[c] = *reinterpret_cast<const bf16x8 *>(Q + (int64_t)qc * D + half * (D / 2) + 8 * c);
-    gop[c] = *reinterpret_cast<const bf16x8 *>(G + (int64_t)qc * D + half * (D / 2) + 8 * c);
+    qop[c] = *reinterpret_cast<const bf16x8 *>(Q + qrow * D + half * (D / 2) + 8 * c);
+    gop[c] = *reinterpret_cast<const bf16x8 *>(G + qrow * D + half * (D / 2) + 8 * c);
   }
-  const float2 rs = *reinterpret_cast<const float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qc));
+  const float2 rs = *reinterpret_cast<const float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qrow));
   const float lse2 = rs.x, delta = rs.y;
   wait_vmem_all();
 
   for (int it = 0; it < ntot; ++it) {
     const int stage = it % kStagesDq;
     wait_tiles_then_barrier<LPT, kStagesDq - 2>(min(ntot - 1 - it, kStagesDq - 2));
-    if (it + kStagesDq - 1 < ntot)
-      issue_tile(tile_of(it + kStagesDq - 1), (it + kStagesDq - 1) % kStagesDq);
+    // (GATHER: the indices of entry it + 2 arrived with the wait above - the
+    // first wave issued them before entry it + 1's copies - those of it + 3 go
+    // out first; slot (it + 3) % 4 last held entry it - 1's.)
+    if constexpr (GATHER) {
+      if (it + 3 < ntot) issue_idx(it + 3);
+    }
+    if (it + kStagesDq - 1 < ntot) issue_tile(it + kStagesDq - 1, (it + kStagesDq - 1) % kStagesDq);
     const char *st = lds + stage * STAGE;
     const int kt = tile_of(it);
 
@@ -240,8 +283,12 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
   __bf16 *Os = reinterpret_cast<__bf16 *>(lds) + wave * 32 * (D + 8);
   stage_rows<D>(acc, a.scale, Os, col, half);
   __syncthreads();
-  write_rows<D>(Os, static_cast<__bf16 *>(a.dq) + slice + (int64_t)(q0 + wave * 32) * D, lane,
-                a.N - (q0 + wave * 32));
+  if constexpr (GATHER)
+    write_rows<D>(Os, static_cast<__bf16 *>(a.dq) + slice, lane, a.N - (q0 + wave * 32),
+                  idx_q + wave * 32);
+  else
+    write_rows<D>(Os, static_cast<__bf16 *>(a.dq) + slice + (int64_t)(q0 + wave * 32) * D, lane,
+                  a.N - (q0 + wave * 32));
 }
 
 // ---------------------------------------------------------------------------
@@ -256,7 +303,7 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
 // The two query halves of a key block are summed through LDS at the end.
 constexpr int kStagesKv = 2;
 
-template <int D, int BMQ>
+template <int D, int BMQ, bool GATHER>
 __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   constexpr int NT = 256;
   constexpr int CPR = D / 8;
@@ -272,12 +319,19 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   constexpr int NDB = D / 32;
   constexpr int XCH = 2 * 2 * NDB * 16 * 64 * 4;           // partial-sum exchange
   constexpr int EPI = XCH > 4 * 32 * (D + 8) * 2 ? XCH : 4 * 32 * (D + 8) * 2;
-  constexpr int LDSB = kStagesKv * STAGE > EPI ? kStagesKv * STAGE : EPI;
+  constexpr int LDSR = kStagesKv * STAGE > EPI ? kStagesKv * STAGE : EPI;
+  // GATHER: the key tile's BN row indices, then four slots of BMQ indices for
+  // query tiles (slot i % 4 holds tile list entry i).
+  constexpr int KIDX = LDSR;
+  constexpr int QIDX = KIDX + BN * 4;
+  constexpr int LDSB = GATHER ? QIDX + 4 * BMQ * 4 : LDSR;
   static_assert(CPW >= 1 && BMQ * CPR % NT == 0, "tile copies must split evenly");
   static_assert(SL <= 64, "stats copies exceed a wave");
   static_assert(4 * SL * 4 == BMQ * 8, "the waves' stats copies cover the tile's rows");
 
   __shared__ __attribute__((aligned(16))) char lds[LDSB];
+  const int32_t *idx_k = reinterpret_cast<const int32_t *>(lds + KIDX);
+  auto idx_q = [&](int i) { return reinterpret_cast<const int32_t *>(lds + QIDX + (i & 3) * BMQ * 4); };
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -315,11 +369,20 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
     offr[j] = r;
     offc[j] = (cs ^ swz<D>(r)) * 8;
   }
-  auto issue_tile = [&](int qt, int stage) {
+  // Copies of the query tile of list entry i: Q, dout and the rows' stats
+  // (GATHER: row r of the tile is the row its index slot names).
+  auto issue_tile = [&](int i, int stage) {
     char *base = lds + stage * STAGE;
+    const int qt = tile_of(i);
     int64_t roff[CPW];
+    if constexpr (GATHER) {
+      const int32_t *rows = idx_q(i);
 #pragma unroll
-    for (int j = 0; j < CPW; ++j) roff[j] = (int64_t)min(qt * BMQ + offr[j], a.N - 1) * D + offc[j];
+      for (int j = 0; j < CPW; ++j) roff[j] = (int64_t)rows[offr[j]] * D + offc[j];
+    } else {
+#pragma unroll
+      for (int j = 0; j < CPW; ++j) roff[j] = (int64_t)min(qt * BMQ + offr[j], a.N - 1) * D + offc[j];
+    }
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
       lds_dma16(Q + roff[j], lds_addr(base + (j * 4 + wave) * 1024));
@@ -329,8 +392,18 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
     // stats value f of the tile = component f % 2 of row f / 2
     if (lane < SL) {
       const int f = wave * SL + lane;
-      lds_dma4(S + 2 * (int64_t)min(qt * BMQ + f / 2, a.N - 1) + (f & 1),
-               lds_addr(base + SOFF + wave * SL * 4));
+      const int64_t row = GATHER ? (int64_t)idx_q(i)[f / 2] : (int64_t)min(qt * BMQ + f / 2, a.N - 1);
+      lds_dma4(S + 2 * row + (f & 1), lds_addr(base + SOFF + wave * SL * 4));
+    }
+  };
+  // GATHER: the row indices of list entry i (first wave, one per lane) into its
+  // slot; positions past the end of the sequence read entry N - 1.
+  auto issue_idx = [&](int i) {
+    if (wave == 0) {
+#pragma unroll
+      for (int c = 0; c < BMQ / 64; ++c)
+        lds_dma4(a.order + min(tile_of(i) * BMQ + 64 * c + lane, a.N - 1),
+                 lds_addr(lds + QIDX + (i & 3) * BMQ * 4 + 256 * c));
     }
   };
 
@@ -353,24 +426,38 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   }
   const float sl2 = a.scale_log2;
 
-  if (ntot > 0) issue_tile(tile_of(0), 0);
+  if constexpr (GATHER) {
+    // Row indices of the key tile and of the first two query tiles, first.
+    if (wave == 0)
+      lds_dma4(a.order + min(k0 + lane, a.N - 1), lds_addr(lds + KIDX));
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      if (i < ntot) issue_idx(i);
+    wait_then_barrier<0>();
+  }
+  if (ntot > 0) issue_tile(0, 0);
   // The wave's own k and v rows, loaded after the first copy so that both
   // latencies overlap; one wait the compiler can see then covers both, so it
   // inserts no wait of its own inside the loop.
   // (a key row past the end of the sequence reads row N - 1 and stores nothing)
-  const int kc = min(kpos, a.N - 1);
+  const int64_t krow = GATHER ? (int64_t)idx_k[kb * 32 + col] : (int64_t)min(kpos, a.N - 1);
   bf16x8 kop[NCH], vop[NCH];
 #pragma unroll
   for (int c = 0; c < NCH; ++c) {
-    kop[c] = *reinterpret_cast<const bf16x8 *>(K + (int64_t)kc * D + half * (D / 2) + 8 * c);
-    vop[c] = *reinterpret_cast<const bf16x8 *>(V + (int64_t)kc * D + half * (D / 2) + 8 * c);
+    kop[c] = *reinterpret_cast<const bf16x8 *>(K + krow * D + half * (D / 2) + 8 * c);
+    vop[c] = *reinterpret_cast<const bf16x8 *>(V + krow * D + half * (D / 2) + 8 * c);
   }
   wait_vmem_all();
 
   for (int it = 0; it < ntot; ++it) {
     const int stage = it % kStagesKv;
     wait_then_barrier<0>();
-    if (it + 1 < ntot) issue_tile(tile_of(it + 1), (it + 1) % kStagesKv);
+    // (GATHER: entry it + 1's indices arrived with the wait above; entry it + 2's
+    // go out first, into slot (it + 2) % 4, last read for entry it - 2.)
+    if constexpr (GATHER) {
+      if (it + 2 < ntot) issue_idx(it + 2);
+    }
+    if (it + 1 < ntot) issue_tile(it + 1, (it + 1) % kStagesKv);
     const char *st = lds + stage * STAGE;
     const int qt = tile_of(it);
 
@@ -450,21 +537,30 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   __bf16 *Os = reinterpret_cast<__bf16 *>(lds) + wave * 32 * (D + 8);
   stage_rows<D>(res, qh == 0 ? a.scale : 1.f, Os, col, half);
   __syncthreads();
-  __bf16 *dst = static_cast<__bf16 *>(qh == 0 ? a.dk : a.dv) + slice + (int64_t)(k0 + kb * 32) * D;
-  write_rows<D>(Os, dst, lane, a.N - (k0 + kb * 32));
+  __bf16 *dst = static_cast<__bf16 *>(qh == 0 ? a.dk : a.dv) + slice;
+  if constexpr (GATHER)
+    write_rows<D>(Os, dst, lane, a.N - (k0 + kb * 32), idx_k + kb * 32);
+  else
+    write_rows<D>(Os, dst + (int64_t)(k0 + kb * 32) * D, lane, a.N - (k0 + kb * 32));
 }
 
 template <int D, int NW>
 hipError_t launch_dq(const AttnBwdArgs &a, hipStream_t s) {
   const int64_t blocks = (int64_t)a.BH * a.n_qtiles;
-  hipLaunchKernelGGL((attn_bwd_dq_bf16<D, NW>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
+  if (a.order)
+    hipLaunchKernelGGL((attn_bwd_dq_bf16<D, NW, true>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_bwd_dq_bf16<D, NW, false>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
   return hipGetLastError();
 }
 
 template <int D, int BMQ>
 hipError_t launch_dkdv(const AttnBwdArgs &a, hipStream_t s) {
   const int64_t blocks = (int64_t)a.BH * a.n_ktiles;
-  hipLaunchKernelGGL((attn_bwd_dkdv_bf16<D, BMQ>), dim3((uint32_t)blocks), dim3(256), 0, s, a);
+  if (a.order)
+    hipLaunchKernelGGL((attn_bwd_dkdv_bf16<D, BMQ, true>), dim3((uint32_t)blocks), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_bwd_dkdv_bf16<D, BMQ, false>), dim3((uint32_t)blocks), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

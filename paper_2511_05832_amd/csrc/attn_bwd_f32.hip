@@ -45,15 +45,17 @@ __global__ void __launch_bounds__(BM * (D / E)) attn_bwd_dq_f32(AttnBwdArgs a) {
 
   // A query row past the end of the sequence (ragged last query tile) reads row
   // N - 1 and stores nothing; key rows past it read row N - 1 and are masked.
-  const int qc = min(qpos, a.N - 1);
+  // With an order (fused reordering) sequence position i is stored in row order[i].
+  auto row_of = [&](int i) -> int64_t { return a.order ? (int64_t)a.order[i] : (int64_t)i; };
+  const int64_t qrow = row_of(min(qpos, a.N - 1));
   float q[E], g[E], acc[E];
 #pragma unroll
   for (int i = 0; i < E; ++i) {
-    q[i] = Q[(int64_t)qc * D + part * E + i];
-    g[i] = G[(int64_t)qc * D + part * E + i];
+    q[i] = Q[qrow * D + part * E + i];
+    g[i] = G[qrow * D + part * E + i];
     acc[i] = 0.f;
   }
-  const float2 rs = *reinterpret_cast<const float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qc));
+  const float2 rs = *reinterpret_cast<const float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qrow));
   const PatternArgs &P = a.pat;
   const Region R = region_of<true>(P, qpos);
   const float sl2 = a.scale_log2;
@@ -66,7 +68,7 @@ __global__ void __launch_bounds__(BM * (D / E)) attn_bwd_dq_f32(AttnBwdArgs a) {
     const int kt = masked ? prow[it - nf] : frow[it];
     __syncthreads();
     for (int i = tid; i < BN * D / 4; i += NT) {
-      const int64_t row = min(kt * BN + i / (D / 4), a.N - 1);
+      const int64_t row = row_of(min(kt * BN + i / (D / 4), a.N - 1));
       reinterpret_cast<float4 *>(Ks)[i] = reinterpret_cast<const float4 *>(K + row * D)[i % (D / 4)];
       reinterpret_cast<float4 *>(Vs)[i] = reinterpret_cast<const float4 *>(V + row * D)[i % (D / 4)];
     }
@@ -90,7 +92,7 @@ __global__ void __launch_bounds__(BM * (D / E)) attn_bwd_dq_f32(AttnBwdArgs a) {
     }
   }
   if (qpos >= a.N) return;
-  float *dQ = static_cast<float *>(a.dq) + slice + (int64_t)qpos * D + part * E;
+  float *dQ = static_cast<float *>(a.dq) + slice + qrow * D + part * E;
 #pragma unroll
   for (int i = 0; i < E; i += 4)
     *reinterpret_cast<float4 *>(dQ + i) =
@@ -120,12 +122,14 @@ __global__ void __launch_bounds__(BN * (D / E)) attn_bwd_dkdv_f32(AttnBwdArgs a)
 
   // A key row past the end of the sequence (ragged last key tile) reads row
   // N - 1 and stores nothing; query rows past it read row N - 1 and are masked.
-  const int kc = min(kpos, a.N - 1);
+  // With an order (fused reordering) sequence position i is stored in row order[i].
+  auto row_of = [&](int64_t i) -> int64_t { return a.order ? (int64_t)a.order[i] : i; };
+  const int64_t krow = row_of(min(kpos, a.N - 1));
   float k[E], v[E], dk[E], dv[E];
 #pragma unroll
   for (int i = 0; i < E; ++i) {
-    k[i] = K[(int64_t)kc * D + part * E + i];
-    v[i] = V[(int64_t)kc * D + part * E + i];
+    k[i] = K[krow * D + part * E + i];
+    v[i] = V[krow * D + part * E + i];
     dk[i] = 0.f;
     dv[i] = 0.f;
   }
@@ -143,11 +147,11 @@ __global__ void __launch_bounds__(BN * (D / E)) attn_bwd_dkdv_f32(AttnBwdArgs a)
       const int64_t r0 = (int64_t)qt * BMQ + c0;
       __syncthreads();
       for (int i = tid; i < QC * D / 4; i += NT) {
-        const int64_t row = min(r0 + i / (D / 4), (int64_t)a.N - 1);
+        const int64_t row = row_of(min(r0 + i / (D / 4), (int64_t)a.N - 1));
         reinterpret_cast<float4 *>(Qs)[i] = reinterpret_cast<const float4 *>(Q + row * D)[i % (D / 4)];
         reinterpret_cast<float4 *>(Gs)[i] = reinterpret_cast<const float4 *>(G + row * D)[i % (D / 4)];
       }
-      for (int i = tid; i < 2 * QC; i += NT) Ss[i] = S[2 * min(r0 + i / 2, (int64_t)a.N - 1) + (i & 1)];
+      for (int i = tid; i < 2 * QC; i += NT) Ss[i] = S[2 * row_of(min(r0 + i / 2, (int64_t)a.N - 1)) + (i & 1)];
       __syncthreads();
       for (int j = 0; j < QC; ++j) {
         const float *qr = Qs + j * D + part * E;
@@ -172,8 +176,8 @@ __global__ void __launch_bounds__(BN * (D / E)) attn_bwd_dkdv_f32(AttnBwdArgs a)
     }
   }
   if (kpos >= a.N) return;
-  float *dK = static_cast<float *>(a.dk) + slice + (int64_t)kpos * D + part * E;
-  float *dV = static_cast<float *>(a.dv) + slice + (int64_t)kpos * D + part * E;
+  float *dK = static_cast<float *>(a.dk) + slice + krow * D + part * E;
+  float *dV = static_cast<float *>(a.dv) + slice + krow * D + part * E;
 #pragma unroll
   for (int i = 0; i < E; i += 4) {
     *reinterpret_cast<float4 *>(dK + i) =

@@ -323,10 +323,11 @@ hla_status hla_attn_fwd_rpb(const void *q, const void *k, const void *v, const i
                   stream, "hla_attn_fwd_rpb");
 }
 
-hla_status hla_attn_bwd(const void *q, const void *k, const void *v, const void *out,
-                        const void *dout, const float *lse, const hla_block_mask *mask, void *dq,
-                        void *dk, void *dv, float *stats, int64_t B, int64_t heads, int64_t N,
-                        int64_t d, hla_dtype dtype, float scale, hla_stream_t stream) {
+static hla_status attn_bwd(const void *q, const void *k, const void *v, const void *out,
+                           const void *dout, const float *lse, const int32_t *order,
+                           const hla_block_mask *mask, void *dq, void *dk, void *dv, float *stats,
+                           int64_t B, int64_t heads, int64_t N, int64_t d, hla_dtype dtype,
+                           float scale, hla_stream_t stream, const char *name) {
   hla_status st;
   const void *ins[5] = {q, k, v, out, dout};
   const char *in_names[5] = {"q", "k", "v", "out", "dout"};
@@ -358,6 +359,11 @@ hla_status hla_attn_bwd(const void *q, const void *k, const void *v, const void 
       return fail(HLA_ERR_INVALID_ARG, "stats overlaps %s", in_names[j]);
   if (overlaps(stats, BH * N * 8, lse, BH * N * 4))
     return fail(HLA_ERR_INVALID_ARG, "stats overlaps lse");
+  if (order) {
+    for (int i = 0; i < 3; ++i)
+      if (overlaps(order, N * 4, outs[i], bytes)) return fail(HLA_ERR_INVALID_ARG, "order overlaps %s", out_names[i]);
+    if (overlaps(order, N * 4, stats, BH * N * 8)) return fail(HLA_ERR_INVALID_ARG, "order overlaps stats");
+  }
   hla::AttnBwdArgs a;
   a.q = q;
   a.k = k;
@@ -369,6 +375,7 @@ hla_status hla_attn_bwd(const void *q, const void *k, const void *v, const void 
   a.dq = dq;
   a.dk = dk;
   a.dv = dv;
+  a.order = order;
   a.n_full = mask->n_full;
   a.full_idx = mask->full_idx;
   a.n_part = mask->n_part;
@@ -388,7 +395,26 @@ hla_status hla_attn_bwd(const void *q, const void *k, const void *v, const void 
       dtype == HLA_BF16
           ? hla::launch_attn_bwd_bf16(a, (int)d, mask->tile_m, mask->tile_n, (hipStream_t)stream)
           : hla::launch_attn_bwd_f32(a, (int)d, mask->tile_m, mask->tile_n, (hipStream_t)stream);
-  return hip_status(e, "hla_attn_bwd");
+  return hip_status(e, name);
+}
+
+hla_status hla_attn_bwd(const void *q, const void *k, const void *v, const void *out,
+                        const void *dout, const float *lse, const hla_block_mask *mask, void *dq,
+                        void *dk, void *dv, float *stats, int64_t B, int64_t heads, int64_t N,
+                        int64_t d, hla_dtype dtype, float scale, hla_stream_t stream) {
+  return attn_bwd(q, k, v, out, dout, lse, nullptr, mask, dq, dk, dv, stats, B, heads, N, d, dtype,
+                  scale, stream, "hla_attn_bwd");
+}
+
+hla_status hla_attn_bwd_perm(const void *q, const void *k, const void *v, const void *out,
+                             const void *dout, const float *lse, const int32_t *order,
+                             const hla_block_mask *mask, void *dq, void *dk, void *dv,
+                             float *stats, int64_t B, int64_t heads, int64_t N, int64_t d,
+                             hla_dtype dtype, float scale, hla_stream_t stream) {
+  if (!order) return fail(HLA_ERR_INVALID_ARG, "order is NULL");
+  if (!aligned(order, 16)) return fail(HLA_ERR_INVALID_ARG, "order is not 16-byte aligned");
+  return attn_bwd(q, k, v, out, dout, lse, order, mask, dq, dk, dv, stats, B, heads, N, d, dtype,
+                  scale, stream, "hla_attn_bwd_perm");
 }
 
 hla_status hla_qkv_proj(const void *x, const void *w_qkv, void *q, void *k, void *v, int64_t B,

@@ -110,6 +110,9 @@ struct AttnBwdArgs {
   const float *lse;
   float *stats;  // per row: (lse * log2 e, delta), 2 floats
   void *dq, *dk, *dv;
+  // Fused reordering: every tensor (and lse, stats) stored in grid order, and
+  // sequence position i is row order[i]; NULL: tensors in sequence order.
+  const int32_t *order;
   const int32_t *n_full, *full_idx, *n_part, *part_idx;          // per query-tile row
   const int32_t *n_full_t, *full_idx_t, *n_part_t, *part_idx_t;  // per key-tile column
   int32_t BH, N, n_qtiles, n_ktiles;

@@ -244,6 +244,28 @@ def test_attn_bwd_validation(L):
     assert call(fake_mask(tm=256, tn=64)) == hla.HLA_ERR_UNSUPPORTED
 
 
+def test_attn_bwd_perm_validation(L):
+    """The fused-reordering backward checks its order array, then everything
+    hla_attn_bwd checks; every call here is invalid, so nothing is launched."""
+    vp = ctypes.c_void_p
+    N, B, heads, d = 4096, 2, 4, 64
+    base = [vp(0x10000000 + i * 0x1000000) for i in range(11)]
+    q, k, v, o, g, lse, dq, dk, dv, st, order = base
+    m = fake_mask()
+    m.n_full_t = m.full_idx_t = m.n_part_t = m.part_idx_t = 0x60000
+
+    def call(**kw):
+        a = dict(order=order, dq=dq, d=d)
+        a.update(kw)
+        return L.hla_attn_bwd_perm(q, k, v, o, g, lse, a["order"], ctypes.byref(m), a["dq"], dk, dv,
+                                   st, B, heads, N, a["d"], hla.HLA_BF16, 0.125, None)
+
+    assert call(order=None) == hla.HLA_ERR_INVALID_ARG and "order" in L.hla_last_error().decode()
+    assert call(order=vp(order.value + 4)) == hla.HLA_ERR_INVALID_ARG and "16-byte" in L.hla_last_error().decode()
+    assert call(order=vp(dq.value + 4096)) == hla.HLA_ERR_INVALID_ARG and "overlap" in L.hla_last_error().decode()
+    assert call(d=48) == hla.HLA_ERR_UNSUPPORTED
+
+
 def test_proj_validation(L):
     vp = ctypes.c_void_p
     x, w, q, k, v = (vp(0x100000 * i) for i in range(1, 6))

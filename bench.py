@@ -573,7 +573,9 @@ def main():
     ap.add_argument("--compare", default=None,
                     help="workload timed through the same kernel for the row-major comparison")
     ap.add_argument("--all", action="store_true",
-                    help="also time every workload and write gpurun_out/bench_all.json")
+                    help="also time every workload (each one's results on stderr)")
+    ap.add_argument("--all-out", default=None,
+                    help="with --all, also write every workload's results to this JSON file")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-backward", action="store_true",
                     help="skip timing the backward pass of the workload")
@@ -662,9 +664,10 @@ def main():
             print(f"[bench] {name}: {json.dumps(r)}", file=sys.stderr, flush=True)
             del p
             torch.cuda.empty_cache()
-        os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
-        with open(os.path.join(ROOT, "gpurun_out", "bench_all.json"), "w") as f:
-            json.dump(allres, f, indent=1)
+        if args.all_out:
+            os.makedirs(os.path.dirname(os.path.abspath(args.all_out)), exist_ok=True)
+            with open(args.all_out, "w") as f:
+                json.dump(allres, f, indent=1)
 
     flops = res["tile_flops"]
     attn_s = res["attn_ms"] * 1e-3

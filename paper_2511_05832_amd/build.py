@@ -24,7 +24,7 @@ LIB = os.path.join(PKG, "libhla.so")
 ARCH = "gfx950"
 
 SOURCES = ["hla_api.cpp", "hilbert.hip", "permute.hip", "blockmask.hip",
-           "attn_bf16.hip", "attn_f32.hip", "attn_bwd_stats.hip", "attn_bwd_bf16.hip",
+           "attn_bf16.hip", "attn_f32.hip", "attn_bwd_bf16.hip",
            "attn_bwd_f32.hip", "proj.hip"]
 
 

@@ -5,14 +5,16 @@
 // backward of every attention it measures, Tables 1, 3, 6, 7, 9, 11) over the same
 // tile structure - empty tiles skipped, full tiles unmasked, partial tiles with
 // the element mask (Sec. 3.1; Eq. 1's per-block cost applies to both passes).
-// With the forward's lse and delta_i = <dout_i, out_i> (row statistics kernel):
+// With the forward's lse and delta_i = <dout_i, out_i> (sum_j P_ij dP_ij, since
+// out_i = sum_j P_ij v_j):
 //   P_ij  = exp(scale <q_i, k_j> - lse_i)   (0 where masked)
 //   dS_ij = P_ij (<dout_i, v_j> - delta_i)
 //   dq_i  = scale sum_j dS_ij k_j       dk_j = scale sum_i dS_ij q_i
 //   dv_j  = sum_i P_ij dout_i
 // Two kernels and no atomics, so every result is deterministic:
 //   dq kernel    one workgroup per (b*h, query tile), walking that tile row's list
-//                of key tiles (as the forward does);
+//                of key tiles (as the forward does); it also computes each row's
+//                statistics (lse * log2 e, delta) and stores them for the next;
 //   dkdv kernel  one workgroup per (b*h, key tile), walking that key tile
 //                column's list of query tiles (the transposed lists).
 // P and dP are recomputed in both; the recomputation costs two of the seven
@@ -232,9 +234,26 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
     qop[c] = *reinterpret_cast<const bf16x8 *>(Q + qrow * D + half * (D / 2) + 8 * c);
     gop[c] = *reinterpret_cast<const bf16x8 *>(G + qrow * D + half * (D / 2) + 8 * c);
   }
-  const float2 rs = *reinterpret_cast<const float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qrow));
-  const float lse2 = rs.x, delta = rs.y;
+  // This query's row statistics, computed here and stored for the dk/dv kernel:
+  // delta = <dout, out> (this lane's half of d, then the other half's from lane
+  // ^ 32) and lse * log2 e (+inf for a row with no allowed key, which makes every
+  // recomputed weight exp2(s - inf) = 0 without a special case).
+  const __bf16 *O = static_cast<const __bf16 *>(a.out) + slice;
+  bf16x8 oop[NCH];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c)
+    oop[c] = *reinterpret_cast<const bf16x8 *>(O + qrow * D + half * (D / 2) + 8 * c);
+  const float lraw = a.lse[(int64_t)bh * a.N + qrow];
   wait_vmem_all();
+  float dpart = 0.f;
+#pragma unroll
+  for (int c = 0; c < NCH; ++c)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dpart = __builtin_fmaf((float)oop[c][e], (float)gop[c][e], dpart);
+  const float delta = dpart + __shfl_xor(dpart, 32);
+  const float lse2 = lraw == -__builtin_inff() ? __builtin_inff() : lraw * 1.4426950408889634f;
+  if (half == 0 && qpos < a.N)
+    *reinterpret_cast<float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qrow)) = make_float2(lse2, delta);
 
   for (int it = 0; it < ntot; ++it) {
     const int stage = it % kStagesDq;
@@ -566,9 +585,8 @@ hipError_t launch_dkdv(const AttnBwdArgs &a, hipStream_t s) {
 
 template <int D, int BM>
 hipError_t launch_all(const AttnBwdArgs &a, hipStream_t s) {
-  hipError_t e = launch_bwd_stats(a, D, true, s);
-  if (e != hipSuccess) return e;
-  e = launch_dq<D, BM / 32>(a, s);
+  // the dq kernel also writes the row statistics the dk/dv kernel reads
+  hipError_t e = launch_dq<D, BM / 32>(a, s);
   if (e != hipSuccess) return e;
   return launch_dkdv<D, BM>(a, s);
 }

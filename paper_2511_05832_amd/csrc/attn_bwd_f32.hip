@@ -8,7 +8,8 @@
 // products are combined with one cross-lane exchange.
 //
 //   dq kernel    one thread group per query row; K and V tiles of the row list
-//                staged in LDS and read as broadcasts.
+//                staged in LDS and read as broadcasts; it also computes the row's
+//                statistics (lse * log2 e, delta = <dout, out>) and stores them.
 //   dkdv kernel  one thread group per key row; query, dout and stats tiles of
 //                the column list staged in LDS, QC query rows at a time.
 #include "attn_common.h"
@@ -55,7 +56,17 @@ __global__ void __launch_bounds__(BM * (D / E)) attn_bwd_dq_f32(AttnBwdArgs a) {
     g[i] = G[qrow * D + part * E + i];
     acc[i] = 0.f;
   }
-  const float2 rs = *reinterpret_cast<const float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qrow));
+  // This query's row statistics, computed here and stored for the dk/dv kernel:
+  // (lse * log2 e, +inf for a row with no allowed key; delta = <dout, out>).
+  const float *O = static_cast<const float *>(a.out) + slice;
+  float dpart = 0.f;
+#pragma unroll
+  for (int i = 0; i < E; ++i) dpart = __builtin_fmaf(O[qrow * D + part * E + i], g[i], dpart);
+  const float lraw = a.lse[(int64_t)bh * a.N + qrow];
+  const float2 rs = make_float2(lraw == -__builtin_inff() ? __builtin_inff() : lraw * 1.4426950408889634f,
+                                row_sum<TPR>(dpart));
+  if (part == 0 && qpos < a.N)
+    *reinterpret_cast<float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qrow)) = rs;
   const PatternArgs &P = a.pat;
   const Region R = region_of<true>(P, qpos);
   const float sl2 = a.scale_log2;
@@ -188,11 +199,10 @@ __global__ void __launch_bounds__(BN * (D / E)) attn_bwd_dkdv_f32(AttnBwdArgs a)
 
 template <int D, int BM>
 hipError_t launch_all(const AttnBwdArgs &a, hipStream_t s) {
-  hipError_t e = launch_bwd_stats(a, D, false, s);
-  if (e != hipSuccess) return e;
+  // the dq kernel also writes the row statistics the dk/dv kernel reads
   hipLaunchKernelGGL((attn_bwd_dq_f32<D, BM>), dim3((uint32_t)((int64_t)a.BH * a.n_qtiles)),
                      dim3(BM * (D / E)), 0, s, a);
-  e = hipGetLastError();
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((attn_bwd_dkdv_f32<D, BM>), dim3((uint32_t)((int64_t)a.BH * a.n_ktiles)),
                      dim3(BN * (D / E)), 0, s, a);

@@ -120,8 +120,6 @@ struct AttnBwdArgs {
   PatternArgs pat;
 };
 
-// Per-row (lse * log2 e, delta = <dout, out>) into a.stats; d in {32, 64}.
-hipError_t launch_bwd_stats(const AttnBwdArgs &a, int d, bool bf16, hipStream_t s);
 
 // Row statistics, then the query gradients (row lists), then the key and value
 // gradients (column lists), all on stream s.

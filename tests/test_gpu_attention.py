@@ -63,6 +63,16 @@ def test_paper_grids_that_are_not_powers_of_two(pat, B, Hh, tm, rows):
     check(pat, q, k, v, tm, 64, 0.125, "bf16", rows=rows)
 
 
+def test_largest_grid_sampled_rows():
+    """A 512 x 512 grid (N = 262144, 2048 x 4096 tiles) through the launch
+    configuration of the measured workloads: positions, tile indices and in-slice
+    offsets at four times the 256 x 256 band's range."""
+    pat = Pat("hilbert_window", 512, 512, 1024)
+    q, k, v = W.attn_inputs(1, 1, pat.N, 64, "bf16", 512)
+    rows = sample_rows(pat.N, 128, 5, n_random=64)
+    check(pat, q, k, v, 128, 64, 0.125, "bf16", rows=rows)
+
+
 def random_cases(n):
     rng = np.random.default_rng(77)
     kinds = list(hla.PATTERN_IDS)

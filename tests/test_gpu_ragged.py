@@ -52,7 +52,9 @@ ODD = [(Pat("hilbert_slide", 7, 9, 10), 64, "bf16", 64),        # N = 63: one ti
        (Pat("rowmajor_slide", 9, 15, 2, 3), 128, "f32", 64),    # N = 135
        (Pat("hilbert_neighborhood", 11, 11, 25), 64, "f32", 32),  # N = 121
        (Pat("rowmajor_window", 13, 10, 4, 3), 64, "bf16", 64),  # N = 130
-       (Pat("hilbert_shifted_window", 9, 21, 40, 17), 128, "bf16", 64)]  # N = 189
+       (Pat("hilbert_shifted_window", 9, 21, 40, 17), 128, "bf16", 64),  # N = 189
+       (Pat("hilbert_slide", 1, 1, 0), 64, "bf16", 64),              # N = 1
+       (Pat("rowmajor_window", 1, 2, 1, 2), 128, "f32", 32)]         # N = 2
 
 
 def ragged_random(n):

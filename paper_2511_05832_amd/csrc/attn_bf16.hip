@@ -532,54 +532,54 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
     // Online softmax in the log2 domain with a lazily moved reference m_run
     // (O and l always share it). Once every row of the wave has a finite
     // reference, a tile first takes its weights against the reference as it
-    // stands, with no row max at all: weights up to 2^kFastLog2 are harmless
-    // (fp32 accumulators, bf16 operands), and since they are >= 0 their sum
-    // bounds each of them, so one compare of the sum (which is needed anyway;
-    // NaN and inf fail it too) validates the tile. Only when some row's sum
-    // fails does the tile fall back: its scores are recomputed from LDS and it
-    // takes the max path below.
+    // stands, with no row max at all: weights up to 2^32 are harmless (fp32
+    // accumulators, bf16 operands), and since they are >= 0 their sum bounds
+    // each of them, so one compare of the sum (which is needed anyway; NaN and
+    // inf fail it too) validates the tile. Only when some row's sum fails does
+    // the tile fall back: its scores are recomputed from LDS and it takes the
+    // max path. (Straight-line code rather than a retry loop: with a loop, the
+    // compiler kept O in two register sets and copied it on every tile.)
     f32x16 s[2];
-    bool fast = primed;
-    for (;;) {
-      // (keeps the compiler from hoisting the K operand reads out of this loop
-      // and holding them in registers across it)
-      asm volatile("" ::: "memory");
-      scores(s);
-      float m_ref = m_run;
-      if (!fast) {
-        // Max path: the reference moves only when a row's tile max exceeds it by
-        // more than kRescaleSlack, so the O / l rescale stays rare.
-        float mq[4];
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x16 &sv = s[g >> 1];
-          const int o = 8 * (g & 1);
-          mq[g] = fmaxf(fmaxf(fmaxf(sv[o], sv[o + 1]), fmaxf(sv[o + 2], sv[o + 3])),
-                        fmaxf(fmaxf(sv[o + 4], sv[o + 5]), fmaxf(sv[o + 6], sv[o + 7])));
-        }
-        const float mx = xhalf_max(fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3])));
-        const float mt = mx * smul;
-        const bool grow = mt > m_run + kRescaleSlack;
-        if (__ballot(grow)) {
-          const float m_new = grow ? mt : m_run;
-          // 1 where unchanged; a row with no allowed key yet has nothing to rescale
-          const float alpha = m_new == -__builtin_inff() ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-          l_run *= alpha;
-#pragma unroll
-          for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
-          m_run = m_new;
-        }
-        m_ref = m_run == -__builtin_inff() ? 0.f : m_run;
+    scores(s);
+    bool slow = !primed;
+    float lt = 0.f;
+    if (primed) {
+      lt = weights(s, m_run);
+      if (__ballot(!(lt <= kFastBound))) {
+        slow = true;
+        // (the memory clobber makes the K operand reads happen again instead of
+        // keeping the first ones in registers across the weights)
+        asm volatile("" ::: "memory");
+        scores(s);
       }
-      const float lt = weights(s, m_ref);
-      if (fast && __ballot(!(lt <= kFastBound))) {
-        fast = false;  // recompute the scores and take the max path
-        continue;
-      }
-      l_run += lt;
-      if (!fast) primed = !__ballot(m_run == -__builtin_inff());
-      break;
     }
+    if (slow) {
+      // Max path: the reference moves only when a row's tile max exceeds it by
+      // more than kRescaleSlack, so the O / l rescale stays rare.
+      float mq[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x16 &sv = s[g >> 1];
+        const int o = 8 * (g & 1);
+        mq[g] = fmaxf(fmaxf(fmaxf(sv[o], sv[o + 1]), fmaxf(sv[o + 2], sv[o + 3])),
+                      fmaxf(fmaxf(sv[o + 4], sv[o + 5]), fmaxf(sv[o + 6], sv[o + 7])));
+      }
+      const float mx = xhalf_max(fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3])));
+      const float mt = mx * smul;
+      const bool grow = mt > m_run + kRescaleSlack;
+      if (__ballot(grow)) {
+        const float m_new = grow ? mt : m_run;
+        // 1 where unchanged; a row with no allowed key yet has nothing to rescale
+        const float alpha = m_new == -__builtin_inff() ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
+        m_run = m_new;
+      }
+      lt = weights(s, m_run == -__builtin_inff() ? 0.f : m_run);
+      primed = !__ballot(m_run == -__builtin_inff());
+    }
+    l_run += lt;
     // Row sums above are fp32 sums of the unrounded weights; P goes to the PV
     // product rounded to bf16.
     bf16x8 pop[4];

@@ -61,8 +61,12 @@ __device__ __forceinline__ Cls axis_cls(int kind, int g, int off, int extent, in
   return c;
 }
 
+// A position interval [a, b] as up to three grid rectangles in fixed slots:
+// 0 = the first row's part, 1 = the whole rows between (if any), 2 = the last
+// row's part (if it is not the first row). Fixed slots keep every field in
+// registers (an array filled at a running index would live in scratch memory).
 struct Rects {
-  int n;
+  bool ok[3];
   int r0[3], r1[3], c0[3], c1[3];
 };
 
@@ -70,21 +74,16 @@ __device__ __forceinline__ Rects split_rows(int a, int b, int W) {
   Rects R;
   const int ra = a / W, ca = a - ra * W;
   const int rb = b / W, cb = b - rb * W;
-  if (ra == rb) {
-    R.n = 1;
-    R.r0[0] = ra; R.r1[0] = ra; R.c0[0] = ca; R.c1[0] = cb;
-    return R;
-  }
-  R.n = 0;
-  R.r0[R.n] = ra; R.r1[R.n] = ra; R.c0[R.n] = ca; R.c1[R.n] = W - 1; ++R.n;
-  if (rb - ra >= 2) {
-    R.r0[R.n] = ra + 1; R.r1[R.n] = rb - 1; R.c0[R.n] = 0; R.c1[R.n] = W - 1; ++R.n;
-  }
-  R.r0[R.n] = rb; R.r1[R.n] = rb; R.c0[R.n] = 0; R.c1[R.n] = cb; ++R.n;
+  const bool one_row = ra == rb;
+  R.ok[0] = true;
+  R.r0[0] = ra; R.r1[0] = ra; R.c0[0] = ca; R.c1[0] = one_row ? cb : W - 1;
+  R.ok[1] = rb - ra >= 2;
+  R.r0[1] = ra + 1; R.r1[1] = rb - 1; R.c0[1] = 0; R.c1[1] = W - 1;
+  R.ok[2] = !one_row;
+  R.r0[2] = rb; R.r1[2] = rb; R.c0[2] = 0; R.c1[2] = cb;
   return R;
 }
 
-// 0 = empty, 1 = partial, 2 = full
 __device__ int classify_tile(const PatternArgs &p, int i0, int i1, int j0, int j1) {
   switch (p.kind) {
     case HLA_HILBERT_WINDOW: {
@@ -112,8 +111,11 @@ __device__ int classify_tile(const PatternArgs &p, int i0, int i1, int j0, int j
   const Rects Q = split_rows(i0, i1, p.W);
   const Rects K = split_rows(j0, j1, p.W);
   bool any = false, all = true;
-  for (int a = 0; a < Q.n; ++a) {
-    for (int b = 0; b < K.n; ++b) {
+#pragma unroll
+  for (int a = 0; a < 3; ++a) {
+#pragma unroll
+    for (int b = 0; b < 3; ++b) {
+      if (!Q.ok[a] || !K.ok[b]) continue;
       const Cls cr = axis_cls(ax, p.p0, 0, p.H, Q.r0[a], Q.r1[a], K.r0[b], K.r1[b]);
       const Cls cc = axis_cls(ax, p.p1, 0, p.W, Q.c0[a], Q.c1[a], K.c0[b], K.c1[b]);
       any = any || (cr.any && cc.any);

@@ -274,14 +274,14 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
     }
   };
 
-  // LDS byte offsets (within a stage) of this lane's operand reads.
-  int kaddr[2][NCH];
+  // LDS byte offsets (within a stage) of this lane's K operand reads for the
+  // first 32-key block. The swizzle ignores row bit 5, so the second block's
+  // reads sit exactly 32 rows further (an immediate offset of the LDS read).
+  int kaddr[NCH];
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
-    const int r = kb * 32 + row_perm(col);
-#pragma unroll
-    for (int c = 0; c < NCH; ++c)
-      kaddr[kb][c] = r * D * 2 + (((half * NCH + c) ^ swz_k<D>(r)) * 16);
+  for (int c = 0; c < NCH; ++c) {
+    const int r = row_perm(col);
+    kaddr[c] = r * D * 2 + (((half * NCH + c) ^ swz_k<D>(r)) * 16);
   }
   // V^T operand for (db, t): two transposing reads e = 0, 1. Lane i of 16-lane
   // group g points at row 16t + 8(g/2) + 4e + i/4, columns db*32 + 16(g%2) + 4(i%4).
@@ -459,7 +459,7 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
       for (int c = 0; c < NCH; ++c)
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
-          const bf16x8 kop = *reinterpret_cast<const bf16x8 *>(st + kaddr[kb][c]);
+          const bf16x8 kop = *reinterpret_cast<const bf16x8 *>(st + kaddr[c] + kb * 32 * D * 2);
           s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[c], s[kb], 0, 0, 0);
         }
       // RPB: scores in natural units plus the bias, s = scale * <q, k> + bias,

@@ -538,20 +538,32 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   auto xidx = [&](int which, int db, int v) {
     return (((kb * 2 + which) * NDB + db) * 16 + v) * 64 + lane;
   };
+  // (qh is wave-uniform: one branch around whole loops, not one per element)
+  const int give = qh == 1 ? 0 : 1, keep = 1 - give;
+  if (qh == 1) {
 #pragma unroll
-  for (int db = 0; db < NDB; ++db)
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      if (qh == 1) xch[xidx(0, db, v)] = dk[db][v];
-      else xch[xidx(1, db, v)] = dv[db][v];
-    }
+      for (int v = 0; v < 16; ++v) xch[xidx(give, db, v)] = dk[db][v];
+  } else {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) xch[xidx(give, db, v)] = dv[db][v];
+  }
   __syncthreads();
   f32x16 res[NDB];
+  if (qh == 0) {
 #pragma unroll
-  for (int db = 0; db < NDB; ++db)
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int v = 0; v < 16; ++v)
-      res[db][v] = qh == 0 ? dk[db][v] + xch[xidx(0, db, v)] : dv[db][v] + xch[xidx(1, db, v)];
+      for (int v = 0; v < 16; ++v) res[db][v] = dk[db][v] + xch[xidx(keep, db, v)];
+  } else {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) res[db][v] = dv[db][v] + xch[xidx(keep, db, v)];
+  }
   __syncthreads();
   __bf16 *Os = reinterpret_cast<__bf16 *>(lds) + wave * 32 * (D + 8);
   stage_rows<D>(res, qh == 0 ? a.scale : 1.f, Os, col, half);

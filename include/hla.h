@@ -251,7 +251,7 @@ hla_status hla_attn_fwd_rpb(const void *q, const void *k, const void *v,
  * returned by hla_attn_fwd for these q, k, v, mask and scale.
  * lse: float32 [B, heads, N] (required).
  * stats: caller-owned float32 [B, heads, N, 2] workspace, overwritten with
- * (lse_i * log2(e), delta_i) per row (+inf in place of the first where
+ * (lse_i * log2(e), -delta_i) per row (+inf in place of the first where
  * lse_i = -inf).
  * dq, dk, dv: [B, heads, N, d] of dtype; they may not overlap each other or any
  * input. A query with no allowed key contributes nothing.

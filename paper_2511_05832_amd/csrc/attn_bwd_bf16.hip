@@ -14,7 +14,7 @@
 // Two kernels and no atomics, so every result is deterministic:
 //   dq kernel    one workgroup per (b*h, query tile), walking that tile row's list
 //                of key tiles (as the forward does); it also computes each row's
-//                statistics (lse * log2 e, delta) and stores them for the next;
+//                statistics (lse * log2 e, -delta) and stores them for the next;
 //   dkdv kernel  one workgroup per (b*h, key tile), walking that key tile
 //                column's list of query tiles (the transposed lists).
 // P and dP are recomputed in both; the recomputation costs two of the seven
@@ -36,6 +36,8 @@
 // Register-resident weights. The A rows of S (dq: key rows; dkdv: query rows) are
 // fed permuted by row_perm, so the S and dP accumulators come out in the B-operand
 // layout of the next product, and P / dS go to bf16 operands in place.
+#include <type_traits>
+
 #include "attn_common.h"
 
 namespace hla {
@@ -253,9 +255,13 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
   const float delta = dpart + __shfl_xor(dpart, 32);
   const float lse2 = lraw == -__builtin_inff() ? __builtin_inff() : lraw * 1.4426950408889634f;
   if (half == 0 && qpos < a.N)
-    *reinterpret_cast<float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qrow)) = make_float2(lse2, delta);
+    *reinterpret_cast<float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qrow)) = make_float2(lse2, -delta);
 
-  for (int it = 0; it < ntot; ++it) {
+  // One key tile. MASKED is a compile-time flag: full and partial tiles run
+  // separate loop bodies (the lists hold the full tiles first), so neither
+  // carries the other's registers (one body with a run-time mask branch copied
+  // all 32 score accumulators on every full tile).
+  auto step = [&](int it, auto masked) __attribute__((always_inline)) {
     const int stage = it % kStagesDq;
     wait_tiles_then_barrier<LPT, kStagesDq - 2>(min(ntot - 1 - it, kStagesDq - 2));
     // (GATHER: the indices of entry it + 2 arrived with the wait above - the
@@ -278,7 +284,7 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
         const bf16x8 vop = *reinterpret_cast<const bf16x8 *>(st + TILE + raddr[kb][c]);
         dp[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, gop[c], dp[kb], 0, 0, 0);
       }
-    if (it >= nf) mask_blocks<2>(s, R, P, kt * BN + 8 * half);
+    if constexpr (decltype(masked)::value) mask_blocks<2>(s, R, P, kt * BN + 8 * half);
 
     bf16x8 dsop[4];
 #pragma unroll
@@ -296,7 +302,10 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
         const bf16x8 kto = lds_read_tr16x2(st + tbase[db] + (16 * t) * D * 2, D * 2);
         acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kto, dsop[t], acc[db], 0, 0, 0);
       }
-  }
+  };
+  int it = 0;
+  for (; it < nf; ++it) step(it, std::false_type{});
+  for (; it < ntot; ++it) step(it, std::true_type{});
 
   wait_then_barrier<0>();
   __bf16 *Os = reinterpret_cast<__bf16 *>(lds) + wave * 32 * (D + 8);
@@ -327,7 +336,8 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   constexpr int NT = 256;
   constexpr int CPR = D / 8;
   constexpr int QT = BMQ * D * 2;       // bytes of a Q (or dout) tile
-  constexpr int SOFF = 2 * QT;          // stats pairs after Q and dout
+  constexpr int SOFF = 2 * QT;          // stats after Q and dout: lse log2e of the rows,
+  constexpr int SND = SOFF + BMQ * 4;   // then -delta of the rows
   constexpr int STAGE = 2 * QT + BMQ * 8;
   constexpr int CPW = BMQ * CPR / NT;   // 16-byte copies per thread per tile (Q or dout)
   constexpr int SL = BMQ / 2;           // stats values copied per wave (4 bytes each)
@@ -408,11 +418,12 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
       lds_dma16(G + roff[j], lds_addr(base + QT + (j * 4 + wave) * 1024));
-    // stats value f of the tile = component f % 2 of row f / 2
+    // stats value f of the tile = component f / BMQ of row f % BMQ, so that the
+    // stage holds lse log2e of every row, then -delta of every row
     if (lane < SL) {
-      const int f = wave * SL + lane;
-      const int64_t row = GATHER ? (int64_t)idx_q(i)[f / 2] : (int64_t)min(qt * BMQ + f / 2, a.N - 1);
-      lds_dma4(S + 2 * row + (f & 1), lds_addr(base + SOFF + wave * SL * 4));
+      const int f = wave * SL + lane, r = f % BMQ;
+      const int64_t row = GATHER ? (int64_t)idx_q(i)[r] : (int64_t)min(qt * BMQ + r, a.N - 1);
+      lds_dma4(S + 2 * row + f / BMQ, lds_addr(base + SOFF + wave * SL * 4));
     }
   };
   // GATHER: the row indices of list entry i (first wave, one per lane) into its
@@ -468,7 +479,9 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   }
   wait_vmem_all();
 
-  for (int it = 0; it < ntot; ++it) {
+  // One query tile; full and partial tiles run separate loop bodies (as in the
+  // dq kernel).
+  auto step = [&](int it, auto masked) __attribute__((always_inline)) {
     const int stage = it % kStagesKv;
     wait_then_barrier<0>();
     // (GATHER: entry it + 1's indices arrived with the wait above; entry it + 2's
@@ -480,11 +493,20 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
     const char *st = lds + stage * STAGE;
     const int qt = tile_of(it);
 
+    // dP - delta directly: each dP accumulator starts at -delta of its rows. Slot
+    // v of block qb is row qh*HALF + 32qb + 16(v/8) + 8half + v%8 (two runs of
+    // eight rows), i.e. two 16-byte reads per run from the staged -delta.
     f32x16 s[QB], dp[QB];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       s[qb] = f32x16{};
-      dp[qb] = f32x16{};
+      const float4 *nd = reinterpret_cast<const float4 *>(st + SND + (qh * HALF + 32 * qb + 8 * half) * 4);
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        const float4 lo = nd[4 * g], hi = nd[4 * g + 1];
+        dp[qb][8 * g + 0] = lo.x; dp[qb][8 * g + 1] = lo.y; dp[qb][8 * g + 2] = lo.z; dp[qb][8 * g + 3] = lo.w;
+        dp[qb][8 * g + 4] = hi.x; dp[qb][8 * g + 5] = hi.y; dp[qb][8 * g + 6] = hi.z; dp[qb][8 * g + 7] = hi.w;
+      }
     }
 #pragma unroll
     for (int c = 0; c < NCH; ++c)
@@ -495,28 +517,25 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
         const bf16x8 ga = *reinterpret_cast<const bf16x8 *>(st + QT + raddr[qb][c]);
         dp[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ga, vop[c], dp[qb], 0, 0, 0);
       }
-    if (it >= nf) mask_blocks<QB>(s, R, P, qt * BMQ + qh * HALF + 8 * half);
+    if constexpr (decltype(masked)::value) mask_blocks<QB>(s, R, P, qt * BMQ + qh * HALF + 8 * half);
 
     bf16x8 pop[2 * QB], dsop[2 * QB];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
-        // rows qh*HALF + 32qb + 16g + 8half + (0..7): four 16-byte reads of
-        // (lse log2e, delta) pairs, every lane of a half on the same address
-        const float4 *sp = reinterpret_cast<const float4 *>(
-            st + SOFF + (qh * HALF + 32 * qb + 16 * g + 8 * half) * 8);
+        // rows qh*HALF + 32qb + 16g + 8half + (0..7): two 16-byte reads of their
+        // lse log2e, every lane of a half on the same address
+        const float4 *ls = reinterpret_cast<const float4 *>(
+            st + SOFF + (qh * HALF + 32 * qb + 16 * g + 8 * half) * 4);
+        const float4 la = ls[0], lb = ls[1];
+        const float l2[8] = {la.x, la.y, la.z, la.w, lb.x, lb.y, lb.z, lb.w};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float4 pr = sp[i];
-#pragma unroll
-          for (int e = 0; e < 2; ++e) {
-            const int v = 8 * g + 2 * i + e;
-            const float l2 = e ? pr.z : pr.x, dl = e ? pr.w : pr.y;
-            const float p = __builtin_amdgcn_exp2f(s[qb][v] * sl2 - l2);
-            pop[2 * qb + g][2 * i + e] = (__bf16)p;
-            dsop[2 * qb + g][2 * i + e] = (__bf16)(p * (dp[qb][v] - dl));
-          }
+        for (int e = 0; e < 8; ++e) {
+          const int v = 8 * g + e;
+          const float p = __builtin_amdgcn_exp2f(s[qb][v] * sl2 - l2[e]);
+          pop[2 * qb + g][e] = (__bf16)p;
+          dsop[2 * qb + g][e] = (__bf16)(p * dp[qb][v]);
         }
       }
 
@@ -529,7 +548,10 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
         const bf16x8 qto = lds_read_tr16x2(st + tbase[db] + (16 * t) * D * 2, D * 2);
         dk[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qto, dsop[t], dk[db], 0, 0, 0);
       }
-  }
+  };
+  int it = 0;
+  for (; it < nf; ++it) step(it, std::false_type{});
+  for (; it < ntot; ++it) step(it, std::true_type{});
 
   // Sum the two query halves: half 1 hands its dk to half 0, half 0 hands its dv
   // to half 1; then half 0 writes dk and half 1 writes dv.

@@ -9,7 +9,7 @@
 //
 //   dq kernel    one thread group per query row; K and V tiles of the row list
 //                staged in LDS and read as broadcasts; it also computes the row's
-//                statistics (lse * log2 e, delta = <dout, out>) and stores them.
+//                statistics (lse * log2 e, -delta; delta = <dout, out>) and stores them.
 //   dkdv kernel  one thread group per key row; query, dout and stats tiles of
 //                the column list staged in LDS, QC query rows at a time.
 #include "attn_common.h"
@@ -65,8 +65,9 @@ __global__ void __launch_bounds__(BM * (D / E)) attn_bwd_dq_f32(AttnBwdArgs a) {
   const float lraw = a.lse[(int64_t)bh * a.N + qrow];
   const float2 rs = make_float2(lraw == -__builtin_inff() ? __builtin_inff() : lraw * 1.4426950408889634f,
                                 row_sum<TPR>(dpart));
+  // stored as (lse log2e, -delta), the workspace's layout
   if (part == 0 && qpos < a.N)
-    *reinterpret_cast<float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qrow)) = rs;
+    *reinterpret_cast<float2 *>(a.stats + 2 * ((int64_t)bh * a.N + qrow)) = make_float2(rs.x, -rs.y);
   const PatternArgs &P = a.pat;
   const Region R = region_of<true>(P, qpos);
   const float sl2 = a.scale_log2;
@@ -177,7 +178,7 @@ __global__ void __launch_bounds__(BN * (D / E)) attn_bwd_dkdv_f32(AttnBwdArgs a)
         dp = row_sum<TPR>(dp);
         const bool ok = !masked || region_has(R, P, (int)r0 + j);
         const float p = ok ? __builtin_amdgcn_exp2f(__builtin_fmaf(s, sl2, -Ss[2 * j])) : 0.f;
-        const float ds = p * (dp - Ss[2 * j + 1]);
+        const float ds = p * (dp + Ss[2 * j + 1]);  // (the stats hold -delta)
 #pragma unroll
         for (int i = 0; i < E; ++i) {
           dv[i] = __builtin_fmaf(p, gr[i], dv[i]);

@@ -108,7 +108,7 @@ hipError_t launch_attn_f32(const AttnArgs &a, int d, int tile_m, int tile_n,
 struct AttnBwdArgs {
   const void *q, *k, *v, *out, *dout;
   const float *lse;
-  float *stats;  // per row: (lse * log2 e, delta), 2 floats
+  float *stats;  // per row: (lse * log2 e, -delta), 2 floats
   void *dq, *dk, *dv;
   // Fused reordering: every tensor (and lse, stats) stored in grid order, and
   // sequence position i is row order[i]; NULL: tensors in sequence order.

@@ -231,3 +231,24 @@ def test_column_lists_match_oracle():
         np.testing.assert_array_equal(mask.n_part_t.cpu().numpy(), ref.n_part)
         np.testing.assert_array_equal(mask.full_idx_t.cpu().numpy(), ref.full_idx)
         np.testing.assert_array_equal(mask.part_idx_t.cpu().numpy(), ref.part_idx)
+
+
+@pytest.mark.parametrize("dtype,d,tm", [("bf16", 64, 128), ("bf16", 32, 64), ("f32", 32, 64)], ids=str)
+def test_stats_workspace_contents(dtype, d, tm):
+    """The stats workspace holds, per row, (lse * log2 e, -delta) with delta =
+    <dout, out>, as the C header documents."""
+    pat = Pat("hilbert_slide", 16, 16, 20)
+    q, k, v = (t.to(DEV) for t in W.attn_inputs(2, 2, pat.N, d, dtype, 404))
+    g = dout_like(q, 405).to(DEV)
+    mask = hla.build_block_mask(pat, tm, 64, columns=True)
+    out, lse = hla.attn_fwd(q, k, v, mask, 0.125)
+    stats = torch.full((2, 2, pat.N, 2), float("nan"), dtype=torch.float32, device=DEV)
+    hla.attn_bwd(q, k, v, out, g, lse, mask, 0.125, stats=stats)
+    torch.cuda.synchronize()
+    st = stats.cpu().numpy().astype(np.float64)
+    want_l2 = (lse.cpu() * 1.4426950408889634).numpy().astype(np.float64)
+    np.testing.assert_allclose(st[..., 0], want_l2, rtol=1e-6, atol=0)
+    prod = np64(out.cpu()) * np64(g.cpu())
+    delta = prod.sum(-1)
+    bound = 1e-5 * np.abs(prod).sum(-1) + 1e-30
+    assert np.all(np.abs(st[..., 1] + delta) <= bound), float(np.max(np.abs(st[..., 1] + delta) / bound))

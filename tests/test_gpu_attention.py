@@ -73,6 +73,27 @@ def test_largest_grid_sampled_rows():
     check(pat, q, k, v, 128, 64, 0.125, "bf16", rows=rows)
 
 
+@pytest.mark.parametrize("pat,tm,d", [(Pat("hilbert_slide", 16, 16, 300), 128, 64),
+                                      (Pat("hilbert_slide", 16, 16, 100), 64, 64),
+                                      (Pat("rowmajor_slide", 16, 16, 7, 7), 128, 32)], ids=str)
+def test_growing_scores_take_the_max_path(pat, tm, d):
+    """Scores that jump by more than 2^32 in weight from one key tile to the next:
+    the tile taken against the stale softmax reference fails its row-sum check and
+    is recomputed on the max path, rescaling O and l (for the even rows only: odd
+    rows' queries point the other way, so their later tiles only shrink). Keys of
+    64-key tile t are scaled by 3^t; with positive keys and queries of +-0.5 the
+    scores grow about 3x per tile (log2 units of about 4.6, 14, 42, 125)."""
+    g = torch.Generator().manual_seed(2024 + d)
+    N = pat.N
+    k = torch.randn((1, 2, N, d), generator=g).abs()
+    k = k * (3.0 ** (torch.arange(N) // 64).float())[None, None, :, None]
+    sign = torch.where(torch.arange(N) % 2 == 0, 1.0, -1.0)
+    q = 0.5 * sign[None, None, :, None].expand(1, 2, N, d).clone()
+    v = torch.randn((1, 2, N, d), generator=g)
+    q, k, v = (t.to(torch.bfloat16) for t in (q, k, v))
+    check(pat, q, k, v, tm, 64, 0.125, "bf16", gather=False)
+
+
 def random_cases(n):
     rng = np.random.default_rng(77)
     kinds = list(hla.PATTERN_IDS)

@@ -13,8 +13,9 @@ import torch
 import paper_2511_05832_amd as hla
 import workloads as W
 from conftest import Pat
-from helpers import (TOL_LSE, TOL_OUT, max_abs, np64, oracle_attention,
+from helpers import (DEV, TOL_LSE, TOL_OUT, max_abs, np64, oracle_attention,
                      run_hip_attention, sample_rows)
+from oracle import attention as o_attn
 
 pytestmark = pytest.mark.gpu
 
@@ -91,7 +92,27 @@ def test_growing_scores_take_the_max_path(pat, tm, d):
     q = 0.5 * sign[None, None, :, None].expand(1, 2, N, d).clone()
     v = torch.randn((1, 2, N, d), generator=g)
     q, k, v = (t.to(torch.bfloat16) for t in (q, k, v))
-    check(pat, q, k, v, tm, 64, 0.125, "bf16", gather=False)
+    out, lse = check(pat, q, k, v, tm, 64, 0.125, "bf16", gather=False)
+    mask = hla.build_block_mask(pat, tm, 64)
+    qd, kd, vd = (t.to(DEV) for t in (q, k, v))
+    # the same tiles through the reordering mode: a random order, bit for bit
+    # against gather -> attention -> scatter
+    order = torch.randperm(N, generator=g).to(torch.int32).to(DEV)
+    qs, ks, vs = (torch.empty_like(t) for t in (qd, kd, vd))
+    qs[:, :, order.long()], ks[:, :, order.long()], vs[:, :, order.long()] = qd, kd, vd
+    out_p, lse_p = hla.attn_fwd_perm(qs, ks, vs, order, mask, 0.125)
+    torch.cuda.synchronize()
+    assert torch.equal(out_p[:, :, order.long()].cpu(), out)
+    assert torch.equal(lse_p[:, :, order.long()].cpu(), lse)
+    # and through the position-bias mode with a table of zeros (the bias, read
+    # again by the recomputation, adds nothing)
+    table = torch.zeros((2, 2 * pat.H - 1, 2 * pat.W - 1), device=DEV)
+    ident = torch.arange(N, dtype=torch.int32, device=DEV)
+    out_b, lse_b = hla.attn_fwd_rpb(qd, kd, vd, ident, table, mask, 0.125)
+    torch.cuda.synchronize()
+    ref_out, ref_lse = o_attn.attention(np64(q), np64(k), np64(v), pat, 0.125)
+    assert max_abs(np64(out_b.cpu()), ref_out) <= TOL_OUT["bf16"]
+    assert max_abs(np64(lse_b.cpu()), ref_lse) <= TOL_LSE
 
 
 def random_cases(n):

@@ -252,3 +252,32 @@ def test_stats_workspace_contents(dtype, d, tm):
     delta = prod.sum(-1)
     bound = 1e-5 * np.abs(prod).sum(-1) + 1e-30
     assert np.all(np.abs(st[..., 1] + delta) <= bound), float(np.max(np.abs(st[..., 1] + delta) / bound))
+
+
+@pytest.mark.parametrize("pat,tm", [(Pat("hilbert_slide", 16, 16, 300), 128),
+                                    (Pat("rowmajor_slide", 16, 16, 7, 7), 64)], ids=str)
+@pytest.mark.parametrize("dtype,growth", [("f32", 3.0), ("bf16", 2.0)], ids=str)
+def test_growing_scores(pat, tm, dtype, growth):
+    """Keys of 64-key tile t scaled by growth^t and queries of +-0.5 (as in the
+    forward's max-path test): scores spread over up to about 120 log2 units across
+    a row, so P is recomputed from an lse far above most of the row's scores. fp32
+    at 3^t checks that arithmetic at the fp32 bar. bf16 runs at 2^t: at 3^t its
+    dq error reaches 2.1% of max |dq| (dS sums to zero along a row, and its bf16
+    rounding is multiplied by keys up to 27 times larger), just past the bar."""
+    g = torch.Generator().manual_seed(77)
+    N, d = pat.N, 32 if dtype == "f32" else 64
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    k = torch.randn((1, 2, N, d), generator=g).abs()
+    k = k * (growth ** (torch.arange(N) // 64).float())[None, None, :, None]
+    sign = torch.where(torch.arange(N) % 2 == 0, 1.0, -1.0)
+    q = 0.5 * sign[None, None, :, None].expand(1, 2, N, d).clone()
+    v = torch.randn((1, 2, N, d), generator=g)
+    q, k, v = (t.to(tdt) for t in (q, k, v))
+    dout = dout_like(q, 78)
+    got = run_hip(pat, q, k, v, dout, tm, 64, 0.125, gather=False)
+    ref = oracle(pat, q, k, v, dout, 0.125, gather=False)
+    for name, a, r in zip(("dq", "dk", "dv"), got, ref):
+        gs = max(1.0, float(np.abs(r).max()))
+        err = max_abs(np64(a), r)
+        print(f"{pat} {dtype} {name}: err {err:.3e} (scale {gs:.3f})")
+        assert err <= TOL_GRAD[dtype] * gs, (name, err, gs)

@@ -74,10 +74,12 @@ def test_largest_grid_sampled_rows():
     check(pat, q, k, v, 128, 64, 0.125, "bf16", rows=rows)
 
 
-@pytest.mark.parametrize("pat,tm,d", [(Pat("hilbert_slide", 16, 16, 300), 128, 64),
-                                      (Pat("hilbert_slide", 16, 16, 100), 64, 64),
-                                      (Pat("rowmajor_slide", 16, 16, 7, 7), 128, 32)], ids=str)
-def test_growing_scores_take_the_max_path(pat, tm, d):
+@pytest.mark.parametrize("pat,tm,d,dtype", [(Pat("hilbert_slide", 16, 16, 300), 128, 64, "bf16"),
+                                            (Pat("hilbert_slide", 16, 16, 100), 64, 64, "bf16"),
+                                            (Pat("rowmajor_slide", 16, 16, 7, 7), 128, 32, "bf16"),
+                                            (Pat("hilbert_slide", 16, 16, 300), 64, 32, "f32"),
+                                            (Pat("rowmajor_slide", 16, 16, 7, 7), 64, 64, "f32")], ids=str)
+def test_growing_scores_take_the_max_path(pat, tm, d, dtype):
     """Scores that jump by more than 2^32 in weight from one key tile to the next:
     the tile taken against the stale softmax reference fails its row-sum check and
     is recomputed on the max path, rescaling O and l (for the even rows only: odd
@@ -91,8 +93,8 @@ def test_growing_scores_take_the_max_path(pat, tm, d):
     sign = torch.where(torch.arange(N) % 2 == 0, 1.0, -1.0)
     q = 0.5 * sign[None, None, :, None].expand(1, 2, N, d).clone()
     v = torch.randn((1, 2, N, d), generator=g)
-    q, k, v = (t.to(torch.bfloat16) for t in (q, k, v))
-    out, lse = check(pat, q, k, v, tm, 64, 0.125, "bf16", gather=False)
+    q, k, v = (t.to(torch.bfloat16 if dtype == "bf16" else torch.float32) for t in (q, k, v))
+    out, lse = check(pat, q, k, v, tm, 64, 0.125, dtype, gather=False)
     mask = hla.build_block_mask(pat, tm, 64)
     qd, kd, vd = (t.to(DEV) for t in (q, k, v))
     # the same tiles through the reordering mode: a random order, bit for bit
@@ -111,7 +113,7 @@ def test_growing_scores_take_the_max_path(pat, tm, d):
     out_b, lse_b = hla.attn_fwd_rpb(qd, kd, vd, ident, table, mask, 0.125)
     torch.cuda.synchronize()
     ref_out, ref_lse = o_attn.attention(np64(q), np64(k), np64(v), pat, 0.125)
-    assert max_abs(np64(out_b.cpu()), ref_out) <= TOL_OUT["bf16"]
+    assert max_abs(np64(out_b.cpu()), ref_out) <= TOL_OUT[dtype]
     assert max_abs(np64(lse_b.cpu()), ref_lse) <= TOL_LSE
 
 

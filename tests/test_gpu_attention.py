@@ -117,6 +117,26 @@ def test_growing_scores_take_the_max_path(pat, tm, d, dtype):
     assert max_abs(np64(lse_b.cpu()), ref_lse) <= TOL_LSE
 
 
+@pytest.mark.parametrize("pat,dtype", [(Pat("hilbert_window", 16, 16, 64), "bf16"),
+                                       (Pat("hilbert_slide", 16, 16, 30), "bf16"),
+                                       (Pat("rowmajor_neighborhood", 16, 16, 5, 3), "f32")], ids=str)
+def test_vanishing_scale_averages_allowed_values(pat, dtype):
+    """A vanishing scale (1e-30; the API takes only positive ones): every allowed key
+    weighs the same, so out is the plain mean of the allowed v rows and lse =
+    ln(number of allowed keys), checked by the oracle and by those closed forms."""
+    d = 64 if dtype == "bf16" else 32
+    q, k, v = W.attn_inputs(1, 2, pat.N, d, dtype, 99)
+    out, lse = check(pat, q, k, v, 64, 64, 1e-30, dtype)
+    from oracle import masks
+    order = hla.hilbert_perm(pat.H, pat.W)[0].cpu().numpy() if pat.hilbert else np.arange(pat.N)
+    pos = np.arange(pat.N)
+    allow = masks.allowed(pat, pos[:, None], pos[None, :])
+    vs = np64(v)[:, :, order]
+    mean = np.einsum("ij,bhjd->bhid", allow / allow.sum(1, keepdims=True), vs)
+    assert max_abs(np64(out), mean) <= TOL_OUT[dtype]
+    assert max_abs(np64(lse), np.broadcast_to(np.log(allow.sum(1)), lse.shape)) <= TOL_LSE
+
+
 def random_cases(n):
     rng = np.random.default_rng(77)
     kinds = list(hla.PATTERN_IDS)

@@ -9,11 +9,18 @@
 //
 // MFMA D = A B with A = a tile of W (features x k), B = the input rows (k x
 // tokens), v_mfma_f32_32x32x16_bf16, fp32 accumulation. A workgroup of four
-// waves handles 128 tokens x FT features; the FT x K weight tile sits in LDS
-// (padded rows) and is shared by the four waves, each wave streams the K-slices
-// of its own 32 tokens straight from global memory (16 contiguous bytes per
-// lane per step). The accumulator lane layout gives each lane one token and
-// runs of four consecutive features, stored as 8-byte bf16 writes.
+// waves handles FT features of a group of blocks of 128 tokens: the FT x K weight
+// tile sits in LDS (padded rows) for all of them, and each wave streams the
+// K-slices of its own 32 tokens of a block straight from global memory (16
+// contiguous bytes per lane per step). The accumulator lane layout gives each
+// lane one token and runs of four consecutive features, stored as 8-byte bf16
+// writes.
+//
+// Grid. A 1-D grid in which the workgroups of one token group (all its feature
+// tiles) get the same blockIdx.x % 8, i.e. the same XCD (workgroups are dealt
+// round-robin to the 8 XCDs), and neighbouring ids, so the input rows that every
+// feature tile reads come from that XCD's L2 after the first read instead of
+// from HBM once per feature tile.
 #include "hla_internal.h"
 
 namespace hla {
@@ -25,12 +32,14 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kWaves = 4;
 constexpr int kTokens = 32 * kWaves;
+constexpr int kXcds = 8;
 
 struct ProjArgs {
   const __bf16 *in;   // x [T, K] (QKV) or o [B, heads, N, d] (out)
   const __bf16 *w;    // [F, K]
   __bf16 *out0, *out1, *out2;  // q, k, v (QKV) or y (out, out0 only)
   int32_t T, N, K, F, heads, d, C;
+  int32_t n_ftiles, group, n_groups;  // feature tiles; token blocks per group; groups
 };
 
 // MODE 0: QKV (head split on output). MODE 1: out projection (head merge on input).
@@ -41,7 +50,14 @@ __global__ void __launch_bounds__(64 * kWaves) proj_kernel(ProjArgs p) {
   const int WS = p.K + 8;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int col = lane & 31, half = lane >> 5;
-  const int fbase = blockIdx.y * FT;
+  // (token group, feature tile) of this workgroup: id L = 8 s + x goes to XCD x;
+  // its s-th slot there is feature tile s % n_ftiles of token group
+  // (s / n_ftiles) * 8 + x. The grid covers a multiple of 8 token groups, the
+  // surplus ones return here.
+  const int xcd = blockIdx.x % kXcds, s = blockIdx.x / kXcds;
+  const int group = (s / p.n_ftiles) * kXcds + xcd;
+  if (group >= p.n_groups) return;
+  const int fbase = (s % p.n_ftiles) * FT;
 
   // weight tile -> LDS
   const int cpr = p.K / 8;
@@ -52,7 +68,9 @@ __global__ void __launch_bounds__(64 * kWaves) proj_kernel(ProjArgs p) {
   }
   __syncthreads();
 
-  const int t = blockIdx.x * kTokens + wave * 32 + col;
+  for (int blk = group * p.group; blk < group * p.group + p.group; ++blk) {
+  const int t = blk * kTokens + wave * 32 + col;
+  if (blk * kTokens >= p.T) break;
   const bool valid = t < p.T;
   const int tt = valid ? t : 0;
   const int b = tt / p.N, n = tt - b * p.N;
@@ -86,7 +104,7 @@ __global__ void __launch_bounds__(64 * kWaves) proj_kernel(ProjArgs p) {
     }
   }
 
-  if (!valid) return;
+  if (!valid) continue;
 #pragma unroll
   for (int f = 0; f < FB; ++f) {
 #pragma unroll
@@ -107,11 +125,12 @@ __global__ void __launch_bounds__(64 * kWaves) proj_kernel(ProjArgs p) {
       *reinterpret_cast<bf16x4 *>(dst) = o4;
     }
   }
+  }
 }
 
 template <int MODE>
-hipError_t launch_fb(const ProjArgs &p, hipStream_t s) {
-  const uint32_t gx = (uint32_t)((p.T + kTokens - 1) / kTokens);
+hipError_t launch_fb(ProjArgs p, hipStream_t s) {
+  const int64_t blocks = (p.T + kTokens - 1) / kTokens;
   // widest feature tile whose weight slice fits the 64 KiB of LDS a workgroup
   // gets without opting in to more
   int fb = 1;
@@ -121,20 +140,36 @@ hipError_t launch_fb(const ProjArgs &p, hipStream_t s) {
       break;
     }
   }
-  const uint32_t gy = (uint32_t)(p.F / (32 * fb));
+  p.n_ftiles = p.F / (32 * fb);
+  // token blocks per workgroup (sharing one weight tile): the most of 4, 2, 1
+  // that still gives three workgroups per CU
+  int cus = 0, dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    cus = 256;
+  p.group = 1;
+  for (int g : {4, 2}) {
+    if ((blocks + g - 1) / g * p.n_ftiles >= 3 * (int64_t)cus) {
+      p.group = g;
+      break;
+    }
+  }
+  p.n_groups = (int32_t)((blocks + p.group - 1) / p.group);
+  const int64_t groups8 = (p.n_groups + kXcds - 1) / kXcds * kXcds;
+  const uint32_t gx = (uint32_t)(groups8 * p.n_ftiles);
   const size_t lds = (size_t)32 * fb * (p.K + 8) * 2;
   switch (fb) {
     case 6:
-      hipLaunchKernelGGL((proj_kernel<6, MODE>), dim3(gx, gy), dim3(64 * kWaves), lds, s, p);
+      hipLaunchKernelGGL((proj_kernel<6, MODE>), dim3(gx), dim3(64 * kWaves), lds, s, p);
       break;
     case 3:
-      hipLaunchKernelGGL((proj_kernel<3, MODE>), dim3(gx, gy), dim3(64 * kWaves), lds, s, p);
+      hipLaunchKernelGGL((proj_kernel<3, MODE>), dim3(gx), dim3(64 * kWaves), lds, s, p);
       break;
     case 2:
-      hipLaunchKernelGGL((proj_kernel<2, MODE>), dim3(gx, gy), dim3(64 * kWaves), lds, s, p);
+      hipLaunchKernelGGL((proj_kernel<2, MODE>), dim3(gx), dim3(64 * kWaves), lds, s, p);
       break;
     default:
-      hipLaunchKernelGGL((proj_kernel<1, MODE>), dim3(gx, gy), dim3(64 * kWaves), lds, s, p);
+      hipLaunchKernelGGL((proj_kernel<1, MODE>), dim3(gx), dim3(64 * kWaves), lds, s, p);
       break;
   }
   return hipGetLastError();

@@ -21,14 +21,10 @@
 // round-robin to the 8 XCDs), and neighbouring ids, so the input rows that every
 // feature tile reads come from that XCD's L2 after the first read instead of
 // from HBM once per feature tile.
-#include "hla_internal.h"
+#include "attn_common.h"
 
 namespace hla {
 namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kWaves = 4;
 constexpr int kTokens = 32 * kWaves;
@@ -128,8 +124,136 @@ __global__ void __launch_bounds__(64 * kWaves) proj_kernel(ProjArgs p) {
   }
 }
 
+// Rows-resident variant (K = 16 KC <= 192): one workgroup per block of 128
+// tokens holds its rows' K-slices in registers (read from HBM once) and walks
+// every feature tile, each tile's weights copied from L2 into one of two LDS
+// buffers with the 16-byte LDS DMA while the previous tile is multiplied. Per
+// tile j: issue tile j + 1's copies, then the stores of tile j - 1 (kept in
+// registers as bf16), then the products, then a wait that leaves exactly those
+// stores in flight (the vmcnt counter is in order, so the older copies must have
+// landed) and a barrier (every wave is done with tile j's buffer). Stores never
+// hold up a wait. A lane past the last token computes and stores row T - 1 again
+// (the same bytes to the same place), so every wave issues the same number of
+// stores per tile.
+template <int KC, int FB, int MODE>
+__global__ void __launch_bounds__(64 * kWaves, 2) proj_rows_kernel(ProjArgs p) {
+  constexpr int K = 16 * KC;
+  constexpr int FT = 32 * FB;
+  constexpr int WS = K + 8;                              // padded LDS row, elements
+  constexpr int TILE_BUF = (FT * WS * 2 + 1023) / 1024 * 1024;
+  constexpr int NCOPY = TILE_BUF / 1024;                 // 1 KiB copies per tile
+  __shared__ __attribute__((aligned(16))) char wl[2 * TILE_BUF];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int col = lane & 31, half = lane >> 5;
+
+  // Copy instruction i of a tile fills LDS bytes [1024 i, 1024 i + 1024) of its
+  // buffer, lane l the 16 bytes at o = 1024 i + 16 l: row o / (2 WS), element
+  // (o % (2 WS)) / 2. Row padding and the slots past the last row copy a chunk
+  // of the weights that nothing reads.
+  auto issue_w = [&](int j, int buf) {
+    const int fbase = j * FT;
+    for (int i = wave; i < NCOPY; i += kWaves) {
+      const int o = 1024 * i + 16 * lane;
+      int r = o / (2 * WS), e = (o - r * 2 * WS) / 2;
+      if (r >= FT) r = FT - 1;
+      if (e >= K) e = 0;
+      lds_dma16(p.w + (int64_t)(fbase + r) * K + e, lds_addr(wl + buf * TILE_BUF + 1024 * i));
+    }
+  };
+
+  const int t = blockIdx.x * kTokens + wave * 32 + col;
+  const int tt = t < p.T ? t : p.T - 1;
+  const int b = tt / p.N, n = tt - b * p.N;
+  const int ntiles = p.F / FT;
+  constexpr int NST = 4 * FB;   // stores per lane and tile (8 bytes each)
+
+  // The stores of tile j from its bf16 results (4 consecutive features each).
+  // QKV: a 32-feature block lies in one head of one of q, k, v (d % 32 == 0), so
+  // its base is wave-uniform and each lane adds a 32-bit element offset (the
+  // launcher checks that the outputs fit). Stores then share one uniform base
+  // instead of a 64-bit address per store.
+  auto store_tile = [&](int j, const bf16x4 (&o)[NST]) {
+#pragma unroll
+    for (int f = 0; f < FB; ++f) {
+      if (MODE == 0) {
+        const int f0 = j * FT + f * 32;
+        const int which = f0 / p.C, r0 = f0 - which * p.C;
+        const int h = r0 / p.d, e0 = r0 - h * p.d;
+        __bf16 *base = which == 0 ? p.out0 : (which == 1 ? p.out1 : p.out2);
+        const uint32_t row = (uint32_t)((b * p.heads + h) * p.N + n) * (uint32_t)p.d + (uint32_t)e0;
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          *reinterpret_cast<bf16x4 *>(base + (row + 8 * g + 4 * half)) = o[4 * f + g];
+      } else {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int feat = j * FT + f * 32 + 8 * g + 4 * half;
+          *reinterpret_cast<bf16x4 *>(p.out0 + (int64_t)tt * p.F + feat) = o[4 * f + g];
+        }
+      }
+    }
+  };
+
+  issue_w(0, 0);
+  bf16x8 xin[KC];
+#pragma unroll
+  for (int c = 0; c < KC; ++c) {
+    const int k = 16 * c + 8 * half;
+    const __bf16 *src;
+    if (MODE == 0) {
+      src = p.in + (int64_t)tt * K + k;
+    } else {
+      const int h = k / p.d, e = k - h * p.d;
+      src = p.in + ((int64_t)(b * p.heads + h) * p.N + n) * p.d + e;
+    }
+    xin[c] = *reinterpret_cast<const bf16x8 *>(src);
+  }
+  wait_vmem_all();
+  wait_then_barrier<0>();
+
+  bf16x4 pend[NST];
+  for (int j = 0; j < ntiles; ++j) {
+    if (j + 1 < ntiles) issue_w(j + 1, (j + 1) & 1);
+    if (j > 0) store_tile(j - 1, pend);
+    const __bf16 *wt = reinterpret_cast<const __bf16 *>(wl + (j & 1) * TILE_BUF);
+    f32x16 acc[FB];
+#pragma unroll
+    for (int f = 0; f < FB; ++f) acc[f] = f32x16{};
+#pragma unroll
+    for (int c = 0; c < KC; ++c)
+#pragma unroll
+      for (int f = 0; f < FB; ++f) {
+        const bf16x8 wop = *reinterpret_cast<const bf16x8 *>(wt + (f * 32 + col) * WS + 16 * c + 8 * half);
+        acc[f] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wop, xin[c], acc[f], 0, 0, 0);
+      }
+#pragma unroll
+    for (int f = 0; f < FB; ++f)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) pend[4 * f + g][q] = (__bf16)acc[f][4 * g + q];
+    if (j > 0) wait_then_barrier<NST>();
+    else wait_then_barrier<0>();
+  }
+  store_tile(ntiles - 1, pend);
+}
+
+template <int KC, int MODE>
+hipError_t launch_rows(const ProjArgs &p, hipStream_t s) {
+  const uint32_t gx = (uint32_t)((p.T + kTokens - 1) / kTokens);
+  hipLaunchKernelGGL((proj_rows_kernel<KC, 3, MODE>), dim3(gx), dim3(64 * kWaves), 0, s, p);
+  return hipGetLastError();
+}
+
 template <int MODE>
 hipError_t launch_fb(ProjArgs p, hipStream_t s) {
+  // rows-resident kernel where it applies: 96-feature tiles, K = 64, 128 or 192,
+  // heads of a multiple of 32 channels, outputs addressable with 32-bit offsets
+  if (p.F % 96 == 0 && p.d % 32 == 0 && (int64_t)p.T * p.F < ((int64_t)1 << 31)) {
+    if (p.K == 192) return launch_rows<12, MODE>(p, s);
+    if (p.K == 128) return launch_rows<8, MODE>(p, s);
+    if (p.K == 64) return launch_rows<4, MODE>(p, s);
+  }
   const int64_t blocks = (p.T + kTokens - 1) / kTokens;
   // widest feature tile whose weight slice fits the 64 KiB of LDS a workgroup
   // gets without opting in to more

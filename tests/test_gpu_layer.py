@@ -91,3 +91,17 @@ def test_projection_ragged_token_count():
     ref = (x.double() @ wq.double().T).reshape(B, N, 3, heads, d).permute(2, 0, 3, 1, 4)
     for got, r in zip((q, k, v), ref):
         assert max_abs(np64(got), r.numpy()) <= 2 ** -8 * float(r.abs().max()) + 1e-6
+
+
+def test_out_projection_ragged_token_count():
+    """The output projection with B*N not a multiple of 128 tokens, at widths that
+    take the rows-resident kernel (F a multiple of 96; K = 64 and 192)."""
+    for heads, d, F in ((2, 32, 192), (6, 32, 96)):
+        B, N = 3, 100
+        C = heads * d
+        g = torch.Generator().manual_seed(heads * 7 + F)
+        o = torch.randn((B, heads, N, d), generator=g).to(torch.bfloat16)
+        wp = (torch.randn((F, C), generator=g) * 0.1).to(torch.bfloat16)
+        y = hla.out_proj(o.cuda(), wp.cuda())
+        ref = o.double().permute(0, 2, 1, 3).reshape(B, N, C) @ wp.double().T
+        assert max_abs(np64(y), ref.numpy()) <= 2 ** -8 * float(ref.abs().max()) + 1e-6

@@ -95,8 +95,8 @@ def test_projection_ragged_token_count():
 
 def test_out_projection_ragged_token_count():
     """The output projection with B*N not a multiple of 128 tokens, at widths that
-    take the rows-resident kernel (F a multiple of 96; K = 64 and 192)."""
-    for heads, d, F in ((2, 32, 192), (6, 32, 96)):
+    take the rows-resident kernel (F = 192, a multiple of 96; K = 64 and 192)."""
+    for heads, d, F in ((2, 32, 192), (6, 32, 192)):
         B, N = 3, 100
         C = heads * d
         g = torch.Generator().manual_seed(heads * 7 + F)

@@ -260,8 +260,14 @@ class AttnPipeline:
 
 
 class LayerPipeline:
-    def __init__(self, w: W.LayerWorkload, hla):
+    """The layer step. fused (the default): the QKV projection reads x through the
+    Hilbert order and the output projection writes y through it
+    (hla_qkv_proj_perm, hla_out_proj_perm); otherwise separate gather and scatter
+    passes around hla_qkv_proj and hla_out_proj."""
+
+    def __init__(self, w: W.LayerWorkload, hla, fused: bool = True):
         self.w, self.hla = w, hla
+        self.fused = fused
         self.hilbert = True
         B, N, C, Hh, d = w.B, w.N, w.C, w.heads, w.d
         x, wq, wp = W.layer_inputs(w)
@@ -286,6 +292,16 @@ class LayerPipeline:
         hla, w, s, T = self.hla, self.w, self.sets[i % self.nsets], self.timer
         with T.stage("hilbert"):
             hla.hilbert_perm(w.H, w.W, out=(self.order, self.rank))
+        if self.fused:
+            with T.stage("qkv"):
+                hla.qkv_proj(s["x"], self.wq, w.heads, outs=(s["q"], s["k"], s["v"]), order=self.order)
+            with T.stage("mask"):
+                self.mask.build()
+            with T.stage("attn"):
+                hla.attn_fwd(s["q"], s["k"], s["v"], self.mask, w.scale, out=s["o"], with_lse=False)
+            with T.stage("proj"):
+                hla.out_proj(s["o"], self.wp, out=s["y"], order=self.order)
+            return
         with T.stage("gather"):
             hla.gather(s["x"], self.order, out=s["xh"])
         with T.stage("qkv"):
@@ -751,12 +767,14 @@ def main():
         "config": {"workload": w.name, "description": w.description,
                    "B": w.B, "heads": w.heads, "tokens": w.N, "head_dim": w.d,
                    "tile": [w.tile_m, w.tile_n], "parallelism": "single-gpu"},
-        "step": ("Hilbert index, tile lists, attention with the reordering fused in "
+        "step": ("Hilbert index, QKV projection with the gather fused in, tile lists, attention, "
+                 "output projection with the scatter fused in"
+                 if isinstance(w, W.LayerWorkload) else
+                 "Hilbert index, tile lists, attention with the reordering fused in "
                  "(hla_attn_fwd_perm)" if attn_kernel == "attn_fwd_perm" else
                  "Hilbert index, gather of q/k/v, tile lists, attention, scatter of out"
                  if getattr(getattr(w, "pattern", None), "hilbert", False) else
-                 "tile lists, attention" if isinstance(w, W.AttnWorkload) else
-                 "gather, QKV projection, tile lists, attention, output projection, scatter"),
+                 "tile lists, attention"),
         "attn_ms_per_call": res["attn_ms"],
         "attn_tflops_nonempty_tiles": res["attn_tile_tflops"],
         "attn_pct_bf16_peak": res["attn_pct_peak"],

@@ -313,6 +313,30 @@ hla_status hla_out_proj(const void *o, const void *w_proj, void *y, int64_t B,
                         int64_t N, int64_t heads, int64_t d, int64_t c_out,
                         hla_stream_t stream);
 
+/*
+ * The two projections with the token reordering fused in (the reshape step of
+ * Sec. 4.2 done inside the projections' loads and stores), for a layer whose
+ * features stay in grid (row-major) order while its attention runs in sequence
+ * order: order is hla_hilbert_perm's order (sequence position n of the grid is
+ * row order[n]).
+ *   hla_qkv_proj_perm: x [B, N, C] in grid order; q, k, v in sequence order:
+ *     q[b,h,n,:] = hla_qkv_proj's q for the input row x[b, order[n], :]
+ *     (likewise k, v), i.e. gather -> hla_qkv_proj in one pass.
+ *   hla_out_proj_perm: o in sequence order; y [B, N, C_out] in grid order:
+ *     y[b, order[n], :] = hla_out_proj's y[b, n, :], i.e. hla_out_proj ->
+ *     scatter in one pass.
+ * order: device int32[N], a permutation of 0 .. N-1 (entries in [0, N), not
+ * checked), 16-byte aligned, overlapping no output. The results equal the
+ * composed calls bit for bit. Other arguments, support and errors as
+ * hla_qkv_proj / hla_out_proj; a null order is INVALID_ARG.
+ */
+hla_status hla_qkv_proj_perm(const void *x, const void *w_qkv, const int32_t *order,
+                             void *q, void *k, void *v, int64_t B, int64_t N,
+                             int64_t heads, int64_t d, hla_stream_t stream);
+hla_status hla_out_proj_perm(const void *o, const void *w_proj, const int32_t *order,
+                             void *y, int64_t B, int64_t N, int64_t heads, int64_t d,
+                             int64_t c_out, hla_stream_t stream);
+
 /* Text of the last non-OK status returned on this thread ("" if none). */
 const char *hla_last_error(void);
 

@@ -51,7 +51,7 @@ HLA_F32, HLA_BF16 = 0, 1
 EXPORTED = ("hla_hilbert_perm", "hla_gather", "hla_scatter", "hla_block_mask_dims",
             "hla_build_block_mask", "hla_attn_fwd", "hla_attn_fwd_perm", "hla_attn_fwd_rpb",
             "hla_attn_bwd", "hla_attn_bwd_perm",
-            "hla_qkv_proj", "hla_out_proj",
+            "hla_qkv_proj", "hla_out_proj", "hla_qkv_proj_perm", "hla_out_proj_perm",
             "hla_last_error", "hla_version")
 
 
@@ -114,6 +114,8 @@ def lib() -> ctypes.CDLL:
                                   vp, vp, i64, i64, i64, i64, ctypes.c_int, f32, vp],
             "hla_qkv_proj": [vp, vp, vp, vp, vp, i64, i64, i64, i64, vp],
             "hla_out_proj": [vp, vp, vp, i64, i64, i64, i64, i64, vp],
+            "hla_qkv_proj_perm": [vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, vp],
+            "hla_out_proj_perm": [vp, vp, vp, vp, i64, i64, i64, i64, i64, vp],
         }
         for name, args in sigs.items():
             fn = getattr(L, name)
@@ -155,6 +157,14 @@ def _require(t: torch.Tensor, name: str):
         raise HLAError(HLA_ERR_INVALID_ARG, f"{name} must be on a GPU (got {t.device})")
     if not t.is_contiguous():
         raise HLAError(HLA_ERR_INVALID_ARG, f"{name} must be contiguous")
+
+
+def _require_order(order: torch.Tensor, n: int):
+    _require(order, "order")
+    if order.dtype != torch.int32:
+        raise HLAError(HLA_ERR_INVALID_ARG, "order must be int32")
+    if order.numel() != n:
+        raise HLAError(HLA_ERR_INVALID_ARG, f"order has {order.numel()} entries, expected {n}")
 
 
 def _pattern_desc(pattern) -> PatternDesc:
@@ -414,9 +424,12 @@ def attn_bwd_perm(q, k, v, out, dout, lse, order, mask: BlockMask, scale: Option
     return dq, dk, dv
 
 
-def qkv_proj(x: torch.Tensor, w_qkv: torch.Tensor, heads: int, outs=None):
+def qkv_proj(x: torch.Tensor, w_qkv: torch.Tensor, heads: int, outs=None,
+             order: Optional[torch.Tensor] = None):
     """x [B, N, C] -> q, k, v [B, heads, N, C/heads] (hla_qkv_proj).
-    ``outs`` = preallocated (q, k, v) to write into."""
+    ``outs`` = preallocated (q, k, v) to write into. With ``order`` (int32 [N], the
+    Hilbert order) x is in grid order and q, k, v come out in sequence order, the
+    gather fused in (hla_qkv_proj_perm)."""
     _require(x, "x")
     _require(w_qkv, "w_qkv")
     if x.dtype != torch.bfloat16 or w_qkv.dtype != torch.bfloat16:
@@ -426,13 +439,21 @@ def qkv_proj(x: torch.Tensor, w_qkv: torch.Tensor, heads: int, outs=None):
     if outs is None:
         outs = tuple(torch.empty((B, heads, N, d), dtype=x.dtype, device=x.device) for _ in range(3))
     q, k, v = outs
-    _check(lib().hla_qkv_proj(_ptr(x), _ptr(w_qkv), _ptr(q), _ptr(k), _ptr(v), B, N, heads, d,
-                              _stream(x)))
+    if order is None:
+        _check(lib().hla_qkv_proj(_ptr(x), _ptr(w_qkv), _ptr(q), _ptr(k), _ptr(v), B, N, heads, d,
+                                  _stream(x)))
+    else:
+        _require_order(order, N)
+        _check(lib().hla_qkv_proj_perm(_ptr(x), _ptr(w_qkv), _ptr(order), _ptr(q), _ptr(k), _ptr(v),
+                                       B, N, heads, d, _stream(x)))
     return q, k, v
 
 
-def out_proj(o: torch.Tensor, w_proj: torch.Tensor, out: Optional[torch.Tensor] = None):
-    """o [B, heads, N, d] -> y [B, N, C_out] (hla_out_proj)."""
+def out_proj(o: torch.Tensor, w_proj: torch.Tensor, out: Optional[torch.Tensor] = None,
+             order: Optional[torch.Tensor] = None):
+    """o [B, heads, N, d] -> y [B, N, C_out] (hla_out_proj). With ``order`` o is in
+    sequence order and y comes out in grid order, the scatter fused in
+    (hla_out_proj_perm)."""
     _require(o, "o")
     _require(w_proj, "w_proj")
     if o.dtype != torch.bfloat16 or w_proj.dtype != torch.bfloat16:
@@ -441,5 +462,10 @@ def out_proj(o: torch.Tensor, w_proj: torch.Tensor, out: Optional[torch.Tensor] 
     c_out = w_proj.shape[0]
     if out is None:
         out = torch.empty((B, N, c_out), dtype=o.dtype, device=o.device)
-    _check(lib().hla_out_proj(_ptr(o), _ptr(w_proj), _ptr(out), B, N, Hh, d, c_out, _stream(o)))
+    if order is None:
+        _check(lib().hla_out_proj(_ptr(o), _ptr(w_proj), _ptr(out), B, N, Hh, d, c_out, _stream(o)))
+    else:
+        _require_order(order, N)
+        _check(lib().hla_out_proj_perm(_ptr(o), _ptr(w_proj), _ptr(order), _ptr(out), B, N, Hh, d,
+                                       c_out, _stream(o)))
     return out

@@ -417,8 +417,9 @@ hla_status hla_attn_bwd_perm(const void *q, const void *k, const void *v, const 
                   scale, stream, "hla_attn_bwd_perm");
 }
 
-hla_status hla_qkv_proj(const void *x, const void *w_qkv, void *q, void *k, void *v, int64_t B,
-                        int64_t N, int64_t heads, int64_t d, hla_stream_t stream) {
+static hla_status qkv_proj(const void *x, const void *w_qkv, const int32_t *order, void *q,
+                           void *k, void *v, int64_t B, int64_t N, int64_t heads, int64_t d,
+                           hla_stream_t stream, const char *name) {
   hla_status st;
   if ((st = check_tensor_args(x, "x")) != HLA_OK) return st;
   if ((st = check_tensor_args(w_qkv, "w_qkv")) != HLA_OK) return st;
@@ -431,12 +432,13 @@ hla_status hla_qkv_proj(const void *x, const void *w_qkv, void *q, void *k, void
   if (C % 64 || C > 512) return fail(HLA_ERR_UNSUPPORTED, "C = heads*d = %lld must be a multiple of 64, <= 512", (long long)C);
   if (B * N * C > (1LL << 31) - 1 || B * N > (1LL << 31) - 256)
     return fail(HLA_ERR_UNSUPPORTED, "B * N * C exceeds 2^31");
-  return hip_status(hla::launch_qkv_proj(x, w_qkv, q, k, v, B, N, heads, d, (hipStream_t)stream),
-                    "hla_qkv_proj");
+  return hip_status(hla::launch_qkv_proj(x, w_qkv, order, q, k, v, B, N, heads, d, (hipStream_t)stream),
+                    name);
 }
 
-hla_status hla_out_proj(const void *o, const void *w_proj, void *y, int64_t B, int64_t N,
-                        int64_t heads, int64_t d, int64_t c_out, hla_stream_t stream) {
+static hla_status out_proj(const void *o, const void *w_proj, const int32_t *order, void *y,
+                           int64_t B, int64_t N, int64_t heads, int64_t d, int64_t c_out,
+                           hla_stream_t stream, const char *name) {
   hla_status st;
   if ((st = check_tensor_args(o, "o")) != HLA_OK) return st;
   if ((st = check_tensor_args(w_proj, "w_proj")) != HLA_OK) return st;
@@ -449,8 +451,34 @@ hla_status hla_out_proj(const void *o, const void *w_proj, void *y, int64_t B, i
   if (c_out % 64) return fail(HLA_ERR_UNSUPPORTED, "c_out = %lld must be a multiple of 64", (long long)c_out);
   if (B * N * (C > c_out ? C : c_out) > (1LL << 31) - 1 || B * N > (1LL << 31) - 256)
     return fail(HLA_ERR_UNSUPPORTED, "B * N * C exceeds 2^31");
-  return hip_status(hla::launch_out_proj(o, w_proj, y, B, N, heads, d, c_out, (hipStream_t)stream),
-                    "hla_out_proj");
+  return hip_status(hla::launch_out_proj(o, w_proj, order, y, B, N, heads, d, c_out, (hipStream_t)stream),
+                    name);
+}
+
+hla_status hla_qkv_proj(const void *x, const void *w_qkv, void *q, void *k, void *v, int64_t B,
+                        int64_t N, int64_t heads, int64_t d, hla_stream_t stream) {
+  return qkv_proj(x, w_qkv, nullptr, q, k, v, B, N, heads, d, stream, "hla_qkv_proj");
+}
+
+hla_status hla_qkv_proj_perm(const void *x, const void *w_qkv, const int32_t *order, void *q,
+                             void *k, void *v, int64_t B, int64_t N, int64_t heads, int64_t d,
+                             hla_stream_t stream) {
+  if (!order) return fail(HLA_ERR_INVALID_ARG, "order is null");
+  if (!aligned(order, 16)) return fail(HLA_ERR_INVALID_ARG, "order is not 16-byte aligned");
+  return qkv_proj(x, w_qkv, order, q, k, v, B, N, heads, d, stream, "hla_qkv_proj_perm");
+}
+
+hla_status hla_out_proj(const void *o, const void *w_proj, void *y, int64_t B, int64_t N,
+                        int64_t heads, int64_t d, int64_t c_out, hla_stream_t stream) {
+  return out_proj(o, w_proj, nullptr, y, B, N, heads, d, c_out, stream, "hla_out_proj");
+}
+
+hla_status hla_out_proj_perm(const void *o, const void *w_proj, const int32_t *order, void *y,
+                             int64_t B, int64_t N, int64_t heads, int64_t d, int64_t c_out,
+                             hla_stream_t stream) {
+  if (!order) return fail(HLA_ERR_INVALID_ARG, "order is null");
+  if (!aligned(order, 16)) return fail(HLA_ERR_INVALID_ARG, "order is not 16-byte aligned");
+  return out_proj(o, w_proj, order, y, B, N, heads, d, c_out, stream, "hla_out_proj_perm");
 }
 
 }  // extern "C"

@@ -128,11 +128,12 @@ hipError_t launch_attn_bwd_bf16(const AttnBwdArgs &a, int d, int tile_m, int til
 hipError_t launch_attn_bwd_f32(const AttnBwdArgs &a, int d, int tile_m, int tile_n,
                                hipStream_t s);
 
-hipError_t launch_qkv_proj(const void *x, const void *w, void *q, void *k, void *v,
-                           int64_t B, int64_t N, int64_t heads, int64_t d,
+// order: null, or the reordering fused in (QKV reads x row b*N + order[n],
+// the output projection writes y row b*N + order[n]).
+hipError_t launch_qkv_proj(const void *x, const void *w, const int32_t *order, void *q, void *k,
+                           void *v, int64_t B, int64_t N, int64_t heads, int64_t d,
                            hipStream_t s);
-hipError_t launch_out_proj(const void *o, const void *w, void *y, int64_t B,
-                           int64_t N, int64_t heads, int64_t d, int64_t c_out,
-                           hipStream_t s);
+hipError_t launch_out_proj(const void *o, const void *w, const int32_t *order, void *y, int64_t B,
+                           int64_t N, int64_t heads, int64_t d, int64_t c_out, hipStream_t s);
 
 }  // namespace hla

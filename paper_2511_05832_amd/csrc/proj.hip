@@ -32,6 +32,9 @@ constexpr int kXcds = 8;
 
 struct ProjArgs {
   const __bf16 *in;   // x [T, K] (QKV) or o [B, heads, N, d] (out)
+  // null, or the reordering fused in: QKV reads token n of batch b from input
+  // row b*N + order[n]; the output projection writes it to row b*N + order[n]
+  const int32_t *order;
   const __bf16 *w;    // [F, K]
   __bf16 *out0, *out1, *out2;  // q, k, v (QKV) or y (out, out0 only)
   int32_t T, N, K, F, heads, d, C;
@@ -82,7 +85,7 @@ __global__ void __launch_bounds__(64 * kWaves) proj_kernel(ProjArgs p) {
       const int k = k0 + 16 * c + 8 * half;
       const __bf16 *src;
       if (MODE == 0) {
-        src = p.in + (int64_t)tt * p.K + k;
+        src = p.in + (p.order ? (int64_t)b * p.N + p.order[n] : (int64_t)tt) * p.K + k;
       } else {
         const int h = k / p.d, e = k - h * p.d;
         src = p.in + ((int64_t)(b * p.heads + h) * p.N + n) * p.d + e;
@@ -116,7 +119,7 @@ __global__ void __launch_bounds__(64 * kWaves) proj_kernel(ProjArgs p) {
         __bf16 *base = which == 0 ? p.out0 : (which == 1 ? p.out1 : p.out2);
         dst = base + ((int64_t)(b * p.heads + h) * p.N + n) * p.d + e;
       } else {
-        dst = p.out0 + (int64_t)tt * p.F + feat;
+        dst = p.out0 + (p.order ? (int64_t)b * p.N + p.order[n] : (int64_t)tt) * p.F + feat;
       }
       *reinterpret_cast<bf16x4 *>(dst) = o4;
     }
@@ -185,10 +188,11 @@ __global__ void __launch_bounds__(64 * kWaves, 2) proj_rows_kernel(ProjArgs p) {
         for (int g = 0; g < 4; ++g)
           *reinterpret_cast<bf16x4 *>(base + (row + 8 * g + 4 * half)) = o[4 * f + g];
       } else {
+        const int64_t yrow = p.order ? (int64_t)b * p.N + p.order[n] : (int64_t)tt;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int feat = j * FT + f * 32 + 8 * g + 4 * half;
-          *reinterpret_cast<bf16x4 *>(p.out0 + (int64_t)tt * p.F + feat) = o[4 * f + g];
+          *reinterpret_cast<bf16x4 *>(p.out0 + yrow * p.F + feat) = o[4 * f + g];
         }
       }
     }
@@ -201,7 +205,7 @@ __global__ void __launch_bounds__(64 * kWaves, 2) proj_rows_kernel(ProjArgs p) {
     const int k = 16 * c + 8 * half;
     const __bf16 *src;
     if (MODE == 0) {
-      src = p.in + (int64_t)tt * K + k;
+      src = p.in + (p.order ? (int64_t)b * p.N + p.order[n] : (int64_t)tt) * K + k;
     } else {
       const int h = k / p.d, e = k - h * p.d;
       src = p.in + ((int64_t)(b * p.heads + h) * p.N + n) * p.d + e;
@@ -301,11 +305,12 @@ hipError_t launch_fb(ProjArgs p, hipStream_t s) {
 
 }  // namespace
 
-hipError_t launch_qkv_proj(const void *x, const void *w, void *q, void *k, void *v,
-                           int64_t B, int64_t N, int64_t heads, int64_t d,
+hipError_t launch_qkv_proj(const void *x, const void *w, const int32_t *order, void *q, void *k,
+                           void *v, int64_t B, int64_t N, int64_t heads, int64_t d,
                            hipStream_t s) {
   ProjArgs p;
   p.in = static_cast<const __bf16 *>(x);
+  p.order = order;
   p.w = static_cast<const __bf16 *>(w);
   p.out0 = static_cast<__bf16 *>(q);
   p.out1 = static_cast<__bf16 *>(k);
@@ -320,10 +325,11 @@ hipError_t launch_qkv_proj(const void *x, const void *w, void *q, void *k, void 
   return launch_fb<0>(p, s);
 }
 
-hipError_t launch_out_proj(const void *o, const void *w, void *y, int64_t B, int64_t N,
-                           int64_t heads, int64_t d, int64_t c_out, hipStream_t s) {
+hipError_t launch_out_proj(const void *o, const void *w, const int32_t *order, void *y, int64_t B,
+                           int64_t N, int64_t heads, int64_t d, int64_t c_out, hipStream_t s) {
   ProjArgs p;
   p.in = static_cast<const __bf16 *>(o);
+  p.order = order;
   p.w = static_cast<const __bf16 *>(w);
   p.out0 = static_cast<__bf16 *>(y);
   p.out1 = p.out2 = nullptr;

@@ -105,3 +105,42 @@ def test_out_projection_ragged_token_count():
         y = hla.out_proj(o.cuda(), wp.cuda())
         ref = o.double().permute(0, 2, 1, 3).reshape(B, N, C) @ wp.double().T
         assert max_abs(np64(y), ref.numpy()) <= 2 ** -8 * float(ref.abs().max()) + 1e-6
+
+
+@pytest.mark.parametrize("heads,d,B,N,c_out,kind", [(6, 32, 2, 4096, 192, "hilbert"),   # rows kernel
+                                                    (2, 32, 3, 100, 192, "random"),     # ragged tokens
+                                                    (4, 64, 2, 256, 128, "random")],    # other kernel
+                         ids=str)
+def test_projections_with_the_reordering_fused(heads, d, B, N, c_out, kind):
+    """hla_qkv_proj_perm equals gather -> hla_qkv_proj, and hla_out_proj_perm equals
+    hla_out_proj -> scatter, bit for bit."""
+    C = heads * d
+    g = torch.Generator().manual_seed(heads * 31 + N)
+    x = torch.randn((B, N, C), generator=g).to(torch.bfloat16).cuda()
+    wq = (torch.randn((3 * C, C), generator=g) * 0.05).to(torch.bfloat16).cuda()
+    wp = (torch.randn((c_out, C), generator=g) * 0.05).to(torch.bfloat16).cuda()
+    if kind == "hilbert":
+        side = int(round(N ** 0.5))
+        order = hla.hilbert_perm(side, side)[0]
+    else:
+        order = torch.randperm(N, generator=g).to(torch.int32).cuda()
+    q, k, v = hla.qkv_proj(x, wq, heads, order=order)
+    qc, kc, vc = hla.qkv_proj(hla.gather(x, order), wq, heads)
+    o = torch.randn((B, heads, N, d), generator=g).to(torch.bfloat16).cuda()
+    y = hla.out_proj(o, wp, order=order)
+    yc = hla.scatter(hla.out_proj(o, wp), order)
+    torch.cuda.synchronize()
+    for got, ref in ((q, qc), (k, kc), (v, vc), (y, yc)):
+        assert torch.equal(got, ref)
+
+
+def test_fused_projections_reject_a_null_order():
+    x = torch.zeros((1, 64, 64), dtype=torch.bfloat16, device="cuda")
+    w = torch.zeros((192, 64), dtype=torch.bfloat16, device="cuda")
+    q = torch.zeros((1, 2, 64, 32), dtype=torch.bfloat16, device="cuda")
+    lib = hla.lib()
+    st = lib.hla_qkv_proj_perm(hla._ptr(x), hla._ptr(w), None, hla._ptr(q), hla._ptr(q), hla._ptr(q),
+                               1, 64, 2, 32, None)
+    assert st == hla.HLA_ERR_INVALID_ARG
+    st = lib.hla_out_proj_perm(hla._ptr(q), hla._ptr(w), None, hla._ptr(x), 1, 64, 2, 32, 64, None)
+    assert st == hla.HLA_ERR_INVALID_ARG

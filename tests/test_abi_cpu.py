@@ -277,6 +277,22 @@ def test_proj_validation(L):
     assert L.hla_out_proj(x, w, vp(0x300008), 16, 4096, 6, 32, 192, None) == hla.HLA_ERR_INVALID_ARG
 
 
+def test_proj_perm_validation(L):
+    """The reordering variants: the plain projections' checks plus a null or
+    misaligned order, all rejected on the host before any GPU call."""
+    vp = ctypes.c_void_p
+    x, w, q, k, v = (vp(0x100000 * i) for i in range(1, 6))
+    order = vp(0x700000)
+    assert L.hla_qkv_proj_perm(x, w, order, q, k, v, 16, 4096, 6, 48, None) == hla.HLA_ERR_UNSUPPORTED
+    assert L.hla_qkv_proj_perm(x, w, None, q, k, v, 16, 4096, 6, 32, None) == hla.HLA_ERR_INVALID_ARG
+    assert L.hla_qkv_proj_perm(x, w, vp(0x700004), q, k, v, 16, 4096, 6, 32, None) == hla.HLA_ERR_INVALID_ARG
+    assert L.hla_qkv_proj_perm(None, w, order, q, k, v, 16, 4096, 6, 32, None) == hla.HLA_ERR_INVALID_ARG
+    assert L.hla_out_proj_perm(x, w, order, q, 16, 4096, 6, 32, 100, None) == hla.HLA_ERR_UNSUPPORTED
+    assert L.hla_out_proj_perm(x, w, None, q, 16, 4096, 6, 32, 192, None) == hla.HLA_ERR_INVALID_ARG
+    assert L.hla_out_proj_perm(x, w, vp(0x700008), q, 16, 4096, 6, 32, 192, None) == hla.HLA_ERR_INVALID_ARG
+    assert L.hla_out_proj_perm(x, w, order, q, 0, 4096, 6, 32, 192, None) == hla.HLA_ERR_INVALID_ARG
+
+
 def test_binding_fails_loudly_without_gpu_tensors():
     import torch
     x = torch.zeros(2, 4, 64, 64, dtype=torch.bfloat16)

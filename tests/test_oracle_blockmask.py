@@ -204,3 +204,39 @@ def test_shifted_window_masks_the_wrapped_pair():
     assert not m[0, 255] and not m[255, 0]
     assert m[8, 23] and not m[7, 8]
     assert m[:8, :8].all() and m[248:, 248:].all()
+
+
+def test_shifted_window_moves_each_window_forward():
+    """Sec. 3.2: the shifted windows are the plain windows moved forward along the
+    sequence by s. With w = 16 and s = 4 on 256 positions the windows are [0, 4),
+    [4, 20), [20, 36), ..., [244, 256). A shift that moved them the other way
+    (window id floor((i + s) / w), the same as this one only at s = w / 2) would
+    give [0, 12), [12, 28), ... instead, and fails every check below."""
+    m = masks.dense(Pat("hilbert_shifted_window", 16, 16, 16, 4))
+    assert m[:4, :4].all() and not m[3, 4] and not m[4, 3]
+    assert m[4:20, 4:20].all() and not m[19, 20] and not m[20, 19]
+    assert m[4, 11] and m[11, 12]                  # [0, 12) / [12, 28) would split these
+    assert m[244:, 244:].all() and not m[243, 244]
+    assert not m[0, 255] and not m[255, 0]
+    sizes = m.sum(axis=1)
+    assert (sizes[:4] == 4).all() and (sizes[4:244] == 16).all() and (sizes[244:] == 12).all()
+
+
+def _swin_shifted_mask(N, w, s):
+    """The shifted-window mask built the way the Swin Transformer builds it, on a 1-D
+    sequence (the construction Sec. 3.2 moves onto the Hilbert sequence): roll the
+    sequence back by s (rolled position t holds token (t + s) mod N), cut the rolled
+    sequence into windows of w, label the regions [0, N - w), [N - w, N - s),
+    [N - s, N) of the rolled sequence, and allow a pair when it shares a window and a
+    label (the label masks the pairs the roll joined across the sequence ends)."""
+    t = (np.arange(N) - s) % N                       # rolled position of each token
+    label = np.where(t < N - w, 0, np.where(t < N - s, 1, 2))
+    win = t // w
+    return (win[:, None] == win[None, :]) & (label[:, None] == label[None, :])
+
+
+@pytest.mark.parametrize("H,W,w,s", [(16, 16, 16, 4), (16, 16, 16, 13), (16, 16, 64, 5),
+                                     (8, 8, 8, 1), (16, 16, 16, 8), (32, 32, 64, 48)])
+def test_shifted_window_equals_the_swin_roll_construction(H, W, w, s):
+    m = masks.dense(Pat("hilbert_shifted_window", H, W, w, s))
+    assert np.array_equal(m, _swin_shifted_mask(H * W, w, s))

@@ -3,19 +3,23 @@ attention in float64 on the same seeded inputs.
 
 Bars: out max-abs <= 2e-2 for bf16 I/O (fp32 accumulation) and <= 1e-4 for fp32;
 log-sum-exp max-abs <= 1e-3. The measured workloads run in the launch
-configuration the bench times; the largest ones are checked on sampled query rows
-the oracle computes one by one (tile edges, both sequence ends, random rows).
+configuration the bench times; the largest ones are checked on one whole (b, h)
+slice, every row, and on sampled query rows of every slice (tile edges, both
+sequence ends, random rows).
 """
 import numpy as np
 import pytest
 import torch
 
+import oracle_pool
 import paper_2511_05832_amd as hla
 import workloads as W
 from conftest import Pat
 from helpers import (DEV, TOL_LSE, TOL_OUT, max_abs, np64, oracle_attention,
                      run_hip_attention, sample_rows)
 from oracle import attention as o_attn
+from oracle import hilbert as o_hil
+from oracle import permute as o_perm
 
 pytestmark = pytest.mark.gpu
 
@@ -44,6 +48,39 @@ def test_full_size_workloads_sampled_rows(w):
     q, k, v = W.workload_inputs(w)
     rows = sample_rows(w.N, w.tile_m, w.seed, n_random=96)
     check(w.pattern, q, k, v, w.tile_m, w.tile_n, w.scale, w.dtype, rows=rows)
+
+
+@pytest.mark.parametrize("w", [W.C3, W.C3_ROWMAJOR, W.C4, W.C4_ROWMAJOR], ids=lambda w: w.name)
+def test_full_size_workloads_whole_slice(w):
+    """Every query row of one whole (b, h) slice - the last one, at the largest slice
+    offsets - of the full-size workload, launched as the measured step launches it
+    (all B x heads slices in one call). The oracle evaluates the slice's rows in
+    chunks across worker processes, each row over all N keys."""
+    q, k, v = W.workload_inputs(w)
+    out, lse, _ = run_hip_attention(w.pattern, q, k, v, w.tile_m, w.tile_n, w.scale)
+    b, h = w.B - 1, w.heads - 1
+    qn, kn, vn = (np64(t[b:b + 1, h:h + 1]) for t in (q, k, v))
+    if w.pattern.hilbert:
+        order = o_hil.hilbert_order(w.pattern.H, w.pattern.W)
+        qn, kn, vn = (o_perm.gather(a, order) for a in (qn, kn, vn))
+    ref_out, ref_lse = oracle_pool.attention_rows(qn, kn, vn, w.pattern, w.scale)
+    got_out, got_lse = np64(out[b:b + 1, h:h + 1]), np64(lse[b:b + 1, h:h + 1])
+    e_out, e_lse = max_abs(got_out, ref_out), max_abs(got_lse, ref_lse)
+    print(f"{w.name} slice (b={b}, h={h}), {w.N} rows: out err {e_out:.3e}, lse err {e_lse:.3e}")
+    assert e_out <= TOL_OUT[w.dtype], e_out
+    assert e_lse <= TOL_LSE, e_lse
+    assert np.isfinite(got_out).all()
+
+
+@pytest.mark.parametrize("pat,tm", [(Pat("hilbert_shifted_window", 32, 32, 16, 4), 64),
+                                    (Pat("hilbert_shifted_window", 64, 64, 256, 64), 128),
+                                    (Pat("hilbert_shifted_window", 64, 64, 256, 200), 128)], ids=str)
+def test_shifted_windows_with_an_unequal_shift(pat, tm):
+    """Shifted windows with s != w / 2, where the direction of the shift decides the
+    windows (each window moved forward along the Hilbert sequence by s, Sec. 3.2):
+    every row against the oracle."""
+    q, k, v = W.attn_inputs(2, 2, pat.N, 64, "bf16", 700 + pat.p1)
+    check(pat, q, k, v, tm, 64, 0.125, "bf16")
 
 
 # Feature maps of the paper whose side is not a power of two (Tables 1, 3, 6-8),

@@ -5,18 +5,23 @@ row-major formulation (which never reorders the tensors).
 Tolerance. The HIP path rounds q, k, v and the attention output to bf16 between
 stages (relative error <= 2^-9 each), and the softmax weights to bf16 inside the
 attention; the oracle keeps float64 throughout. With weights ~ N(0, 0.02^2) the
-layer output is small (std ~ 7e-3), so the absolute 2e-2 bar alone would say
-little: the test also bounds the error relative to the output's largest
-magnitude, at 2e-2 (four bf16 roundings in sequence, with margin).
+layer output is small (std ~ 7e-3, max ~ 4e-2), so the absolute 2e-2 bar alone
+would say little: the test also bounds the error relative to the output's
+largest magnitude, at 1e-2. Four bf16 roundings in sequence (q/k/v, P, O, y)
+each add at most 2^-9 relative to the value rounded, so the accumulated error
+stays a few times 2^-9 ~ 2e-3 of max|y|.
 """
 import numpy as np
 import pytest
 import torch
 
+import oracle_pool
 import paper_2511_05832_amd as hla
 import workloads as W
 from helpers import max_abs, np64
 from oracle import layer as o_layer
+
+REL_BAR = 1e-2
 
 pytestmark = pytest.mark.gpu
 
@@ -34,24 +39,22 @@ def run_layer(w, x, wq, wp):
     return y.cpu()
 
 
-def check_layer(w, rows=None):
+def check_layer(w, pooled=False):
     x, wq, wp = W.layer_inputs(w)
     y = np64(run_layer(w, x, wq, wp))
-    ref = o_layer.hnt_layer(np64(x), np64(wq), np64(wp), w.H, w.W, w.heads, w.half_width,
-                            w.scale, rows=rows)
-    got = y if rows is None else y[:, rows]
-    err = max_abs(got, ref)
+    args = (np64(x), np64(wq), np64(wp), w.H, w.W, w.heads, w.half_width, w.scale)
+    ref = oracle_pool.layer(*args) if pooled else o_layer.hnt_layer(*args)
+    err = max_abs(y, ref)
     rel = err / float(np.abs(ref).max())
     print(f"{w.name}: max-abs {err:.3e}, relative to max|ref| {rel:.3e}")
     assert err <= 2e-2
-    assert rel <= 2e-2
+    assert rel <= REL_BAR
     return y
 
 
-def test_layer_full_size_sampled_rows():
-    w = W.C5
-    rows = np.unique(np.concatenate([[0, 1, w.N - 1], np.random.default_rng(4).choice(w.N, 96, replace=False)]))
-    check_layer(w, rows)
+def test_layer_full_size_every_row():
+    """The whole 64 x 64 layer workload (16 x 4096 tokens x 192 features), every row."""
+    check_layer(W.C5, pooled=True)
 
 
 def test_layer_small_every_row():

@@ -14,7 +14,8 @@
  *    than HLA_OK nothing has been enqueued and no output has been written; the
  *    text of the error is available from hla_last_error() on the same thread.
  *  - Device pointers are plain device addresses owned by the caller. The library
- *    allocates and frees no device memory.
+ *    allocates and frees no device memory; its only device memory of its own is
+ *    the array of hla_attn_bwd_noalloc, part of its code object.
  *  - Work is enqueued on the caller's stream (NULL = the default stream) and the
  *    calls never synchronise, so they may be captured into a HIP graph.
  *  - Tensors are dense and contiguous, innermost dimension last:
@@ -27,8 +28,9 @@
  *    or inconsistent size. HLA_ERR_UNSUPPORTED: valid but outside what this
  *    build implements (listed per call). HLA_ERR_HIP: a HIP launch failed; the
  *    HIP error text is in hla_last_error().
- *  - Thread safety: re-entrant. The only global state is the per-thread error
- *    text. Calls that write the same buffers on different streams race.
+ *  - Thread safety: re-entrant. The global state is the per-thread error text
+ *    and hla_attn_bwd_noalloc's per-device array. Calls that write the same
+ *    buffers on different streams race.
  */
 #ifndef HLA_H
 #define HLA_H
@@ -288,6 +290,31 @@ hla_status hla_attn_bwd_perm(const void *q, const void *k, const void *v, const 
                              const hla_block_mask *mask, void *dq, void *dk, void *dv,
                              float *stats, int64_t B, int64_t heads, int64_t N, int64_t d,
                              hla_dtype dtype, float scale, hla_stream_t stream);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): hla_attn_bwd without
+ * the stats workspace. The row statistics go instead to an array this library
+ * holds on every device it runs on: 8 MiB (two floats for each of 2^20 rows),
+ * held from the library's load on that device until the process ends. So
+ * B * heads * N must be at most 1048576; a larger call returns
+ * HLA_ERR_UNSUPPORTED (hla_attn_bwd takes any size).
+ * The call allocates and frees nothing. It runs on the current device; stream,
+ * if not NULL, must belong to it (else HLA_ERR_INVALID_ARG). Its first call on
+ * a device looks the array's address up once (hipGetSymbolAddress).
+ * Every call on one device shares that device's array, which keeps the last
+ * call's contents. Calls in one stream's order are safe. Calls whose work
+ * overlaps in time on one device (on different streams, or from several
+ * threads) race on the array and give wrong gradients; serialise them. The
+ * array needs no clearing: each call's first kernel writes the statistics of
+ * every row before its second kernel reads them.
+ * Results equal hla_attn_bwd's bit for bit. Other arguments, support and errors
+ * as hla_attn_bwd.
+ */
+hla_status hla_attn_bwd_noalloc(const void *q, const void *k, const void *v, const void *out,
+                                const void *dout, const float *lse, const hla_block_mask *mask,
+                                void *dq, void *dk, void *dv, int64_t B, int64_t heads, int64_t N,
+                                int64_t d, hla_dtype dtype, float scale, hla_stream_t stream);
 
 /*
  * QKV projection with head split (Sec. 4.2, input processing: the Linear layer

@@ -50,7 +50,7 @@ HLA_F32, HLA_BF16 = 0, 1
 
 EXPORTED = ("hla_hilbert_perm", "hla_gather", "hla_scatter", "hla_block_mask_dims",
             "hla_build_block_mask", "hla_attn_fwd", "hla_attn_fwd_perm", "hla_attn_fwd_rpb",
-            "hla_attn_bwd", "hla_attn_bwd_perm",
+            "hla_attn_bwd", "hla_attn_bwd_perm", "hla_attn_bwd_noalloc",
             "hla_qkv_proj", "hla_out_proj", "hla_qkv_proj_perm", "hla_out_proj_perm",
             "hla_last_error", "hla_version")
 
@@ -112,6 +112,8 @@ def lib() -> ctypes.CDLL:
                              vp, i64, i64, i64, i64, ctypes.c_int, f32, vp],
             "hla_attn_bwd_perm": [vp, vp, vp, vp, vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp,
                                   vp, vp, i64, i64, i64, i64, ctypes.c_int, f32, vp],
+            "hla_attn_bwd_noalloc": [vp, vp, vp, vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp,
+                                     vp, i64, i64, i64, i64, ctypes.c_int, f32, vp],
             "hla_qkv_proj": [vp, vp, vp, vp, vp, i64, i64, i64, i64, vp],
             "hla_out_proj": [vp, vp, vp, i64, i64, i64, i64, i64, vp],
             "hla_qkv_proj_perm": [vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, vp],
@@ -421,6 +423,30 @@ def attn_bwd_perm(q, k, v, out, dout, lse, order, mask: BlockMask, scale: Option
                                    _ptr(order), ctypes.byref(mask.struct), _ptr(dq), _ptr(dk),
                                    _ptr(dv), _ptr(stats), B, Hh, N, d, _dtype_code(q), scale,
                                    _stream(q)))
+    return dq, dk, dv
+
+
+def attn_bwd_noalloc(q, k, v, out, dout, lse, mask: BlockMask, scale: Optional[float] = None,
+                     dq: Optional[torch.Tensor] = None, dk: Optional[torch.Tensor] = None,
+                     dv: Optional[torch.Tensor] = None):
+    """hla_attn_bwd_noalloc: the backward with the row statistics in the library's own
+    per-device array (B * heads * N <= 2^20) instead of a workspace. The library
+    allocates nothing; pass dq, dk, dv to make the call allocate nothing here either.
+    Calls that overlap in time on one device race. Returns (dq, dk, dv)."""
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (out, "out"), (dout, "dout"), (lse, "lse")):
+        _require(t, n)
+    if q.dim() != 4 or any(t.shape != q.shape for t in (k, v, out, dout)):
+        raise HLAError(HLA_ERR_INVALID_ARG, "q, k, v, out, dout must all be [B, heads, N, d] of one shape")
+    B, Hh, N, d = q.shape
+    scale = 1.0 / float(d) ** 0.5 if scale is None else float(scale)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    for t, n in ((dq, "dq"), (dk, "dk"), (dv, "dv")):
+        _require(t, n)
+    _check(lib().hla_attn_bwd_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse),
+                                      ctypes.byref(mask.struct), _ptr(dq), _ptr(dk), _ptr(dv),
+                                      B, Hh, N, d, _dtype_code(q), scale, _stream(q)))
     return dq, dk, dv
 
 

@@ -4,9 +4,19 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "hla_internal.h"
+
+// Row statistics of the allocation-free backward (hla_attn_bwd_noalloc): two
+// floats per (b, h, row), up to kScratchRows rows. Every device the library
+// runs on holds its own copy for the life of the process. Host code never
+// passes this name to a kernel (on the host it is only a stand-in for the
+// symbol): it uses the address hipGetSymbolAddress returns for the current
+// device, kept in g_scratch_ptr.
+constexpr int64_t kScratchRows = 1LL << 20;
+static __device__ __align__(256) float scratch[2 * kScratchRows];
 
 namespace {
 
@@ -90,6 +100,38 @@ hla_status check_tensor_args(const void *a, const char *name) {
 bool overlaps(const void *a, int64_t na, const void *b, int64_t nb) {
   const char *x = static_cast<const char *>(a), *y = static_cast<const char *>(b);
   return x < y + nb && y < x + na;
+}
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float *g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept. The stream, if given, must
+// belong to the current device.
+hla_status scratch_on_current_device(hipStream_t stream, float **ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(HLA_ERR_UNSUPPORTED, "device %d beyond the %d this library tracks", dev, kMaxDevices);
+  if (stream) {
+    hipDevice_t sdev = -1;
+    e = hipStreamGetDevice(stream, &sdev);
+    if (e != hipSuccess) return hip_status(e, "hipStreamGetDevice");
+    if (sdev != dev)
+      return fail(HLA_ERR_INVALID_ARG, "stream belongs to device %d, the current device is %d", (int)sdev, dev);
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(HLA_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = static_cast<float *>(p);
+  }
+  *ptr = g_scratch_ptr[dev];
+  return HLA_OK;
 }
 
 }  // namespace
@@ -323,12 +365,16 @@ hla_status hla_attn_fwd_rpb(const void *q, const void *k, const void *v, const i
                   stream, "hla_attn_fwd_rpb");
 }
 
+// stats == nullptr: the row statistics go to the library's own `scratch` array
+// (hla_attn_bwd_noalloc); the public entry points with a stats argument reject
+// a null one before calling this.
 static hla_status attn_bwd(const void *q, const void *k, const void *v, const void *out,
                            const void *dout, const float *lse, const int32_t *order,
                            const hla_block_mask *mask, void *dq, void *dk, void *dv, float *stats,
                            int64_t B, int64_t heads, int64_t N, int64_t d, hla_dtype dtype,
                            float scale, hla_stream_t stream, const char *name) {
   hla_status st;
+  const bool own_stats = stats == nullptr;
   const void *ins[5] = {q, k, v, out, dout};
   const char *in_names[5] = {"q", "k", "v", "out", "dout"};
   for (int i = 0; i < 5; ++i)
@@ -338,12 +384,16 @@ static hla_status attn_bwd(const void *q, const void *k, const void *v, const vo
   for (int i = 0; i < 3; ++i)
     if ((st = check_tensor_args(outs[i], out_names[i])) != HLA_OK) return st;
   if ((st = check_tensor_args(lse, "lse")) != HLA_OK) return st;
-  if ((st = check_tensor_args(stats, "stats")) != HLA_OK) return st;
+  if (!own_stats && (st = check_tensor_args(stats, "stats")) != HLA_OK) return st;
   if ((st = check_attn(mask, B, heads, N, d, dtype, scale)) != HLA_OK) return st;
   if (!mask->n_full_t || !mask->full_idx_t || !mask->n_part_t || !mask->part_idx_t)
     return fail(HLA_ERR_INVALID_ARG, "the mask has no transposed lists (set them before building it)");
   const int64_t BH = B * heads;
   const int64_t bytes = BH * N * d * dtype_size(dtype);
+  if (own_stats && BH * N > kScratchRows)
+    return fail(HLA_ERR_UNSUPPORTED, "B * heads * N = %lld rows exceeds the %lld the library's "
+                "row-statistics array holds (use hla_attn_bwd with a stats workspace)",
+                (long long)(BH * N), (long long)kScratchRows);
   for (int i = 0; i < 3; ++i) {
     for (int j = 0; j < 5; ++j)
       if (overlaps(outs[i], bytes, ins[j], bytes))
@@ -351,19 +401,24 @@ static hla_status attn_bwd(const void *q, const void *k, const void *v, const vo
     for (int j = i + 1; j < 3; ++j)
       if (overlaps(outs[i], bytes, outs[j], bytes))
         return fail(HLA_ERR_INVALID_ARG, "%s overlaps %s", out_names[i], out_names[j]);
-    if (overlaps(outs[i], bytes, stats, BH * N * 8))
+    if (!own_stats && overlaps(outs[i], bytes, stats, BH * N * 8))
       return fail(HLA_ERR_INVALID_ARG, "%s overlaps stats", out_names[i]);
   }
-  for (int j = 0; j < 5; ++j)
-    if (overlaps(stats, BH * N * 8, ins[j], bytes))
-      return fail(HLA_ERR_INVALID_ARG, "stats overlaps %s", in_names[j]);
-  if (overlaps(stats, BH * N * 8, lse, BH * N * 4))
-    return fail(HLA_ERR_INVALID_ARG, "stats overlaps lse");
+  if (!own_stats) {
+    for (int j = 0; j < 5; ++j)
+      if (overlaps(stats, BH * N * 8, ins[j], bytes))
+        return fail(HLA_ERR_INVALID_ARG, "stats overlaps %s", in_names[j]);
+    if (overlaps(stats, BH * N * 8, lse, BH * N * 4))
+      return fail(HLA_ERR_INVALID_ARG, "stats overlaps lse");
+  }
   if (order) {
     for (int i = 0; i < 3; ++i)
       if (overlaps(order, N * 4, outs[i], bytes)) return fail(HLA_ERR_INVALID_ARG, "order overlaps %s", out_names[i]);
-    if (overlaps(order, N * 4, stats, BH * N * 8)) return fail(HLA_ERR_INVALID_ARG, "order overlaps stats");
+    if (!own_stats && overlaps(order, N * 4, stats, BH * N * 8))
+      return fail(HLA_ERR_INVALID_ARG, "order overlaps stats");
   }
+  // every argument is valid: only now look up the library's array (a HIP call)
+  if (own_stats && (st = scratch_on_current_device((hipStream_t)stream, &stats)) != HLA_OK) return st;
   hla::AttnBwdArgs a;
   a.q = q;
   a.k = k;
@@ -402,6 +457,7 @@ hla_status hla_attn_bwd(const void *q, const void *k, const void *v, const void 
                         const void *dout, const float *lse, const hla_block_mask *mask, void *dq,
                         void *dk, void *dv, float *stats, int64_t B, int64_t heads, int64_t N,
                         int64_t d, hla_dtype dtype, float scale, hla_stream_t stream) {
+  if (!stats) return fail(HLA_ERR_INVALID_ARG, "stats is NULL");
   return attn_bwd(q, k, v, out, dout, lse, nullptr, mask, dq, dk, dv, stats, B, heads, N, d, dtype,
                   scale, stream, "hla_attn_bwd");
 }
@@ -413,8 +469,17 @@ hla_status hla_attn_bwd_perm(const void *q, const void *k, const void *v, const 
                              hla_dtype dtype, float scale, hla_stream_t stream) {
   if (!order) return fail(HLA_ERR_INVALID_ARG, "order is NULL");
   if (!aligned(order, 16)) return fail(HLA_ERR_INVALID_ARG, "order is not 16-byte aligned");
+  if (!stats) return fail(HLA_ERR_INVALID_ARG, "stats is NULL");
   return attn_bwd(q, k, v, out, dout, lse, order, mask, dq, dk, dv, stats, B, heads, N, d, dtype,
                   scale, stream, "hla_attn_bwd_perm");
+}
+
+hla_status hla_attn_bwd_noalloc(const void *q, const void *k, const void *v, const void *out,
+                                const void *dout, const float *lse, const hla_block_mask *mask,
+                                void *dq, void *dk, void *dv, int64_t B, int64_t heads, int64_t N,
+                                int64_t d, hla_dtype dtype, float scale, hla_stream_t stream) {
+  return attn_bwd(q, k, v, out, dout, lse, nullptr, mask, dq, dk, dv, nullptr, B, heads, N, d,
+                  dtype, scale, stream, "hla_attn_bwd_noalloc");
 }
 
 static hla_status qkv_proj(const void *x, const void *w_qkv, const int32_t *order, void *q,

@@ -266,6 +266,34 @@ def test_attn_bwd_perm_validation(L):
     assert call(d=48) == hla.HLA_ERR_UNSUPPORTED
 
 
+def test_attn_bwd_noalloc_validation(L):
+    """The allocation-free backward checks what hla_attn_bwd checks (less the stats
+    workspace it does not take), and rejects more than 2^20 (b, h, row) rows, the
+    capacity of its own array; every call here is invalid, so nothing is launched
+    and no HIP call is made."""
+    vp = ctypes.c_void_p
+    N, d = 4096, 64
+    base = [vp(0x100000000 + i * 0x10000000) for i in range(9)]   # 256 MiB apart
+    q, k, v, o, g, lse, dq, dk, dv = base
+    m = fake_mask()
+
+    def call(mask, B=2, heads=4, **kw):
+        a = dict(q=q, dq=dq, dk=dk, d=d, scale=0.125)
+        a.update(kw)
+        return L.hla_attn_bwd_noalloc(a["q"], k, v, o, g, lse, ctypes.byref(mask), a["dq"], a["dk"],
+                                      dv, B, heads, N, a["d"], hla.HLA_BF16, a["scale"], None)
+
+    assert call(m) == hla.HLA_ERR_INVALID_ARG and "transposed" in L.hla_last_error().decode()
+    m.n_full_t = m.full_idx_t = m.n_part_t = m.part_idx_t = 0x60000
+    assert call(m, q=None) == hla.HLA_ERR_INVALID_ARG
+    assert call(m, d=48) == hla.HLA_ERR_UNSUPPORTED
+    assert call(m, scale=0.0) == hla.HLA_ERR_INVALID_ARG
+    assert call(m, dk=vp(dq.value + 64)) == hla.HLA_ERR_INVALID_ARG and "overlaps" in L.hla_last_error().decode()
+    # 2 x 129 x 4096 = 1056768 rows > 2^20 (each tensor 129 MiB, inside the spacing)
+    assert call(m, B=2, heads=129) == hla.HLA_ERR_UNSUPPORTED
+    assert "exceeds" in L.hla_last_error().decode()
+
+
 def test_proj_validation(L):
     vp = ctypes.c_void_p
     x, w, q, k, v = (vp(0x100000 * i) for i in range(1, 6))

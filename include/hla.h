@@ -156,8 +156,9 @@ hla_status hla_scatter(const void *src, void *dst, const int32_t *order,
                        hla_dtype dtype, hla_stream_t stream);
 
 /*
- * Host-only: tile-grid sizes for a pattern and tile, so the caller can size the
- * block-mask arrays: n_qtiles = ceil(N / tile_m), n_ktiles = ceil(N / tile_n),
+ * Host-only: tile-grid sizes of the block-sparse metadata (Sec. 3.1: the score
+ * matrix cut into b_q x b_k blocks, each full, partial or empty), so the caller
+ * can size the block-mask arrays: n_qtiles = ceil(N / tile_m), n_ktiles = ceil(N / tile_n),
  * N = H*W (any N; tiles may be ragged). Tile sizes are powers of two in
  * [16, 1024]. Pattern parameters must be >= 1
  * (slide radii and half-widths >= 0; neighbourhood kernels <= the grid extent).

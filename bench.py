@@ -27,6 +27,14 @@ dq, dk, dv; per-call time of hla_attn_bwd from an eager pass) and reported under
 tensors) under "backward_fused"; --no-backward skips both. The attention with the global relative
 position bias (hla_attn_fwd_rpb) is timed per call on the same inputs and
 reported under "rpb"; --no-rpb skips it.
+
+Every measured configuration (the 32x32 fp32 window, the 64x64 and 256x256
+bands, the 128x128 window, the row-major twins run through the same kernel, and
+the 64x64 layer) then gets a record under "configs": its step, its attention
+kernel alone (back-to-back launches) with TFLOP/s, % of its dtype's peak and a
+roofline record, and, for the Hilbert ones, the gather and scatter kernels with
+GB/s and the fraction of the 8 TB/s HBM peak. The Hilbert index is timed at
+128x128, 256x256 and 4096x4096 under "hilbert_index". --no-configs skips both.
 """
 from __future__ import annotations
 
@@ -96,6 +104,43 @@ class Timer:
 
     def count(self, name):
         return len(self.pairs.get(name, []))
+
+
+def b2b_ms(call, n):
+    """Average duration of call(i) for n back-to-back launches between one event pair
+    on the current stream (no event between launches); call(0) runs once before."""
+    call(0)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(n):
+        call(i + 1)
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / n
+
+
+def roofline_record(kernel, ms, nbytes, flops, dtype):
+    """The roofline of one kernel: HBM-bound when its algorithmic bytes take longer at
+    the HBM peak than its FLOPs at the compute peak of its dtype, else compute-bound."""
+    peak_tf = BF16_PEAK_TFLOPS if dtype == "bf16" else FP32_PEAK_TFLOPS
+    t = ms * 1e-3
+    rec = {"kernel": kernel, "kernel_ms_per_launch": ms, "algorithmic_bytes": nbytes,
+           "algorithmic_flops": flops}
+    if nbytes / (HBM_PEAK_GBS * 1e9) >= flops / (peak_tf * 1e12):
+        ach = nbytes / t / 1e9
+        rec.update(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s", frac=ach / HBM_PEAK_GBS,
+                   compute_frac=(flops / t / 1e12) / peak_tf if flops else 0.0)
+    else:
+        ach = flops / t / 1e12
+        rec.update(bound="mfma" if dtype == "bf16" else "fp32", achieved=ach, peak=peak_tf,
+                   unit="TFLOP/s", frac=ach / peak_tf, hbm_frac=nbytes / t / 1e9 / HBM_PEAK_GBS)
+    return rec
+
+
+def perm_record(kernel_ms, nbytes):
+    gbs = nbytes / (kernel_ms * 1e-3) / 1e9
+    return {"ms_per_call": kernel_ms, "gbs": gbs, "frac": gbs / HBM_PEAK_GBS, "bytes": nbytes}
 
 
 # ----------------------------------------------------------------------------
@@ -184,6 +229,16 @@ class AttnPipeline:
         end.record()
         torch.cuda.synchronize()
         return start.elapsed_time(end) / n
+
+    def perm_kernel_ms(self, n, scatter=False):
+        """Average duration of one gather (or scatter) of a [B, heads, N, d] tensor:
+        n back-to-back launches on rotating input sets between one event pair."""
+        hla = self.hla
+        if scatter:
+            return b2b_ms(lambda i: hla.scatter(self.sets[i % self.nsets]["oh"], self.order,
+                                                out=self.sets[i % self.nsets]["o"]), n)
+        return b2b_ms(lambda i: hla.gather(self.sets[i % self.nsets]["q"], self.order,
+                                           out=self.sets[i % self.nsets]["qh"]), n)
 
     # algorithmic figures -------------------------------------------------
     def tile_flops(self):
@@ -315,6 +370,26 @@ class LayerPipeline:
         with T.stage("scatter"):
             hla.scatter(s["yh"], self.order, out=s["y"])
 
+    def kernel_ms(self, which, n):
+        """Average duration of one stage's kernel alone (qkv, attn, proj, gather,
+        scatter), n back-to-back launches on rotating input sets; the projections
+        take the step's order (fused) or none."""
+        hla, w = self.hla, self.w
+        order = self.order if self.fused else None
+
+        def S(i):
+            return self.sets[i % self.nsets]
+        calls = {
+            "qkv": lambda i: hla.qkv_proj(S(i)["x"], self.wq, w.heads, outs=(S(i)["q"], S(i)["k"], S(i)["v"]),
+                                          order=order),
+            "attn": lambda i: hla.attn_fwd(S(i)["q"], S(i)["k"], S(i)["v"], self.mask, w.scale,
+                                           out=S(i)["o"], with_lse=False),
+            "proj": lambda i: hla.out_proj(S(i)["o"], self.wp, out=S(i)["y"], order=order),
+            "gather": lambda i: hla.gather(S(i)["x"], self.order, out=S(i)["xh"]),
+            "scatter": lambda i: hla.scatter(S(i)["yh"], self.order, out=S(i)["y"]),
+        }
+        return b2b_ms(calls[which], n)
+
     def tile_flops(self):
         tf, tp = self.mask.host_totals()
         w = self.w
@@ -323,6 +398,16 @@ class LayerPipeline:
     def attn_bytes(self):
         w = self.w
         return 4 * w.N * w.d * 2 * w.B * w.heads
+
+    def proj_figures(self, which):
+        """(algorithmic bytes, FLOPs) of one projection call: the activations read and
+        written once, the weights once, the order array once when fused."""
+        w = self.w
+        T, C = w.B * w.N, w.C
+        idx = 4 * w.N if self.fused else 0
+        if which == "qkv":
+            return 2 * (T * C + 3 * T * C + 3 * C * C) + idx, 2.0 * T * C * 3 * C
+        return 2 * (T * C + T * C + C * C) + idx, 2.0 * T * C * C
 
     def perm_bytes_per_tensor(self):
         w = self.w
@@ -537,6 +622,112 @@ def summarize(pipe, timing):
 
 
 # ----------------------------------------------------------------------------
+# one record per measured configuration
+
+
+def attn_config_record(w, hla, steps, warmup, fused_step=True):
+    """A configuration's numbers: its step (for Hilbert patterns the reordering fused
+    into the attention, else the plain attention), the attention kernel alone
+    (back-to-back launches) with its roofline, and the gather / scatter kernels of
+    the composed step with theirs."""
+    n = max(steps, 20)
+    rec = {"description": w.description, "pattern": w.pattern.kind, "B": w.B, "heads": w.heads,
+           "tokens": w.N, "head_dim": w.d, "dtype": w.dtype, "tile": [w.tile_m, w.tile_n]}
+    comp = make_pipeline(w, hla)
+    rc = summarize(comp, run_timed(comp, steps, warmup))
+    kms_c = comp.kernel_ms(n)
+    flops, tf, tp = comp.tile_flops()
+    nbytes = comp.attn_bytes()
+    rec["tiles"] = {"full": tf, "partial": tp}
+    rec["tile_flops"] = flops
+    if comp.hilbert:
+        pb = comp.perm_bytes_per_tensor()
+        rec["perm"] = {"gather": perm_record(comp.perm_kernel_ms(n), pb),
+                       "scatter": perm_record(comp.perm_kernel_ms(n, scatter=True), pb)}
+    rec["composed_step"] = {"ms_per_step": rc["ms_per_step"], "ms_per_step_eager": rc["ms_per_step_eager"],
+                            "attn_kernel_ms": kms_c, "value": flops / (rc["ms_per_step"] * 1e-3) / 1e12}
+    del comp
+    torch.cuda.empty_cache()
+    res, kms, kernel = rc, kms_c, "attn_fwd"
+    if w.pattern.hilbert and fused_step:
+        fp = make_pipeline(w, hla, fused=True)
+        res = summarize(fp, run_timed(fp, steps, warmup))
+        kms, kernel = fp.kernel_ms(n), "attn_fwd_perm"
+        del fp
+        torch.cuda.empty_cache()
+    peak = BF16_PEAK_TFLOPS if w.dtype == "bf16" else FP32_PEAK_TFLOPS
+    rec.update({
+        "step": ("Hilbert index, tile lists, attention with the reordering fused in"
+                 if kernel == "attn_fwd_perm" else "tile lists, attention"),
+        "ms_per_step": res["ms_per_step"], "ms_per_step_eager": res["ms_per_step_eager"],
+        "value": flops / (res["ms_per_step"] * 1e-3) / 1e12, "unit": "TFLOP/s",
+        "attn_ms_per_call": kms,
+        "attn_tflops_nonempty_tiles": flops / (kms * 1e-3) / 1e12,
+        "attn_pct_peak": 100.0 * flops / (kms * 1e-3) / 1e12 / peak,
+        "peak_tflops": peak,
+        "roofline": roofline_record(kernel, kms, nbytes, flops, w.dtype),
+        "stages_ms": res["stages_ms"],
+    })
+    return rec
+
+
+def layer_config_record(w, hla, steps, warmup):
+    """The layer: its step (reordering fused into the projections), each kernel alone
+    with its roofline, and the feature gather / scatter of the unfused step."""
+    n = max(steps, 20)
+    rec = {"description": w.description, "B": w.B, "heads": w.heads, "tokens": w.N,
+           "head_dim": w.d, "embed": w.C, "dtype": "bf16", "tile": [w.tile_m, w.tile_n],
+           "half_width": w.half_width}
+    un = LayerPipeline(w, hla, fused=False)
+    ru = summarize(un, run_timed(un, steps, warmup))
+    pb = un.perm_bytes_per_tensor()
+    rec["perm"] = {"gather": perm_record(un.kernel_ms("gather", n), pb),
+                   "scatter": perm_record(un.kernel_ms("scatter", n), pb)}
+    rec["unfused_step"] = {"ms_per_step": ru["ms_per_step"], "ms_per_step_eager": ru["ms_per_step_eager"]}
+    del un
+    torch.cuda.empty_cache()
+    lp = LayerPipeline(w, hla, fused=True)
+    res = summarize(lp, run_timed(lp, steps, warmup))
+    flops, tf, tp = lp.tile_flops()
+    kernels = {}
+    for which, name in (("qkv", "qkv_proj_perm"), ("attn", "attn_fwd"), ("proj", "out_proj_perm")):
+        ms = lp.kernel_ms(which, n)
+        if which == "attn":
+            nb, fl = lp.attn_bytes(), flops
+        else:
+            nb, fl = lp.proj_figures(which)
+        kernels[which] = roofline_record(name, ms, nb, fl, "bf16")
+    att = kernels["attn"]["kernel_ms_per_launch"]
+    rec.update({
+        "step": "Hilbert index, QKV projection with the gather fused in, tile lists, attention, "
+                "output projection with the scatter fused in",
+        "ms_per_step": res["ms_per_step"], "ms_per_step_eager": res["ms_per_step_eager"],
+        "value": flops / (res["ms_per_step"] * 1e-3) / 1e12, "unit": "TFLOP/s",
+        "tiles": {"full": tf, "partial": tp}, "tile_flops": flops,
+        "attn_ms_per_call": att,
+        "attn_tflops_nonempty_tiles": flops / (att * 1e-3) / 1e12,
+        "attn_pct_peak": 100.0 * flops / (att * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+        "roofline": max(kernels.values(), key=lambda r: r["kernel_ms_per_launch"]),
+        "kernels": kernels, "stages_ms": res["stages_ms"],
+    })
+    del lp
+    torch.cuda.empty_cache()
+    return rec
+
+
+def hilbert_index_record(hla, side, n):
+    """hla_hilbert_perm on a side x side grid: order and rank (8 bytes per cell
+    written), n back-to-back launches."""
+    N = side * side
+    order = torch.empty(N, dtype=torch.int32, device="cuda")
+    rank = torch.empty(N, dtype=torch.int32, device="cuda")
+    ms = b2b_ms(lambda i: hla.hilbert_perm(side, side, out=(order, rank)), n)
+    gbs = 8 * N / (ms * 1e-3) / 1e9
+    return {"grid": [side, side], "tokens": N, "ms_per_call": ms, "bytes_written": 8 * N,
+            "gbs": gbs, "frac": gbs / HBM_PEAK_GBS}
+
+
+# ----------------------------------------------------------------------------
 # CPU baseline: the oracle on a bounded sample of the same step
 
 
@@ -575,10 +766,13 @@ def cpu_baseline(w: W.AttnWorkload, flops_per_step: float, budget_s: float = 12.
     o_bm.build(pat, w.tile_m, w.tile_n, rows_t)
     t_mask = (time.perf_counter() - t0) * nq / len(rows_t)
     # attention: calibrate the row sample on a pilot, then time the sample
+    # (the second pilot: the first one's time includes first-touch costs that the
+    # sample does not pay again)
     pilot = np.arange(0, w.N, max(1, w.N // 16))[:16]
-    t0 = time.perf_counter()
-    o_attn.attention(qh, kh, vh, pat, w.scale, rows=pilot)
-    per_row = (time.perf_counter() - t0) / len(pilot)
+    for _ in range(2):
+        t0 = time.perf_counter()
+        o_attn.attention(qh, kh, vh, pat, w.scale, rows=pilot)
+        per_row = (time.perf_counter() - t0) / len(pilot)
     n_rows = int(max(16, min(w.N, budget_s / max(per_row, 1e-9))))
     rows = np.linspace(0, w.N - 1, n_rows).astype(np.int64)
     t0 = time.perf_counter()
@@ -630,6 +824,10 @@ def main():
                          "reordering fused into the attention (hla_attn_fwd_perm) or separate "
                          "gather / attention / scatter calls; the other is reported beside it "
                          "(composed-only: skip the fused step)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-configuration records (every measured workload's step, "
+                         "attention kernel, gather / scatter kernels and rooflines) and the "
+                         "Hilbert index at 4096 x 4096")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="before the steps, time a plain device-to-device copy of this many MiB "
                          "(a kernel of known traffic, to calibrate HBM byte counters)")
@@ -716,6 +914,21 @@ def main():
             with open(args.all_out, "w") as f:
                 json.dump(allres, f, indent=1)
 
+    configs, hilbert_index = None, None
+    if not args.no_configs and not args.copy_mib:
+        configs = {}
+        for cw in (W.C1, W.C2, W.C3, W.C3_ROWMAJOR, W.C4, W.C4_ROWMAJOR, W.C5):
+            if isinstance(cw, W.LayerWorkload):
+                configs[cw.name] = layer_config_record(cw, hla, args.steps, args.warmup)
+            else:
+                configs[cw.name] = attn_config_record(cw, hla, args.steps, args.warmup)
+            print(f"[bench] config {cw.name}: {json.dumps(configs[cw.name])}", file=sys.stderr, flush=True)
+        # the index at the configurations' sizes is launch-bound; at 4096 x 4096
+        # (16.8 M cells, 128 MiB written) its GB/s means something
+        hilbert_index = {f"{sd}x{sd}": hilbert_index_record(hla, sd, max(args.steps, 20))
+                         for sd in (128, 256, 4096)}
+        print(f"[bench] hilbert index: {json.dumps(hilbert_index)}", file=sys.stderr, flush=True)
+
     flops = res["tile_flops"]
     # the dominant kernel's average duration: back-to-back launches between one
     # event pair where measured, else the eager pass's per-stage events
@@ -779,7 +992,8 @@ def main():
         "attn_tflops_nonempty_tiles": res["attn_tile_tflops"],
         "attn_pct_bf16_peak": res["attn_pct_peak"],
         "perm_gbs": {"gather": res_composed.get("gather_gbs"),
-                     "scatter": res_composed.get("scatter_gbs")},
+                     "scatter": res_composed.get("scatter_gbs"),
+                     "note": "eager step's stage events (three gathers, one scatter)"},
         "stages_ms": res["stages_ms"],
         "tiles": {"full": res["tiles_full"], "partial": res["tiles_partial"]},
         "roofline": roofline,
@@ -791,6 +1005,17 @@ def main():
             "ms_per_step": other["ms_per_step"], "ms_per_step_eager": other["ms_per_step_eager"],
             "value": flops / (other["ms_per_step"] * 1e-3) / 1e12,
             "attn_ms_per_call": other["attn_ms"], "stages_ms": other["stages_ms"]}
+    if configs and w.name in configs and "perm" in configs[w.name]:
+        pr = configs[w.name]["perm"]
+        line["perm_gbs"].update({
+            "gather_kernel": pr["gather"]["gbs"], "gather_frac": pr["gather"]["frac"],
+            "scatter_kernel": pr["scatter"]["gbs"], "scatter_frac": pr["scatter"]["frac"],
+            "kernel_note": "one [B, heads, N, d] tensor per launch, back-to-back launches; "
+                           "frac = achieved / 8 TB/s"})
+    if configs:
+        line["configs"] = configs
+    if hilbert_index:
+        line["hilbert_index"] = hilbert_index
     if bwd:
         line["backward"] = bwd
     if bwd_fused:

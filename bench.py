@@ -181,25 +181,23 @@ class AttnPipeline:
     def step(self, i):
         hla, w, s, T = self.hla, self.w, self.sets[i % self.nsets], self.timer
         if self.fused:
-            with T.stage("hilbert"):
-                hla.hilbert_perm(w.pattern.H, w.pattern.W, out=(self.order, self.rank))
-            with T.stage("mask"):
-                self.mask.build()
+            with T.stage("path_mask"):
+                self.mask.build_with_path(self.order, self.rank)
             with T.stage("attn"):
                 hla.attn_fwd_perm(s["q"], s["k"], s["v"], self.order, self.mask, w.scale,
                                   out=s["o"], lse=s["lse"])
             return
         if self.hilbert:
-            with T.stage("hilbert"):
-                hla.hilbert_perm(w.pattern.H, w.pattern.W, out=(self.order, self.rank))
+            with T.stage("path_mask"):
+                self.mask.build_with_path(self.order, self.rank)
             with T.stage("gather"):
                 for a, b in (("q", "qh"), ("k", "kh"), ("v", "vh")):
                     hla.gather(s[a], self.order, out=s[b])
             qn, kn, vn, on = "qh", "kh", "vh", "oh"
         else:
             qn, kn, vn, on = "q", "k", "v", "o"
-        with T.stage("mask"):
-            self.mask.build()
+            with T.stage("mask"):
+                self.mask.build()
         with T.stage("attn"):
             hla.attn_fwd(s[qn], s[kn], s[vn], self.mask, w.scale, out=s[on], lse=s["lse"])
         if self.hilbert:
@@ -345,13 +343,11 @@ class LayerPipeline:
 
     def step(self, i):
         hla, w, s, T = self.hla, self.w, self.sets[i % self.nsets], self.timer
-        with T.stage("hilbert"):
-            hla.hilbert_perm(w.H, w.W, out=(self.order, self.rank))
+        with T.stage("path_mask"):
+            self.mask.build_with_path(self.order, self.rank)
         if self.fused:
             with T.stage("qkv"):
                 hla.qkv_proj(s["x"], self.wq, w.heads, outs=(s["q"], s["k"], s["v"]), order=self.order)
-            with T.stage("mask"):
-                self.mask.build()
             with T.stage("attn"):
                 hla.attn_fwd(s["q"], s["k"], s["v"], self.mask, w.scale, out=s["o"], with_lse=False)
             with T.stage("proj"):
@@ -361,8 +357,6 @@ class LayerPipeline:
             hla.gather(s["x"], self.order, out=s["xh"])
         with T.stage("qkv"):
             hla.qkv_proj(s["xh"], self.wq, w.heads, outs=(s["q"], s["k"], s["v"]))
-        with T.stage("mask"):
-            self.mask.build()
         with T.stage("attn"):
             hla.attn_fwd(s["q"], s["k"], s["v"], self.mask, w.scale, out=s["o"], with_lse=False)
         with T.stage("proj"):
@@ -657,7 +651,7 @@ def attn_config_record(w, hla, steps, warmup, fused_step=True):
         torch.cuda.empty_cache()
     peak = BF16_PEAK_TFLOPS if w.dtype == "bf16" else FP32_PEAK_TFLOPS
     rec.update({
-        "step": ("Hilbert index, tile lists, attention with the reordering fused in"
+        "step": ("Hilbert index and tile lists (one launch), attention with the reordering fused in"
                  if kernel == "attn_fwd_perm" else "tile lists, attention"),
         "ms_per_step": res["ms_per_step"], "ms_per_step_eager": res["ms_per_step_eager"],
         "value": flops / (res["ms_per_step"] * 1e-3) / 1e12, "unit": "TFLOP/s",
@@ -699,8 +693,8 @@ def layer_config_record(w, hla, steps, warmup):
         kernels[which] = roofline_record(name, ms, nb, fl, "bf16")
     att = kernels["attn"]["kernel_ms_per_launch"]
     rec.update({
-        "step": "Hilbert index, QKV projection with the gather fused in, tile lists, attention, "
-                "output projection with the scatter fused in",
+        "step": "Hilbert index and tile lists (one launch), QKV projection with the gather fused in, "
+                "attention, output projection with the scatter fused in",
         "ms_per_step": res["ms_per_step"], "ms_per_step_eager": res["ms_per_step_eager"],
         "value": flops / (res["ms_per_step"] * 1e-3) / 1e12, "unit": "TFLOP/s",
         "tiles": {"full": tf, "partial": tp}, "tile_flops": flops,
@@ -980,12 +974,12 @@ def main():
         "config": {"workload": w.name, "description": w.description,
                    "B": w.B, "heads": w.heads, "tokens": w.N, "head_dim": w.d,
                    "tile": [w.tile_m, w.tile_n], "parallelism": "single-gpu"},
-        "step": ("Hilbert index, QKV projection with the gather fused in, tile lists, attention, "
-                 "output projection with the scatter fused in"
+        "step": ("Hilbert index and tile lists (one launch), QKV projection with the gather fused "
+                 "in, attention, output projection with the scatter fused in"
                  if isinstance(w, W.LayerWorkload) else
-                 "Hilbert index, tile lists, attention with the reordering fused in "
+                 "Hilbert index and tile lists (one launch), attention with the reordering fused in "
                  "(hla_attn_fwd_perm)" if attn_kernel == "attn_fwd_perm" else
-                 "Hilbert index, gather of q/k/v, tile lists, attention, scatter of out"
+                 "Hilbert index and tile lists (one launch), gather of q/k/v, attention, scatter of out"
                  if getattr(getattr(w, "pattern", None), "hilbert", False) else
                  "tile lists, attention"),
         "attn_ms_per_call": res["attn_ms"],

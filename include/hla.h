@@ -179,6 +179,22 @@ hla_status hla_block_mask_dims(const hla_pattern_desc *pat, int32_t tile_m,
 hla_status hla_build_block_mask(hla_block_mask *mask, hla_stream_t stream);
 
 /*
+ * hla_hilbert_perm and hla_build_block_mask in one call, for a step that builds
+ * both: the path P_(H,W) (Sec. 3.2) and the block metadata of a pattern on the
+ * same H x W grid (Sec. 3.1). On a 2^k x 2^k grid with k >= 2 the index and the
+ * row lists come from a single launch (one graph node instead of two; the
+ * transposed lists and the totals, if asked for, take their usual launches
+ * after it); on any other grid the two calls' launches run in sequence. The
+ * results equal hla_hilbert_perm followed by hla_build_block_mask bit for bit.
+ * order, rank: as for hla_hilbert_perm (either or both may be NULL), not
+ * overlapping any of the mask's arrays. mask: as for hla_build_block_mask, with
+ * mask->pat on the same grid (pat.H == H, pat.W == W; else INVALID_ARG). Both are
+ * validated before anything is enqueued; errors as the two calls'.
+ */
+hla_status hla_build_path_and_mask(int32_t H, int32_t W, int32_t *order, int32_t *rank,
+                                   hla_block_mask *mask, hla_stream_t stream);
+
+/*
  * Block-sparse attention forward (Sec. 3.1; Eq. 1's per-tile work). For every
  * (b, h) and query-tile row, walks only the listed key tiles: full tiles
  * without a mask, partial tiles with the element mask of mask->pat. Computes

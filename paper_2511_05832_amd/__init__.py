@@ -49,7 +49,7 @@ HLA_OK, HLA_ERR_INVALID_ARG, HLA_ERR_UNSUPPORTED, HLA_ERR_HIP = 0, 1, 2, 3
 HLA_F32, HLA_BF16 = 0, 1
 
 EXPORTED = ("hla_hilbert_perm", "hla_gather", "hla_scatter", "hla_block_mask_dims",
-            "hla_build_block_mask", "hla_attn_fwd", "hla_attn_fwd_perm", "hla_attn_fwd_rpb",
+            "hla_build_block_mask", "hla_build_path_and_mask", "hla_attn_fwd", "hla_attn_fwd_perm", "hla_attn_fwd_rpb",
             "hla_attn_bwd", "hla_attn_bwd_perm", "hla_attn_bwd_noalloc",
             "hla_qkv_proj", "hla_out_proj", "hla_qkv_proj_perm", "hla_out_proj_perm",
             "hla_last_error", "hla_version")
@@ -102,6 +102,7 @@ def lib() -> ctypes.CDLL:
             "hla_scatter": [vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp],
             "hla_block_mask_dims": [ctypes.POINTER(PatternDesc), i32, i32, _i32p, _i32p],
             "hla_build_block_mask": [ctypes.POINTER(BlockMaskStruct), vp],
+            "hla_build_path_and_mask": [i32, i32, vp, vp, ctypes.POINTER(BlockMaskStruct), vp],
             "hla_attn_fwd": [vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp,
                              i64, i64, i64, i64, ctypes.c_int, f32, vp],
             "hla_attn_fwd_perm": [vp, vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp,
@@ -280,6 +281,22 @@ class BlockMask:
 
     def build(self):
         _check(lib().hla_build_block_mask(ctypes.byref(self.struct), _stream(self.n_full)))
+        return self
+
+    def build_with_path(self, order: Optional[torch.Tensor] = None,
+                        rank: Optional[torch.Tensor] = None):
+        """Build the lists and the Hilbert index of the pattern's grid together
+        (hla_build_path_and_mask: one launch on 2^k x 2^k grids). order, rank:
+        int32 [H*W] outputs, either may be None."""
+        n = self.struct.pat.H * self.struct.pat.W
+        for t, name in ((order, "order"), (rank, "rank")):
+            if t is not None:
+                _require(t, name)
+                if t.dtype != torch.int32 or t.numel() != n:
+                    raise HLAError(HLA_ERR_INVALID_ARG, f"{name} must be int32 with H*W entries")
+        _check(lib().hla_build_path_and_mask(int(self.struct.pat.H), int(self.struct.pat.W),
+                                             _ptr(order), _ptr(rank), ctypes.byref(self.struct),
+                                             _stream(self.n_full)))
         return self
 
     @property

@@ -21,7 +21,7 @@
 // then pads the rest of both lists with -1. A line is a query-tile row (the
 // forward pass and the query gradients walk these) or, for the optional
 // transposed lists, a key-tile column (the key and value gradients walk these).
-#include "hla_internal.h"
+#include "hilbert_common.h"
 
 namespace hla {
 namespace {
@@ -132,11 +132,22 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
 
 // COLS = false: line = query-tile row q, entries = key tiles.
 // COLS = true:  line = key-tile column k, entries = query tiles.
-template <bool COLS>
+// PATH: the grid carries `path.blocks` more workgroups after the lines, which
+// compute the Hilbert index of the same launch (hla_build_path_and_mask): the two
+// jobs are independent, and one launch is one graph node instead of two.
+template <bool COLS, bool PATH>
 __global__ void __launch_bounds__(kThreads)
     classify_lines(PatternArgs p, int32_t tile_m, int32_t tile_n, int32_t n_entries,
                    int32_t *__restrict__ n_full, int32_t *__restrict__ full_idx,
-                   int32_t *__restrict__ n_part, int32_t *__restrict__ part_idx) {
+                   int32_t *__restrict__ n_part, int32_t *__restrict__ part_idx,
+                   HilbertJob path) {
+  if constexpr (PATH) {
+    const int32_t b = (int32_t)blockIdx.x - ((int32_t)gridDim.x - path.blocks);
+    if (b >= 0) {   // uniform over the workgroup: it leaves before any barrier
+      hilbert4_block(path, b, (int32_t)threadIdx.x);
+      return;
+    }
+  }
   __shared__ int32_t wave_f[kWaves], wave_p[kWaves];
   const int line = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -219,15 +230,23 @@ __global__ void __launch_bounds__(kThreads)
 
 hipError_t launch_block_mask(const PatternArgs &pat, int32_t tile_m, int32_t tile_n,
                              int32_t n_qtiles, int32_t n_ktiles, const BlockLists &rows,
-                             const BlockLists *cols, int32_t *totals, hipStream_t s) {
-  hipLaunchKernelGGL(classify_lines<false>, dim3(n_qtiles), dim3(kThreads), 0, s, pat, tile_m,
-                     tile_n, n_ktiles, rows.n_full, rows.full_idx, rows.n_part, rows.part_idx);
+                             const BlockLists *cols, int32_t *totals, hipStream_t s,
+                             const HilbertJob *path) {
+  if (path && path->blocks > 0) {
+    hipLaunchKernelGGL((classify_lines<false, true>), dim3(n_qtiles + path->blocks), dim3(kThreads),
+                       0, s, pat, tile_m, tile_n, n_ktiles, rows.n_full, rows.full_idx, rows.n_part,
+                       rows.part_idx, *path);
+  } else {
+    hipLaunchKernelGGL((classify_lines<false, false>), dim3(n_qtiles), dim3(kThreads), 0, s, pat,
+                       tile_m, tile_n, n_ktiles, rows.n_full, rows.full_idx, rows.n_part,
+                       rows.part_idx, HilbertJob{});
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (cols) {
-    hipLaunchKernelGGL(classify_lines<true>, dim3(n_ktiles), dim3(kThreads), 0, s, pat, tile_m,
-                       tile_n, n_qtiles, cols->n_full, cols->full_idx, cols->n_part,
-                       cols->part_idx);
+    hipLaunchKernelGGL((classify_lines<true, false>), dim3(n_ktiles), dim3(kThreads), 0, s, pat,
+                       tile_m, tile_n, n_qtiles, cols->n_full, cols->full_idx, cols->n_part,
+                       cols->part_idx, HilbertJob{});
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -235,6 +254,16 @@ hipError_t launch_block_mask(const PatternArgs &pat, int32_t tile_m, int32_t til
   hipLaunchKernelGGL(sum_totals, dim3(1), dim3(kThreads), 0, s, rows.n_full, rows.n_part,
                      n_qtiles, totals);
   return hipGetLastError();
+}
+
+hipError_t launch_path_and_mask(int32_t side, int32_t *order, int32_t *rank,
+                                const PatternArgs &pat, int32_t tile_m, int32_t tile_n,
+                                int32_t n_qtiles, int32_t n_ktiles, const BlockLists &rows,
+                                const BlockLists *cols, int32_t *totals, hipStream_t s) {
+  int32_t lg = 0;
+  while ((1 << lg) < side) ++lg;
+  const HilbertJob job = make_hilbert_job(lg, order, rank);
+  return launch_block_mask(pat, tile_m, tile_n, n_qtiles, n_ktiles, rows, cols, totals, s, &job);
 }
 
 }  // namespace hla

@@ -2,85 +2,47 @@
 // Hilbert curve; the path depends only on (H, W) and is computed once and
 // cached).
 //
-// One launch, one thread per output element, both outputs written coalesced:
-//   hilbert_d2xy: thread d walks the curve index two bits per level, from the
-//                 finest quadrant up, and writes order[d] = y*W + x;
-//   hilbert_xy2d: thread t = y*W + x walks the cell's coordinate bits from the
-//                 coarsest level down and writes rank[t] = d.
+// One launch writes both outputs, coalesced:
+//   order[d] = y*W + x of the d-th cell on the curve,
+//   rank[t]  = the curve position of cell t = y*W + x.
 // Writing rank directly (instead of rank[order[d]] = d) keeps both passes
-// coalesced. Curve convention: starts at (0,0), first step to (0,1), ends at
-// (side-1, 0); at each level the lower-left quadrant is transposed and the
-// lower-right anti-transposed.
+// coalesced. Both directions walk the curve's levels from the coarsest down,
+// carrying the orientation of the current sub-square as two bits: sw (the axes
+// are swapped) and fl (both axes are reflected). Curve convention: starts at
+// (0,0), first step to (0,1), ends at (side-1, 0); the four quadrants are
+// visited lower-left, upper-left, upper-right, lower-right, and the sub-curves
+// of the lower-left and lower-right quadrants are the transposed and the
+// anti-transposed curve. In (sw, fl) those transforms are (1, 0) and (1, 1) and
+// composing them is an xor, so a level costs a few bit operations and no branch.
+// Four consecutive positions (or four cells of a row) share every level but the
+// last one (two), so each thread walks the shared levels once and writes four
+// results with one 16-byte store.
 //
-// Any other H x W grid (the paper also measures 56^2, 96^2, 160^2 and 128 x 256
-// grids without saying how its curve covers them): the path is the curve on the
-// smallest 2^k square holding the grid, with the cells outside the grid left out
-// in the curve's order. hilbert_grid is one thread per grid cell: the cell's
-// position d on the enclosing curve, then its rank = the number of grid cells
-// the curve visits before d, summed top-down over the curve's levels as the
-// areas of grid inside the earlier sibling quadrants - no scan and no scratch
-// memory. rank is written coalesced, order scattered (once per grid size).
-#include "hla_internal.h"
+#include "hilbert_common.h"
 
 namespace hla {
 namespace {
 
-__device__ __forceinline__ void hilbert_d2xy(int32_t side, int32_t d,
-                                             int32_t *__restrict__ order) {
-  uint32_t x = 0, y = 0, t = (uint32_t)d;
-  for (uint32_t s = 1; s < (uint32_t)side; s <<= 1) {
-    // quadrant at this level: 0 lower-left, 1 upper-left, 2 upper-right, 3 lower-right
-    const uint32_t qx = (t >> 1) & 1u;          // right half
-    const uint32_t qy = (t ^ qx) & 1u;          // upper half
-    if (!qy) {                                  // lower quadrants are reflected
-      if (qx) {
-        x = s - 1 - x;
-        y = s - 1 - y;
-      }
-      const uint32_t tmp = x;
-      x = y;
-      y = tmp;
-    }
-    x += s * qx;
-    y += s * qy;
-    t >>= 2;
-  }
-  order[d] = (int32_t)(y * (uint32_t)side + x);
+// side = 2^lg >= 4: every 256-thread workgroup is one block of the job.
+__global__ void __launch_bounds__(256) hilbert_square4(HilbertJob job) {
+  hilbert4_block(job, (int32_t)blockIdx.x, (int32_t)threadIdx.x);
 }
 
-__device__ __forceinline__ void hilbert_xy2d(int32_t side, int32_t id,
-                                             int32_t *__restrict__ rank) {
-  uint32_t x = (uint32_t)id % (uint32_t)side;
-  uint32_t y = (uint32_t)id / (uint32_t)side;
-  uint32_t d = 0;
-  for (uint32_t s = (uint32_t)side >> 1; s > 0; s >>= 1) {
-    const uint32_t qx = (x & s) ? 1u : 0u;
-    const uint32_t qy = (y & s) ? 1u : 0u;
-    d += s * s * ((3u * qx) ^ qy);
-    if (!qy) {  // undo the reflection of the lower quadrants (only low bits matter below)
-      if (qx) {
-        x = (s - 1) - (x & (s - 1));
-        y = (s - 1) - (y & (s - 1));
-      }
-      const uint32_t tmp = x;
-      x = y;
-      y = tmp;
-    }
+// Any side = 2^lg (the small squares, side < 4): one thread per entry.
+__global__ void __launch_bounds__(256) hilbert_square1(int32_t lg, int32_t n,
+                                                       int32_t *__restrict__ order,
+                                                       int32_t *__restrict__ rank) {
+  const int32_t i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  if (order) {
+    uint32_t x = 0, y = 0, sw = 0, fl = 0;
+    d2xy_levels((uint32_t)i, lg, 0, x, y, sw, fl);
+    order[i] = (int32_t)((y << lg) | x);
   }
-  rank[id] = (int32_t)d;
-}
-
-// One launch for both directions: the first `blocks_order` workgroups write order,
-// the rest write rank (either part may be absent).
-__global__ void __launch_bounds__(256) hilbert_square(int32_t side, int32_t n, int32_t blocks_order,
-                                                      int32_t *__restrict__ order,
-                                                      int32_t *__restrict__ rank) {
-  if ((int32_t)blockIdx.x < blocks_order) {
-    const int32_t d = blockIdx.x * 256 + threadIdx.x;
-    if (d < n) hilbert_d2xy(side, d, order);
-  } else {
-    const int32_t id = (blockIdx.x - blocks_order) * 256 + threadIdx.x;
-    if (id < n) hilbert_xy2d(side, id, rank);
+  if (rank) {
+    uint32_t d = 0, sw = 0, fl = 0;
+    xy2d_levels((uint32_t)i & ((1u << lg) - 1u), (uint32_t)i >> lg, lg, 0, d, sw, fl);
+    rank[i] = (int32_t)d;
   }
 }
 
@@ -99,24 +61,13 @@ __global__ void __launch_bounds__(256) hilbert_grid(int32_t H, int32_t W, int32_
   const int32_t t = blockIdx.x * 256 + threadIdx.x;
   if (t >= H * W) return;
   const int32_t cx = t % W, cy = t / W;
+  int32_t lg = 0;
+  while ((1 << lg) < side) ++lg;
   // position of (cx, cy) on the enclosing side x side curve
   uint32_t d = 0;
   {
-    uint32_t x = (uint32_t)cx, y = (uint32_t)cy;
-    for (uint32_t s = (uint32_t)side >> 1; s > 0; s >>= 1) {
-      const uint32_t qx = (x & s) ? 1u : 0u;
-      const uint32_t qy = (y & s) ? 1u : 0u;
-      d += s * s * ((3u * qx) ^ qy);
-      if (!qy) {
-        if (qx) {
-          x = (s - 1) - (x & (s - 1));
-          y = (s - 1) - (y & (s - 1));
-        }
-        const uint32_t tmp = x;
-        x = y;
-        y = tmp;
-      }
-    }
+    uint32_t sw = 0, fl = 0;
+    xy2d_levels((uint32_t)cx, (uint32_t)cy, lg, 0, d, sw, fl);
   }
   // Walk the curve's quadrant tree top-down. The current sub-square's local
   // coordinates p map to grid coordinates P + M p (M a signed permutation).
@@ -124,8 +75,6 @@ __global__ void __launch_bounds__(256) hilbert_grid(int32_t H, int32_t W, int32_
   // quadrant 0 is transposed, quadrant 3 anti-transposed.
   int32_t px = 0, py = 0, m00 = 1, m01 = 0, m10 = 0, m11 = 1;
   uint32_t before = 0;
-  int32_t lg = 0;
-  while ((1 << lg) < side) ++lg;
   for (int32_t l = lg - 1; l >= 0; --l) {
     const int32_t s = 1 << l;
     const uint32_t j = (d >> (2 * l)) & 3u;
@@ -170,11 +119,16 @@ hipError_t launch_hilbert_grid(int32_t H, int32_t W, int32_t *order, int32_t *ra
 
 hipError_t launch_hilbert_perm(int32_t side, int32_t *order, int32_t *rank,
                                hipStream_t s) {
+  if (!order && !rank) return hipSuccess;
+  int32_t lg = 0;
+  while ((1 << lg) < side) ++lg;
   const int32_t n = side * side;
-  const int32_t blocks = (n + 255) / 256;
-  const int32_t bo = order ? blocks : 0, br = rank ? blocks : 0;
-  if (bo + br == 0) return hipSuccess;
-  hipLaunchKernelGGL(hilbert_square, dim3(bo + br), dim3(256), 0, s, side, n, bo, order, rank);
+  if (lg < 2) {
+    hipLaunchKernelGGL(hilbert_square1, dim3((n + 255) / 256), dim3(256), 0, s, lg, n, order, rank);
+    return hipGetLastError();
+  }
+  const HilbertJob job = make_hilbert_job(lg, order, rank);
+  hipLaunchKernelGGL(hilbert_square4, dim3(job.blocks), dim3(256), 0, s, job);
   return hipGetLastError();
 }
 

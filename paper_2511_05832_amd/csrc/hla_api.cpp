@@ -142,8 +142,7 @@ const char *hla_last_error(void) { return g_last_error.c_str(); }
 
 const char *hla_version(void) { return "libhla 0.1 (gfx950)"; }
 
-hla_status hla_hilbert_perm(int32_t H, int32_t W, int32_t *order, int32_t *rank,
-                            hla_stream_t stream) {
+static hla_status check_hilbert(int32_t H, int32_t W, const int32_t *order, const int32_t *rank) {
   if (H < 1 || W < 1) return fail(HLA_ERR_INVALID_ARG, "grid %dx%d must be positive", H, W);
   if (H > (1 << 15) || W > (1 << 15))
     return fail(HLA_ERR_UNSUPPORTED, "Hilbert order needs H, W <= 32768 (got %dx%d)", H, W);
@@ -151,6 +150,13 @@ hla_status hla_hilbert_perm(int32_t H, int32_t W, int32_t *order, int32_t *rank,
   if (rank && !aligned(rank, 4)) return fail(HLA_ERR_INVALID_ARG, "rank is not 4-byte aligned");
   if (order && rank && overlaps(order, (int64_t)H * W * 4, rank, (int64_t)H * W * 4))
     return fail(HLA_ERR_INVALID_ARG, "order and rank overlap");
+  return HLA_OK;
+}
+
+hla_status hla_hilbert_perm(int32_t H, int32_t W, int32_t *order, int32_t *rank,
+                            hla_stream_t stream) {
+  hla_status st = check_hilbert(H, W, order, rank);
+  if (st != HLA_OK) return st;
   if (!order && !rank) return HLA_OK;
   if (H == W && is_pow2(H))
     return hip_status(hla::launch_hilbert_perm(H, order, rank, (hipStream_t)stream), "hla_hilbert_perm");
@@ -206,7 +212,9 @@ hla_status hla_block_mask_dims(const hla_pattern_desc *pat, int32_t tile_m, int3
   return HLA_OK;
 }
 
-hla_status hla_build_block_mask(hla_block_mask *mask, hla_stream_t stream) {
+// Validates a block mask for building and fills its host fields (N, n_qtiles,
+// n_ktiles); *with_cols tells whether the transposed lists are asked for.
+static hla_status check_block_mask(hla_block_mask *mask, bool *with_cols) {
   if (!mask) return fail(HLA_ERR_INVALID_ARG, "mask is NULL");
   int32_t nq = 0, nk = 0;
   hla_status st = hla_block_mask_dims(&mask->pat, mask->tile_m, mask->tile_n, &nq, &nk);
@@ -231,13 +239,67 @@ hla_status hla_build_block_mask(hla_block_mask *mask, hla_stream_t stream) {
   mask->N = mask->pat.H * mask->pat.W;
   mask->n_qtiles = nq;
   mask->n_ktiles = nk;
+  *with_cols = nset == 4;
+  return HLA_OK;
+}
+
+hla_status hla_build_block_mask(hla_block_mask *mask, hla_stream_t stream) {
+  bool with_cols = false;
+  hla_status st = check_block_mask(mask, &with_cols);
+  if (st != HLA_OK) return st;
   const hla::PatternArgs pa = hla::make_pattern_args(mask->pat);
   const hla::BlockLists rows = {mask->n_full, mask->full_idx, mask->n_part, mask->part_idx};
   const hla::BlockLists tcols = {mask->n_full_t, mask->full_idx_t, mask->n_part_t, mask->part_idx_t};
-  return hip_status(hla::launch_block_mask(pa, mask->tile_m, mask->tile_n, nq, nk, rows,
-                                           nset ? &tcols : nullptr, mask->totals,
-                                           (hipStream_t)stream),
+  return hip_status(hla::launch_block_mask(pa, mask->tile_m, mask->tile_n, mask->n_qtiles,
+                                           mask->n_ktiles, rows, with_cols ? &tcols : nullptr,
+                                           mask->totals, (hipStream_t)stream),
                     "hla_build_block_mask");
+}
+
+hla_status hla_build_path_and_mask(int32_t H, int32_t W, int32_t *order, int32_t *rank,
+                                   hla_block_mask *mask, hla_stream_t stream) {
+  hla_status st = check_hilbert(H, W, order, rank);
+  if (st != HLA_OK) return st;
+  bool with_cols = false;
+  if ((st = check_block_mask(mask, &with_cols)) != HLA_OK) return st;
+  if (mask->pat.H != H || mask->pat.W != W)
+    return fail(HLA_ERR_INVALID_ARG, "the mask's pattern is on a %dx%d grid, the path on %dx%d",
+                mask->pat.H, mask->pat.W, H, W);
+  const int64_t nb = (int64_t)H * W * 4;
+  int32_t *outs[2] = {order, rank};
+  const char *onames[2] = {"order", "rank"};
+  int32_t *arrs[8] = {mask->n_full, mask->full_idx, mask->n_part, mask->part_idx,
+                      mask->n_full_t, mask->full_idx_t, mask->n_part_t, mask->part_idx_t};
+  const int64_t alen[8] = {(int64_t)mask->n_qtiles * 4, (int64_t)mask->n_qtiles * mask->n_ktiles * 4,
+                           (int64_t)mask->n_qtiles * 4, (int64_t)mask->n_qtiles * mask->n_ktiles * 4,
+                           (int64_t)mask->n_ktiles * 4, (int64_t)mask->n_qtiles * mask->n_ktiles * 4,
+                           (int64_t)mask->n_ktiles * 4, (int64_t)mask->n_qtiles * mask->n_ktiles * 4};
+  for (int o = 0; o < 2; ++o) {
+    if (!outs[o]) continue;
+    for (int i = 0; i < 8; ++i)
+      if (arrs[i] && overlaps(outs[o], nb, arrs[i], alen[i]))
+        return fail(HLA_ERR_INVALID_ARG, "%s overlaps the mask's arrays", onames[o]);
+    if (mask->totals && overlaps(outs[o], nb, mask->totals, 8))
+      return fail(HLA_ERR_INVALID_ARG, "%s overlaps mask->totals", onames[o]);
+  }
+  const hla::PatternArgs pa = hla::make_pattern_args(mask->pat);
+  const hla::BlockLists rows = {mask->n_full, mask->full_idx, mask->n_part, mask->part_idx};
+  const hla::BlockLists tcols = {mask->n_full_t, mask->full_idx_t, mask->n_part_t, mask->part_idx_t};
+  const hipStream_t s = (hipStream_t)stream;
+  if (H == W && is_pow2(H) && H >= 4 && (order || rank))
+    return hip_status(hla::launch_path_and_mask(H, order, rank, pa, mask->tile_m, mask->tile_n,
+                                                mask->n_qtiles, mask->n_ktiles, rows,
+                                                with_cols ? &tcols : nullptr, mask->totals, s),
+                      "hla_build_path_and_mask");
+  if (order || rank) {
+    const hipError_t e = H == W && is_pow2(H) ? hla::launch_hilbert_perm(H, order, rank, s)
+                                              : hla::launch_hilbert_grid(H, W, order, rank, s);
+    if (e != hipSuccess) return hip_status(e, "hla_build_path_and_mask");
+  }
+  return hip_status(hla::launch_block_mask(pa, mask->tile_m, mask->tile_n, mask->n_qtiles,
+                                           mask->n_ktiles, rows, with_cols ? &tcols : nullptr,
+                                           mask->totals, s),
+                    "hla_build_path_and_mask");
 }
 
 }  // extern "C"

@@ -75,12 +75,22 @@ struct BlockLists {
   int32_t *n_full, *full_idx, *n_part, *part_idx;
 };
 
+struct HilbertJob;
+
 // Row lists always; column lists when cols is not NULL; totals (of the row
-// lists) when totals is not NULL.
+// lists) when totals is not NULL. path (optional): a Hilbert index job run by
+// extra workgroups of the row-list launch.
 hipError_t launch_block_mask(const PatternArgs &pat, int32_t tile_m,
                              int32_t tile_n, int32_t n_qtiles, int32_t n_ktiles,
                              const BlockLists &rows, const BlockLists *cols,
-                             int32_t *totals, hipStream_t s);
+                             int32_t *totals, hipStream_t s, const HilbertJob *path = nullptr);
+
+// The Hilbert index of a side x side square (side a power of two >= 4) and the
+// tile lists in one launch (plus the column-list and totals launches if asked).
+hipError_t launch_path_and_mask(int32_t side, int32_t *order, int32_t *rank,
+                                const PatternArgs &pat, int32_t tile_m, int32_t tile_n,
+                                int32_t n_qtiles, int32_t n_ktiles, const BlockLists &rows,
+                                const BlockLists *cols, int32_t *totals, hipStream_t s);
 
 // Forward modes: plain (tensors in sequence order), gather (tensors in grid
 // order, sequence position i is row order[i]), rpb (tensors in sequence order,

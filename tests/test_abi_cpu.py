@@ -194,6 +194,26 @@ def test_attn_fwd_rpb_validation(L):
     assert call(good_o, good_t, d=48) == hla.HLA_ERR_UNSUPPORTED
 
 
+def test_build_path_and_mask_validation(L):
+    """Both halves are validated before anything is enqueued; the mask must be on
+    the path's grid and the outputs may not overlap its arrays."""
+    vp = ctypes.c_void_p
+    m = fake_mask(H=64, W=64)
+    order, rank = vp(0x1000000), vp(0x2000000)
+    assert L.hla_build_path_and_mask(64, 32, order, rank, ctypes.byref(m), None) == hla.HLA_ERR_INVALID_ARG
+    assert "grid" in L.hla_last_error().decode()
+    assert L.hla_build_path_and_mask(0, 64, order, rank, ctypes.byref(m), None) == hla.HLA_ERR_INVALID_ARG
+    assert L.hla_build_path_and_mask(64, 64, vp(0x1000002), rank, ctypes.byref(m), None) == hla.HLA_ERR_INVALID_ARG
+    assert L.hla_build_path_and_mask(64, 64, order, vp(0x1000000 + 64), ctypes.byref(m), None) == hla.HLA_ERR_INVALID_ARG
+    assert L.hla_build_path_and_mask(64, 64, order, rank, None, None) == hla.HLA_ERR_INVALID_ARG
+    assert L.hla_build_path_and_mask(64, 64, vp(m.full_idx + 8), rank, ctypes.byref(m), None) == hla.HLA_ERR_INVALID_ARG
+    assert "overlaps" in L.hla_last_error().decode()
+    m.n_full_t = 0x60000      # one of four transposed-list pointers
+    assert L.hla_build_path_and_mask(64, 64, order, rank, ctypes.byref(m), None) == hla.HLA_ERR_INVALID_ARG
+    bad = fake_mask(H=64, W=64, tm=2048)
+    assert L.hla_build_path_and_mask(64, 64, order, rank, ctypes.byref(bad), None) == hla.HLA_ERR_UNSUPPORTED
+
+
 def test_build_block_mask_rejects_partial_column_lists(L):
     m = hla.BlockMaskStruct()
     m.pat = desc("hilbert_slide", 64, 64, 128)

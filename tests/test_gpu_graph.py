@@ -51,6 +51,42 @@ def test_attention_step_graph_replays_match_eager():
         assert torch.equal(mask.part_idx, ref_lists), r
 
 
+def test_fused_attention_step_graph_replays_match_eager():
+    """The measured step: the Hilbert index and the tile lists in one launch, then the
+    attention with the reordering fused in, on grid-ordered q, k, v."""
+    pat = W.Pattern(W.HILBERT_WINDOW, 64, 64, 256)
+    B, Hh, N, d = 2, 2, 4096, 64
+    q, k, v = (t.cuda() for t in W.attn_inputs(B, Hh, N, d, "bf16", seed=22))
+    o = torch.empty_like(q)
+    lse = torch.empty((B, Hh, N), dtype=torch.float32, device="cuda")
+    order = torch.empty(N, dtype=torch.int32, device="cuda")
+    rank = torch.empty(N, dtype=torch.int32, device="cuda")
+    mask = hla.BlockMask(pat, 128, 64, totals=False)
+
+    def step():
+        mask.build_with_path(order, rank)
+        hla.attn_fwd_perm(q, k, v, order, mask, 0.125, out=o, lse=lse)
+
+    step()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (o, lse, order, rank, mask.full_idx, mask.n_full)]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for r in range(4):
+        o.normal_()
+        lse.fill_(float("nan"))
+        order.fill_(0)
+        rank.fill_(-1)
+        mask.full_idx.fill_(-7)
+        mask.n_full.fill_(3)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for got, want in zip((o, lse, order, rank, mask.full_idx, mask.n_full), ref):
+            assert torch.equal(got, want), r
+
+
 def test_layer_step_graph_replays_match_eager():
     w = W.LayerWorkload("graph_layer", H=16, W=16, B=2, heads=2, d=32, half_width=20,
                         tile_m=128, tile_n=64, seed=22)

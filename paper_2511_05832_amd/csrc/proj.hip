@@ -169,6 +169,11 @@ __global__ void __launch_bounds__(64 * kWaves, 2) proj_rows_kernel(ProjArgs p) {
   const int b = tt / p.N, n = tt - b * p.N;
   const int ntiles = p.F / FT;
   constexpr int NST = 4 * FB;   // stores per lane and tile (8 bytes each)
+  // Output projection: this token's output row, loaded once, before the loop (a
+  // load of the order entry beside the stores made the compiler wait for every
+  // copy in flight on each tile).
+  int64_t yrow = (int64_t)tt;
+  if (MODE == 1 && p.order) yrow = (int64_t)b * p.N + p.order[n];
 
   // The stores of tile j from its bf16 results (4 consecutive features each).
   // QKV: a 32-feature block lies in one head of one of q, k, v (d % 32 == 0), so
@@ -188,7 +193,6 @@ __global__ void __launch_bounds__(64 * kWaves, 2) proj_rows_kernel(ProjArgs p) {
         for (int g = 0; g < 4; ++g)
           *reinterpret_cast<bf16x4 *>(base + (row + 8 * g + 4 * half)) = o[4 * f + g];
       } else {
-        const int64_t yrow = p.order ? (int64_t)b * p.N + p.order[n] : (int64_t)tt;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int feat = j * FT + f * 32 + 8 * g + 4 * half;

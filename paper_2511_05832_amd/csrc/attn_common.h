@@ -39,9 +39,10 @@ __device__ __forceinline__ int sload(const int32_t *p) {
 // the queries that may attend key x (the same relation read the other way; only
 // the neighbourhood patterns are not symmetric).
 
+// (The row-major patterns keep their row range [rlo, rhi] in lo, hi.)
 struct Region {
   bool one_d;
-  int lo, hi, rlo, rhi, clo, chi;
+  int lo, hi, clo, chi;
 };
 
 // Neighbourhood of length k on an axis of `extent` cells: query x attends
@@ -63,7 +64,7 @@ __device__ __forceinline__ Region region_of(const PatternArgs &P, int x) {
   Region R;
   R.one_d = P.kind == HLA_HILBERT_WINDOW || P.kind == HLA_HILBERT_SLIDE ||
             P.kind == HLA_HILBERT_NEIGHBORHOOD || P.kind == HLA_HILBERT_SHIFTED_WINDOW;
-  R.lo = R.hi = R.rlo = R.rhi = R.clo = R.chi = 0;
+  R.lo = R.hi = R.clo = R.chi = 0;
   if (P.kind == HLA_HILBERT_WINDOW) {
     R.lo = (x / P.p0) * P.p0;
     R.hi = R.lo + P.p0 - 1;
@@ -80,30 +81,29 @@ __device__ __forceinline__ Region region_of(const PatternArgs &P, int x) {
   } else {
     const int r = (int)fdiv((uint32_t)x, P.wdiv), c = x - r * P.W;
     if (P.kind == HLA_ROWMAJOR_WINDOW) {
-      R.rlo = (r / P.p0) * P.p0; R.rhi = R.rlo + P.p0 - 1;
+      R.lo = (r / P.p0) * P.p0; R.hi = R.lo + P.p0 - 1;
       R.clo = (c / P.p1) * P.p1; R.chi = R.clo + P.p1 - 1;
     } else if (P.kind == HLA_ROWMAJOR_SLIDE) {
-      R.rlo = r - P.p0; R.rhi = r + P.p0;
+      R.lo = r - P.p0; R.hi = r + P.p0;
       R.clo = c - P.p1; R.chi = c + P.p1;
     } else if (KEYS_OF_QUERY) {
-      neigh_fwd(r, P.p0, P.H, R.rlo, R.rhi);
+      neigh_fwd(r, P.p0, P.H, R.lo, R.hi);
       neigh_fwd(c, P.p1, P.W, R.clo, R.chi);
     } else {
-      neigh_bwd(r, P.p0, P.H, R.rlo, R.rhi);
+      neigh_bwd(r, P.p0, P.H, R.lo, R.hi);
       neigh_bwd(c, P.p1, P.W, R.clo, R.chi);
     }
   }
   // Clip at the end of the sequence: on a ragged tiling the edge tiles hold
   // padded positions >= N (grid rows >= H), which pair with nothing.
-  R.hi = min(R.hi, P.N - 1);
-  R.rhi = min(R.rhi, P.H - 1);
+  R.hi = min(R.hi, R.one_d ? P.N - 1 : P.H - 1);
   return R;
 }
 
 __device__ __forceinline__ bool region_has(const Region &R, const PatternArgs &P, int y) {
   if (R.one_d) return y >= R.lo && y <= R.hi;
   const int r = (int)fdiv((uint32_t)y, P.wdiv), c = y - r * P.W;
-  return r >= R.rlo && r <= R.rhi && c >= R.clo && c <= R.chi;
+  return r >= R.lo && r <= R.hi && c >= R.clo && c <= R.chi;
 }
 
 // Element mask over NB 32x32 accumulator blocks. Slot v of this lane in block
@@ -127,7 +127,7 @@ __device__ __forceinline__ void mask_blocks(f32x16 (&s)[NB], const Region &R,
         s[kb][v] = ok ? s[kb][v] : -__builtin_inff();
       }
   } else if ((P.W & 7) == 0) {
-    const uint32_t rspan = (uint32_t)(R.rhi - R.rlo), cspan = (uint32_t)(R.chi - R.clo);
+    const uint32_t rspan = (uint32_t)(R.hi - R.lo), cspan = (uint32_t)(R.chi - R.clo);
 #pragma unroll
     for (int kb = 0; kb < NB; ++kb)
 #pragma unroll
@@ -135,7 +135,7 @@ __device__ __forceinline__ void mask_blocks(f32x16 (&s)[NB], const Region &R,
         const int y0 = base + 32 * kb + 16 * g;
         const int r = (int)fdiv((uint32_t)y0, P.wdiv);
         const int c0 = y0 - r * P.W - R.clo;
-        const bool row_ok = (uint32_t)(r - R.rlo) <= rspan;
+        const bool row_ok = (uint32_t)(r - R.lo) <= rspan;
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
           const bool ok = row_ok & ((uint32_t)(c0 + t) <= cspan);
@@ -245,6 +245,21 @@ __device__ __forceinline__ void wait_then_barrier() {
   static_assert(N >= 0 && N < 64, "vmcnt out of range");
   asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
+// Wait until at most n of this wave's vector memory operations are in flight
+// (0 <= n <= MAXN; a larger n waits for MAXN), then barrier the workgroup.
+template <int MAXN>
+__device__ __forceinline__ void wait_n_then_barrier(int n) {
+  if constexpr (MAXN > 0) {
+    if (n >= MAXN) {
+      wait_then_barrier<MAXN>();
+      return;
+    }
+    wait_n_then_barrier<MAXN - 1>(n);
+  } else {
+    wait_then_barrier<0>();
+  }
+}
+
 // Dispatch on the number of tiles still allowed in flight (0 .. MAXA), LPT
 // vector memory operations per tile.
 template <int LPT, int MAXA>

@@ -284,21 +284,6 @@ struct StreamArgs {
   FastDiv ndiv;            // division by N
 };
 
-// Wait until at most n of this wave's vector memory operations are in flight
-// (0 <= n <= MAXN), then barrier the workgroup.
-template <int MAXN>
-__device__ __forceinline__ void wait_n_then_barrier(int n) {
-  if constexpr (MAXN > 0) {
-    if (n >= MAXN) {
-      wait_then_barrier<MAXN>();
-      return;
-    }
-    wait_n_then_barrier<MAXN - 1>(n);
-  } else {
-    wait_then_barrier<0>();
-  }
-}
-
 // LDS writes of this wave done, then barrier (vector memory left in flight).
 __device__ __forceinline__ void lds_then_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");

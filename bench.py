@@ -138,9 +138,13 @@ def roofline_record(kernel, ms, nbytes, flops, dtype):
     return rec
 
 
-def perm_record(kernel_ms, nbytes):
+def perm_record(kernel_ms, nbytes, traffic=None):
+    """A permutation kernel: algorithmic bytes (tensor read and written once, plus
+    the order array) per launch, their rate, its fraction of the HBM peak, and the
+    counter-measured bytes per launch where a current summary exists."""
     gbs = nbytes / (kernel_ms * 1e-3) / 1e9
-    return {"ms_per_call": kernel_ms, "gbs": gbs, "frac": gbs / HBM_PEAK_GBS, "bytes": nbytes}
+    return {"ms_per_call": kernel_ms, "gbs": gbs, "frac": gbs / HBM_PEAK_GBS, "bytes": nbytes,
+            "traffic": traffic}
 
 
 # ----------------------------------------------------------------------------
@@ -410,14 +414,17 @@ class LayerPipeline:
 
 ATTN_SOURCES = ("paper_2511_05832_amd/csrc/attn_bf16.hip", "paper_2511_05832_amd/csrc/attn_common.h",
                 "paper_2511_05832_amd/csrc/hla_internal.h")
+PERM_SOURCES = ("paper_2511_05832_amd/csrc/permute.hip", "paper_2511_05832_amd/csrc/hla_internal.h")
+PROJ_SOURCES = ("paper_2511_05832_amd/csrc/proj.hip", "paper_2511_05832_amd/csrc/attn_common.h",
+                "paper_2511_05832_amd/csrc/hla_internal.h")
 
 
-def measured_traffic(workload_name, kernel="attn_fwd"):
-    """HBM bytes per attention dispatch from the committed rocprofv3 counter summary
-    for this workload and kernel (attn_fwd or attn_fwd_perm), or None if there is
-    none or the kernel source changed since."""
+def profile_traffic(name, sources):
+    """HBM bytes per dispatch from the committed rocprofv3 counter summary
+    profiles/<name>_traffic.txt, or None if there is none or one of the kernel's
+    source files changed since the counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"{kernel}_bf16_{workload_name}_traffic.txt")
+    path = os.path.join(ROOT, "profiles", f"{name}_traffic.txt")
     if not os.path.exists(path):
         return None
     fields = {}
@@ -426,7 +433,7 @@ def measured_traffic(workload_name, kernel="attn_fwd"):
         if sep:
             fields[k.strip()] = v.strip()
     h = hashlib.sha256()
-    for src in ATTN_SOURCES:
+    for src in sources:
         h.update(open(os.path.join(ROOT, src), "rb").read())
     if fields.get("kernel_source_sha256") != h.hexdigest():
         return None
@@ -434,6 +441,12 @@ def measured_traffic(workload_name, kernel="attn_fwd"):
         return int(fields["traffic_bytes_per_dispatch"])
     except (KeyError, ValueError):
         return None
+
+
+def measured_traffic(workload_name, kernel="attn_fwd"):
+    """HBM bytes per attention dispatch (kernel attn_fwd, attn_fwd_perm or
+    attn_fwd_rpb) on this workload from the committed counter summary."""
+    return profile_traffic(f"{kernel}_bf16_{workload_name}", ATTN_SOURCES)
 
 
 def make_pipeline(w, hla, fused=False):
@@ -636,8 +649,10 @@ def attn_config_record(w, hla, steps, warmup, fused_step=True):
     rec["tile_flops"] = flops
     if comp.hilbert:
         pb = comp.perm_bytes_per_tensor()
-        rec["perm"] = {"gather": perm_record(comp.perm_kernel_ms(n), pb),
-                       "scatter": perm_record(comp.perm_kernel_ms(n, scatter=True), pb)}
+        rec["perm"] = {"gather": perm_record(comp.perm_kernel_ms(n), pb,
+                                             profile_traffic(f"permute_rows_gather_{w.name}", PERM_SOURCES)),
+                       "scatter": perm_record(comp.perm_kernel_ms(n, scatter=True), pb,
+                                              profile_traffic(f"permute_rows_scatter_{w.name}", PERM_SOURCES))}
     rec["composed_step"] = {"ms_per_step": rc["ms_per_step"], "ms_per_step_eager": rc["ms_per_step_eager"],
                             "attn_kernel_ms": kms_c, "value": flops / (rc["ms_per_step"] * 1e-3) / 1e12}
     del comp
@@ -691,6 +706,9 @@ def layer_config_record(w, hla, steps, warmup):
         else:
             nb, fl = lp.proj_figures(which)
         kernels[which] = roofline_record(name, ms, nb, fl, "bf16")
+        kernels[which]["traffic"] = (measured_traffic(w.name, "attn_fwd") if which == "attn" else
+                                     profile_traffic(f"proj_stream_{'qkv' if which == 'qkv' else 'out'}_{w.name}",
+                                                     PROJ_SOURCES))
     att = kernels["attn"]["kernel_ms_per_launch"]
     rec.update({
         "step": "Hilbert index and tile lists (one launch), QKV projection with the gather fused in, "

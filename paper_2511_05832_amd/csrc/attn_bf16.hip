@@ -80,8 +80,9 @@ namespace {
 
 constexpr int BN = 64;
 constexpr float kRescaleSlack = 8.f;  // log2 units the softmax reference may lag the max
-// Largest weight sum per lane and tile the max-free softmax step accepts
-// against a stale reference (2^32: far from fp32 overflow in O and l).
+// Largest running weight sum per lane (its l, after adding the tile) the
+// max-free softmax step accepts against a stale reference (2^32: far from fp32
+// overflow in O and l).
 constexpr float kFastBound = 4294967296.f;
 // LDS ring depth. Three 16 KiB stages (d = 64) let three workgroups share a
 // CU's 160 KiB; with the launch bound below that is the occupancy that measured
@@ -232,32 +233,56 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
     kch[j] = (cs ^ swz_k<D>(r)) * 8;
     vch[j] = (cs ^ swz_v<D>(r)) * 8;
   }
-  // Copies of the K/V tile of list entry i into a ring stage.
+  // Copies of the K/V tile of list entry i into a ring stage, each from the
+  // wave-uniform slice base plus this lane's 32-bit byte offset (a slice holds at
+  // most 2^30 elements).
+  // (Plain mode: a tile inside the sequence takes its first row into the scalar
+  // base, so its offsets are the loop-invariant in-tile ones; the ragged last
+  // tile's rows past the end of the sequence read row N - 1, and the mask of that
+  // always partial tile drops them.)
+  uint32_t kin[CPW], vin[CPW];
+#pragma unroll
+  for (int j = 0; j < CPW; ++j) {
+    kin[j] = (uint32_t)(krow[j] * D + kch[j]) * 2u;
+    vin[j] = (uint32_t)(krow[j] * D + vch[j]) * 2u;
+  }
   auto issue_tile = [&](int i, int stage) {
     char *base = lds + stage * STAGE;
-    const __bf16 *Kt, *Vt;
-    int64_t roff[CPW];
+    const __bf16 *Kt = K, *Vt = V;
+    uint32_t ko[CPW], vo[CPW];
     if constexpr (GATHER) {
       const int32_t *rows = idx_k(i);
-      Kt = K;
-      Vt = V;
 #pragma unroll
-      for (int j = 0; j < CPW; ++j) roff[j] = (int64_t)rows[krow[j]] * D;
+      for (int j = 0; j < CPW; ++j) {
+        const uint32_t r = (uint32_t)rows[krow[j]] * (uint32_t)(D * 2);
+        ko[j] = r + (uint32_t)kch[j] * 2u;
+        vo[j] = r + (uint32_t)vch[j] * 2u;
+      }
     } else {
-      // rows past the end of the sequence (ragged last key tile) read row N - 1;
-      // the mask of that (always partial) tile drops them
       const int k0 = tile_of(i) * BN;
-      Kt = K;
-      Vt = V;
+      if (k0 + BN <= a.N) {
+        Kt = K + (int64_t)k0 * D;
+        Vt = V + (int64_t)k0 * D;
 #pragma unroll
-      for (int j = 0; j < CPW; ++j) roff[j] = (int64_t)min(k0 + krow[j], a.N - 1) * D;
+        for (int j = 0; j < CPW; ++j) {
+          ko[j] = kin[j];
+          vo[j] = vin[j];
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < CPW; ++j) {
+          const uint32_t r = (uint32_t)min(k0 + krow[j], a.N - 1) * (uint32_t)(D * 2);
+          ko[j] = r + (uint32_t)kch[j] * 2u;
+          vo[j] = r + (uint32_t)vch[j] * 2u;
+        }
+      }
     }
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
-      lds_dma16(Kt + roff[j] + kch[j], lds_addr(base + (j * NW + wave) * 1024));
+      lds_dma16_at(Kt, ko[j], lds_addr(base + (j * NW + wave) * 1024));
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
-      lds_dma16(Vt + roff[j] + vch[j], lds_addr(base + TILE + (j * NW + wave) * 1024));
+      lds_dma16_at(Vt, vo[j], lds_addr(base + TILE + (j * NW + wave) * 1024));
   };
   // GATHER: the row indices of list entry i (one per lane of the first wave)
   // into its slot. RPB: every wave copies BN / NW of them. Positions past the end
@@ -511,41 +536,41 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
       }
       if constexpr (decltype(masked)::value) mask_blocks<2>(s, R, P, tile_of(it) * BN + 8 * half);
     };
-    // Weights p = 2^(s * smul - m) in place of the scores, and this lane's sum.
-    auto weights = [&](f32x16 (&s)[2], float m) {
-      float lq[4];
+    // Weights p = 2^(s * smul - m) in place of the scores; returns l0 plus this
+    // lane's sum of them (two running sums, one per key block, the first seeded
+    // with l0).
+    auto weights = [&](f32x16 (&s)[2], float m, float l0) {
+      float la = l0, lb = 0.f;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int o = 8 * (g & 1);
-        float acc = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s[g >> 1][o + e], smul, -m));
-          acc += pv;
-          s[g >> 1][o + e] = pv;
-        }
-        lq[g] = acc;
+      for (int v = 0; v < 16; ++v) {
+        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[0][v], smul, -m));
+        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[1][v], smul, -m));
+        la += p0;
+        lb += p1;
+        s[0][v] = p0;
+        s[1][v] = p1;
       }
-      return (lq[0] + lq[1]) + (lq[2] + lq[3]);
+      return la + lb;
     };
 
     // Online softmax in the log2 domain with a lazily moved reference m_run
     // (O and l always share it). Once every row of the wave has a finite
     // reference, a tile first takes its weights against the reference as it
     // stands, with no row max at all: weights up to 2^32 are harmless (fp32
-    // accumulators, bf16 operands), and since they are >= 0 their sum bounds
-    // each of them, so one compare of the sum (which is needed anyway; NaN and
-    // inf fail it too) validates the tile. Only when some row's sum fails does
-    // the tile fall back: its scores are recomputed from LDS and it takes the
-    // max path. (Straight-line code rather than a retry loop: with a loop, the
-    // compiler kept O in two register sets and copied it on every tile.)
+    // accumulators, bf16 operands), and since they and l_run are >= 0 the new
+    // running sum bounds each of them, so one compare of it (NaN and inf fail it
+    // too) validates the tile. Only when some row's sum fails does the tile
+    // fall back: its scores are recomputed from LDS and it takes the max path,
+    // l_run being untouched until the tile is accepted. (Straight-line code
+    // rather than a retry loop: with a loop, the compiler kept O in two register
+    // sets and copied it on every tile.)
     f32x16 s[2];
     scores(s);
     bool slow = !primed;
-    float lt = 0.f;
+    float ln = 0.f;
     if (primed) {
-      lt = weights(s, m_run);
-      if (__ballot(!(lt <= kFastBound))) {
+      ln = weights(s, m_run, l_run);
+      if (__ballot(!(ln <= kFastBound))) {
         slow = true;
         // (the memory clobber makes the K operand reads happen again instead of
         // keeping the first ones in registers across the weights)
@@ -576,10 +601,10 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
         for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
         m_run = m_new;
       }
-      lt = weights(s, m_run == -__builtin_inff() ? 0.f : m_run);
+      ln = weights(s, m_run == -__builtin_inff() ? 0.f : m_run, l_run);
       primed = !__ballot(m_run == -__builtin_inff());
     }
-    l_run += lt;
+    l_run = ln;
     // Row sums above are fp32 sums of the unrounded weights; P goes to the PV
     // product rounded to bf16.
     bf16x8 pop[4];

@@ -109,23 +109,49 @@ __device__ __forceinline__ bool region_has(const Region &R, const PatternArgs &P
 // Element mask over NB 32x32 accumulator blocks. Slot v of this lane in block
 // kb holds the position base + 32*kb + 16*(v/8) + v%8 (runs of eight
 // consecutive positions; base = first position of block 0 + 8 * lane half).
-// Disallowed entries become -inf. For the 1-D patterns one unsigned compare per
-// entry; for the row-major patterns with W a multiple of 8 a run never crosses a
-// grid row, so one division per run. The pattern branch is taken once for all
-// blocks.
+// Disallowed entries become -inf. For the row-major patterns with W a multiple
+// of 8 a run never crosses a grid row, so one division per run. The pattern
+// branch is taken once for all blocks.
+//
+// 1-D patterns: the lane's allowed slots are the offsets c = position - base in
+// [R.lo - base, R.hi - base]. A partial tile at the edge of a band or a window
+// usually cuts that interval on one side only, for every lane of the wave; two
+// ballots find out, and then one compare per entry against the cut side's bound
+// does (instead of the two-sided unsigned compare, which needs an add per
+// entry), or nothing at all when no lane of the wave loses a slot. (A row with
+// an empty interval - only padded rows past the end of the sequence, whose
+// results are never stored - may keep slots; every stored row is exact.)
 template <int NB>
 __device__ __forceinline__ void mask_blocks(f32x16 (&s)[NB], const Region &R,
                                             const PatternArgs &P, int base) {
   if (R.one_d) {
-    const int off = base - R.lo;
-    const uint32_t span = (uint32_t)(R.hi - R.lo);
+    constexpr int CMAX = 32 * (NB - 1) + 23;   // largest offset a lane holds
+    const int lo = R.lo - base, hi = R.hi - base;
+    const bool cut_lo = __ballot(lo > 0) != 0;
+    const bool cut_hi = __ballot(hi < CMAX) != 0;
+    if (!cut_lo && !cut_hi) return;
+    if (cut_lo && cut_hi) {
+      const uint32_t span = (uint32_t)(hi - lo);
 #pragma unroll
-    for (int kb = 0; kb < NB; ++kb)
+      for (int kb = 0; kb < NB; ++kb)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const bool ok = (uint32_t)(off + 32 * kb + 16 * (v >> 3) + (v & 7)) <= span;
-        s[kb][v] = ok ? s[kb][v] : -__builtin_inff();
-      }
+        for (int v = 0; v < 16; ++v) {
+          const bool ok = (uint32_t)(32 * kb + 16 * (v >> 3) + (v & 7) - lo) <= span;
+          s[kb][v] = ok ? s[kb][v] : -__builtin_inff();
+        }
+    } else if (cut_lo) {   // every lane keeps all slots from its lower bound on
+#pragma unroll
+      for (int kb = 0; kb < NB; ++kb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          s[kb][v] = 32 * kb + 16 * (v >> 3) + (v & 7) >= lo ? s[kb][v] : -__builtin_inff();
+    } else {               // every lane keeps all slots up to its upper bound
+#pragma unroll
+      for (int kb = 0; kb < NB; ++kb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          s[kb][v] = 32 * kb + 16 * (v >> 3) + (v & 7) <= hi ? s[kb][v] : -__builtin_inff();
+    }
   } else if ((P.W & 7) == 0) {
     const uint32_t rspan = (uint32_t)(R.hi - R.lo), cspan = (uint32_t)(R.chi - R.clo);
 #pragma unroll
@@ -198,6 +224,17 @@ __device__ __forceinline__ void lds_dma16(const void *src, uint32_t dst) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                :
                : "v"(src), "s"(__builtin_amdgcn_readfirstlane(dst))
+               : "memory", "m0");
+#endif
+}
+// The same copy from a wave-uniform base plus a per-lane 32-bit byte offset (the
+// saddr form): the 64-bit address add happens in the memory pipeline instead of
+// taking two vector instructions per copy. The offset must stay below 2^31.
+__device__ __forceinline__ void lds_dma16_at(const void *base, uint32_t off, uint32_t dst) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(off), "s"(base), "s"(__builtin_amdgcn_readfirstlane(dst))
                : "memory", "m0");
 #endif
 }

@@ -11,8 +11,8 @@ namespace hla {
 
 // Orientation change on entering quadrant q (0..3 in visiting order): transpose
 // for q = 0, anti-transpose for q = 3, none otherwise.
-__device__ __forceinline__ uint32_t turn_sw(uint32_t q) { return 1u ^ ((q ^ (q >> 1)) & 1u); }
-__device__ __forceinline__ uint32_t turn_fl(uint32_t q) { return q & (q >> 1) & 1u; }
+constexpr uint32_t turn_sw(uint32_t q) { return 1u ^ ((q ^ (q >> 1)) & 1u); }
+constexpr uint32_t turn_fl(uint32_t q) { return q & (q >> 1) & 1u; }
 
 // Levels lg-1 .. lo of curve position d: ORs the cell's x, y bits of those
 // levels into x, y and leaves the orientation of the level-lo sub-square.
@@ -76,6 +76,19 @@ inline HilbertJob make_hilbert_job(int32_t lg, int32_t *order, int32_t *rank) {
   return j;
 }
 
+// store4 with non-temporal 16-byte stores (the index kernel's outputs stream
+// past the caches: 27.8 -> 25.5 us at 4096 x 4096).
+typedef unsigned int u32x4h __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void store4nt(int32_t *p, int32_t i4, const uint32_t (&v)[4], bool vec) {
+  if (vec) {
+    const u32x4h w = {v[0], v[1], v[2], v[3]};
+    __builtin_nontemporal_store(w, reinterpret_cast<u32x4h *>(p + 4 * i4));
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) p[4 * i4 + j] = (int32_t)v[j];
+  }
+}
+
 // Block b (< job.blocks) of the job, thread tid (< 256).
 __device__ __forceinline__ void hilbert4_block(const HilbertJob &job, int32_t b, int32_t tid) {
   const int32_t lg = job.lg, n4 = job.n4;
@@ -106,6 +119,103 @@ __device__ __forceinline__ void hilbert4_block(const HilbertJob &job, int32_t b,
       out[j] = dj;
     }
     store4(job.rank, m, out, vec);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Four levels per step: lookup tables indexed by the orientation state
+// s = sw | fl << 1 and four levels' worth of input, top level first.
+//   d2xy[s << 8 | four curve digits]   = x4 | y4 << 4 | s' << 8
+//   xy2d[s << 8 | x4 << 4 | y4]        = four curve digits | s' << 8
+// (s' = the state after the four levels). Built at compile time by the same
+// per-level rules as d2xy_levels / xy2d_levels.
+struct HilbertLut {
+  uint16_t d2xy[1024];
+  uint16_t xy2d[1024];
+};
+
+constexpr HilbertLut make_hilbert_lut() {
+  HilbertLut t{};
+  for (uint32_t s = 0; s < 4; ++s) {
+    for (uint32_t dg = 0; dg < 256; ++dg) {
+      uint32_t sw = s & 1u, fl = s >> 1, x = 0, y = 0;
+      for (int l = 3; l >= 0; --l) {
+        const uint32_t q = (dg >> (2 * l)) & 3u;
+        const uint32_t a = q >> 1, b = (q ^ a) & 1u, tt = ((a ^ b) & sw) ^ fl;
+        x |= (a ^ tt) << l;
+        y |= (b ^ tt) << l;
+        sw ^= turn_sw(q);
+        fl ^= turn_fl(q);
+      }
+      t.d2xy[s << 8 | dg] = (uint16_t)(x | y << 4 | (sw | fl << 1) << 8);
+    }
+    for (uint32_t xy = 0; xy < 256; ++xy) {
+      const uint32_t x4 = xy >> 4, y4 = xy & 15u;
+      uint32_t sw = s & 1u, fl = s >> 1, d = 0;
+      for (int l = 3; l >= 0; --l) {
+        uint32_t a = ((x4 >> l) & 1u) ^ fl, b = ((y4 >> l) & 1u) ^ fl;
+        const uint32_t tt = (a ^ b) & sw;
+        a ^= tt;
+        b ^= tt;
+        const uint32_t q = (a << 1) | (a ^ b);
+        d |= q << (2 * l);
+        sw ^= turn_sw(q);
+        fl ^= turn_fl(q);
+      }
+      t.xy2d[s << 8 | xy] = (uint16_t)(d | (sw | fl << 1) << 8);
+    }
+  }
+  return t;
+}
+
+// Block b of the job with the tables in LDS. A walk of nl levels starts at the
+// top of ceil(nl / 4) groups: the padding levels above the curve have digit 0
+// and coordinate bits 0, and each of them only toggles sw, so the walk starts
+// with sw = (number of padding levels) mod 2.
+__device__ __forceinline__ void hilbert4_block_lut(const HilbertJob &job, int32_t b, int32_t tid,
+                                                   const HilbertLut &lut) {
+  const int32_t lg = job.lg, n4 = job.n4;
+  const bool vec = job.vec != 0;
+  uint32_t out[4];
+  if (b < job.blocks_order) {
+    const int32_t m = b * 256 + tid;
+    if (m >= n4) return;
+    // levels lg-1 .. 1 of d = 4m are levels lg-2 .. 0 of m (a curve of side
+    // 2^(lg-1), one level coarser); level 0 is digit j of entry j
+    const int nl = lg - 1, ng = (nl + 3) >> 2;
+    uint32_t st = (uint32_t)(4 * ng - nl) & 1u, x = 0, y = 0;
+    for (int g = ng - 1; g >= 0; --g) {
+      const uint32_t e = lut.d2xy[st << 8 | (((uint32_t)m >> (8 * g)) & 255u)];
+      x = x << 4 | (e & 15u);
+      y = y << 4 | ((e >> 4) & 15u);
+      st = e >> 8;
+    }
+    const uint32_t sw = st & 1u, fl = st >> 1;
+#pragma unroll
+    for (uint32_t j = 0; j < 4; ++j) {
+      const uint32_t a = j >> 1, bb = (j ^ a) & 1u, t = ((a ^ bb) & sw) ^ fl;
+      out[j] = ((y << 1 | (bb ^ t)) << lg) | (x << 1 | (a ^ t));
+    }
+    store4nt(job.order, m, out, vec);
+  } else {
+    const int32_t m = (b - job.blocks_order) * 256 + tid;
+    if (m >= n4) return;
+    const uint32_t t0 = 4u * (uint32_t)m;
+    const uint32_t y = t0 >> lg, xs = (t0 & ((1u << lg) - 1u)) >> 2, ys = y >> 2;
+    // levels lg-1 .. 2 (shared by the four cells x0 .. x0+3 of row y)
+    const int nl = lg - 2, ng = (nl + 3) >> 2;
+    uint32_t st = (uint32_t)(4 * ng - nl) & 1u, d = 0;
+    for (int g = ng - 1; g >= 0; --g) {
+      const uint32_t e = lut.xy2d[st << 8 | ((xs >> (4 * g)) & 15u) << 4 | ((ys >> (4 * g)) & 15u)];
+      d = d << 8 | (e & 255u);
+      st = e >> 8;
+    }
+    // levels 1, 0 of cell x0 + j: a lookup whose top two levels are padding
+    // (two toggles of sw: the state is unchanged)
+#pragma unroll
+    for (uint32_t j = 0; j < 4; ++j)
+      out[j] = d << 4 | (lut.xy2d[st << 8 | j << 4 | (y & 3u)] & 15u);
+    store4nt(job.rank, m, out, vec);
   }
 }
 

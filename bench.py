@@ -151,17 +151,28 @@ def perm_record(kernel_ms, nbytes, traffic=None):
 # attention workloads
 
 
+def single_ok(w) -> bool:
+    """hla_attn_fwd_hilbert covers the workload: a 1-D Hilbert pattern on a 2^k x 2^k
+    grid (side >= 4), bf16."""
+    p = getattr(w, "pattern", None)
+    return (p is not None and p.hilbert and getattr(w, "dtype", "bf16") == "bf16" and p.H == p.W
+            and p.W >= 4 and (p.W & (p.W - 1)) == 0)
+
+
 class AttnPipeline:
     """One step of an attention workload. Hilbert patterns either reorder with
     separate gather and scatter passes around hla_attn_fwd (composed), or hand the
     grid-ordered tensors and the Hilbert order to hla_attn_fwd_perm, which does the
-    reordering inside its loads and stores (fused)."""
+    reordering inside its loads and stores (fused), or run the whole step - index,
+    tile lists, reordered attention - as one launch of hla_attn_fwd_hilbert
+    (single)."""
 
-    def __init__(self, w: W.AttnWorkload, hla, fused: bool = False):
+    def __init__(self, w: W.AttnWorkload, hla, fused: bool = False, single: bool = False):
         self.w, self.hla = w, hla
         pat = w.pattern
         self.hilbert = pat.hilbert
-        self.fused = fused and self.hilbert
+        self.single = single and single_ok(w)
+        self.fused = (fused or self.single) and self.hilbert
         B, Hh, N, d = w.B, w.heads, w.N, w.d
         tensor_bytes = B * Hh * N * d * esize(w.dtype)
         set_bytes = tensor_bytes * (7 if self.hilbert and not self.fused else 4)
@@ -180,10 +191,18 @@ class AttnPipeline:
         self.order = torch.empty(N, dtype=torch.int32, device="cuda")
         self.rank = torch.empty(N, dtype=torch.int32, device="cuda")
         self.mask = hla.BlockMask(pat, w.tile_m, w.tile_n, totals=False)
+        if self.single:
+            # the step computes its own; these serve the FLOP count and the backward
+            self.mask.build_with_path(self.order, self.rank)
         self.timer = Timer()
 
     def step(self, i):
         hla, w, s, T = self.hla, self.w, self.sets[i % self.nsets], self.timer
+        if self.single:
+            with T.stage("attn"):
+                hla.attn_fwd_hilbert(s["q"], s["k"], s["v"], w.pattern, w.tile_m, w.tile_n, w.scale,
+                                     out=s["o"], lse=s["lse"])
+            return
         if self.fused:
             with T.stage("path_mask"):
                 self.mask.build_with_path(self.order, self.rank)
@@ -216,7 +235,10 @@ class AttnPipeline:
 
         def call(i):
             s = self.sets[i % self.nsets]
-            if self.fused:
+            if self.single:
+                hla.attn_fwd_hilbert(s["q"], s["k"], s["v"], w.pattern, w.tile_m, w.tile_n, w.scale,
+                                     out=s["o"], lse=s["lse"])
+            elif self.fused:
                 hla.attn_fwd_perm(s["q"], s["k"], s["v"], self.order, self.mask, w.scale,
                                   out=s["o"], lse=s["lse"])
             else:
@@ -449,8 +471,9 @@ def measured_traffic(workload_name, kernel="attn_fwd"):
     return profile_traffic(f"{kernel}_bf16_{workload_name}", ATTN_SOURCES)
 
 
-def make_pipeline(w, hla, fused=False):
-    return LayerPipeline(w, hla) if isinstance(w, W.LayerWorkload) else AttnPipeline(w, hla, fused)
+def make_pipeline(w, hla, fused=False, single=False):
+    return (LayerPipeline(w, hla) if isinstance(w, W.LayerWorkload)
+            else AttnPipeline(w, hla, fused, single))
 
 
 def capture_step_graphs(pipe):
@@ -464,6 +487,26 @@ def capture_step_graphs(pipe):
         graphs.append(g)
     torch.cuda.synchronize()
     return graphs
+
+
+WARM_MS = 150.0
+
+
+def warm_replays(graphs, warmup):
+    """Untimed replays before a timed pass: the W warm-up steps, then more until
+    WARM_MS of them have run, so the timed steps start at the GPU's steady clock
+    (right after a pipeline is built the first ~5 ms of steps run up to 15%
+    slower)."""
+    for i in range(max(warmup, 1)):
+        graphs[i % len(graphs)].replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    i = 0
+    while (time.perf_counter() - t0) * 1e3 < WARM_MS:
+        for _ in range(16):
+            graphs[i % len(graphs)].replay()
+            i += 1
+        torch.cuda.synchronize()
 
 
 def run_timed(pipe, steps, warmup):
@@ -488,9 +531,7 @@ def run_timed(pipe, steps, warmup):
     eager_ms = statistics.median(marks[i].elapsed_time(marks[i + 1]) for i in range(steps))
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     graphs = capture_step_graphs(pipe)
-    for i in range(min(warmup, len(graphs)) or 1):
-        graphs[i % len(graphs)].replay()
-    torch.cuda.synchronize()
+    warm_replays(graphs, warmup)
     start.record()
     for i in range(steps):
         graphs[i % len(graphs)].replay()
@@ -525,9 +566,7 @@ def time_backward(pipe, steps, warmup):
             pipe.step_backward(i)
         graphs.append(g)
     torch.cuda.synchronize()
-    for i in range(min(warmup, len(graphs)) or 1):
-        graphs[i % len(graphs)].replay()
-    torch.cuda.synchronize()
+    warm_replays(graphs, warmup)
     start.record()
     for i in range(steps):
         graphs[i % len(graphs)].replay()
@@ -632,6 +671,15 @@ def summarize(pipe, timing):
 # one record per measured configuration
 
 
+STEP_TEXT = {
+    "attn_fwd_hilbert": "Hilbert index, tile lists and attention with the reordering fused in, in one "
+                        "launch (hla_attn_fwd_hilbert)",
+    "attn_fwd_perm": "Hilbert index and tile lists (one launch), attention with the reordering fused in "
+                     "(hla_attn_fwd_perm)",
+    "attn_fwd": "tile lists, attention",
+}
+
+
 def attn_config_record(w, hla, steps, warmup, fused_step=True):
     """A configuration's numbers: its step (for Hilbert patterns the reordering fused
     into the attention, else the plain attention), the attention kernel alone
@@ -664,10 +712,19 @@ def attn_config_record(w, hla, steps, warmup, fused_step=True):
         kms, kernel = fp.kernel_ms(n), "attn_fwd_perm"
         del fp
         torch.cuda.empty_cache()
+        if single_ok(w):
+            rec["fused_step"] = {"ms_per_step": res["ms_per_step"],
+                                 "ms_per_step_eager": res["ms_per_step_eager"],
+                                 "attn_kernel_ms": kms,
+                                 "value": flops / (res["ms_per_step"] * 1e-3) / 1e12}
+            sp = make_pipeline(w, hla, single=True)
+            res = summarize(sp, run_timed(sp, steps, warmup))
+            kms, kernel = sp.kernel_ms(n), "attn_fwd_hilbert"
+            del sp
+            torch.cuda.empty_cache()
     peak = BF16_PEAK_TFLOPS if w.dtype == "bf16" else FP32_PEAK_TFLOPS
     rec.update({
-        "step": ("Hilbert index and tile lists (one launch), attention with the reordering fused in"
-                 if kernel == "attn_fwd_perm" else "tile lists, attention"),
+        "step": STEP_TEXT[kernel],
         "ms_per_step": res["ms_per_step"], "ms_per_step_eager": res["ms_per_step_eager"],
         "value": flops / (res["ms_per_step"] * 1e-3) / 1e12, "unit": "TFLOP/s",
         "attn_ms_per_call": kms,
@@ -831,11 +888,13 @@ def main():
                     help="skip timing the backward pass of the workload")
     ap.add_argument("--no-rpb", action="store_true",
                     help="skip timing the attention with the relative position bias")
-    ap.add_argument("--step", default="fused", choices=["fused", "composed", "composed-only"],
-                    help="which step of a Hilbert workload the headline value times: the "
-                         "reordering fused into the attention (hla_attn_fwd_perm) or separate "
-                         "gather / attention / scatter calls; the other is reported beside it "
-                         "(composed-only: skip the fused step)")
+    ap.add_argument("--step", default="single", choices=["single", "fused", "composed", "composed-only"],
+                    help="which step of a Hilbert workload the headline value times: the whole "
+                         "step in one launch (hla_attn_fwd_hilbert; on 2^k x 2^k grids, else as "
+                         "fused), the reordering fused into the attention after one index-and-lists "
+                         "launch (hla_attn_fwd_perm), or separate gather / attention / scatter "
+                         "calls; the others are reported beside it (composed-only: skip the fused "
+                         "steps)")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the per-configuration records (every measured workload's step, "
                          "attention kernel, gather / scatter kernels and rooflines) and the "
@@ -890,15 +949,29 @@ def main():
             bwd_fused = time_backward(fpipe, args.steps, args.warmup)
             print(f"[bench] {w.name} backward (fused): {json.dumps(bwd_fused)}", file=sys.stderr, flush=True)
         pipe = fpipe   # the algorithmic figures below depend on the workload only
+    # The whole step as one launch (index, lists and reordered attention inside
+    # hla_attn_fwd_hilbert), where the workload allows it.
+    res_single = None
+    if (isinstance(w, W.AttnWorkload) and single_ok(w) and args.step in ("single", "fused")
+            and res_fused is not None):
+        spipe = make_pipeline(w, hla, single=True)
+        res_single = summarize(spipe, run_timed(spipe, args.steps, args.warmup))
+        res_single["attn_kernel_ms"] = spipe.kernel_ms(max(args.steps, 20))
+        print(f"[bench] {w.name} (single launch): {json.dumps(res_single)}", file=sys.stderr, flush=True)
+        del spipe
+        torch.cuda.empty_cache()
     rpb = None
     if isinstance(w, W.AttnWorkload) and not args.no_rpb:
         rpb = time_rpb(pipe, args.steps, args.warmup)
         print(f"[bench] {w.name} with the position bias: {json.dumps(rpb)}", file=sys.stderr, flush=True)
     res_composed = res
-    if args.step == "fused" and res_fused:
+    if args.step == "single" and res_single:
+        res = res_single
+    elif args.step in ("single", "fused") and res_fused:
         res = res_fused
     ms = res["ms_per_step"]
-    attn_kernel = "attn_fwd_perm" if res is res_fused else "attn_fwd"
+    attn_kernel = ("attn_fwd_hilbert" if res is res_single else
+                   "attn_fwd_perm" if res is res_fused else "attn_fwd")
 
     compare = args.compare
     if compare is None and not args.copy_mib:
@@ -995,8 +1068,7 @@ def main():
         "step": ("Hilbert index and tile lists (one launch), QKV projection with the gather fused "
                  "in, attention, output projection with the scatter fused in"
                  if isinstance(w, W.LayerWorkload) else
-                 "Hilbert index and tile lists (one launch), attention with the reordering fused in "
-                 "(hla_attn_fwd_perm)" if attn_kernel == "attn_fwd_perm" else
+                 STEP_TEXT[attn_kernel] if attn_kernel != "attn_fwd" else
                  "Hilbert index and tile lists (one launch), gather of q/k/v, attention, scatter of out"
                  if getattr(getattr(w, "pattern", None), "hilbert", False) else
                  "tile lists, attention"),
@@ -1011,12 +1083,15 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
-    other = res_composed if res is res_fused else res_fused
-    if other:
-        line["composed_step" if other is res_composed else "fused_step"] = {
-            "ms_per_step": other["ms_per_step"], "ms_per_step_eager": other["ms_per_step_eager"],
-            "value": flops / (other["ms_per_step"] * 1e-3) / 1e12,
-            "attn_ms_per_call": other["attn_ms"], "stages_ms": other["stages_ms"]}
+    for key, other in (("single_step", res_single), ("fused_step", res_fused),
+                       ("composed_step", res_composed)):
+        if other and other is not res:
+            line[key] = {
+                "ms_per_step": other["ms_per_step"], "ms_per_step_eager": other["ms_per_step_eager"],
+                "value": flops / (other["ms_per_step"] * 1e-3) / 1e12,
+                "attn_ms_per_call": other["attn_ms"], "stages_ms": other["stages_ms"]}
+            if "attn_kernel_ms" in other:
+                line[key]["attn_kernel_ms"] = other["attn_kernel_ms"]
     if configs and w.name in configs and "perm" in configs[w.name]:
         pr = configs[w.name]["perm"]
         line["perm_gbs"].update({

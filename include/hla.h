@@ -235,6 +235,33 @@ hla_status hla_attn_fwd_perm(const void *q, const void *k, const void *v,
                              hla_stream_t stream);
 
 /*
+ * hla_attn_fwd_perm with the Hilbert index and the tile lists computed inside
+ * the kernel, so that the whole step of a Hilbert attention - curve, tile lists,
+ * reordered attention (Sec. 3.1-3.2; the reshape of Sec. 4.2 fused in) - is one
+ * launch with no metadata in memory. Every workgroup takes its rows' grid ids
+ * from the curve of the 2^k x 2^k grid (the order hla_hilbert_perm writes: 64
+ * consecutive positions from a multiple of 64 are one aligned 8 x 8 block of the
+ * curve) and classifies its row of tiles with hla_build_block_mask's classifier.
+ * q, k, v, out: bf16 [B, heads, N, d] in grid order, as hla_attn_fwd_perm.
+ * lse: as hla_attn_fwd_perm (may be NULL).
+ * pat: a Hilbert pattern (window, slide, neighborhood, shifted window) on a grid
+ * with H == W == 2^k >= 8; N must equal H * W. tile_m, tile_n, d: as
+ * hla_attn_fwd (128 x 64 or 64 x 64; d 32 or 64). The results equal
+ * hla_hilbert_perm -> hla_build_block_mask -> hla_attn_fwd_perm bit for bit.
+ * A workgroup serves one query tile for up to 8 consecutive (batch, head)
+ * slices, chosen by the library from the pattern's key span and the grid size;
+ * the environment variable HLA_HILBERT_HEADS_PER_WORKGROUP (1 .. 64) sets that
+ * number instead (read at every call; the results do not depend on it).
+ * Errors: HLA_ERR_UNSUPPORTED for other patterns, grids or dtypes (use
+ * hla_attn_fwd_perm with a precomputed order and mask); otherwise as
+ * hla_attn_fwd.
+ */
+hla_status hla_attn_fwd_hilbert(const void *q, const void *k, const void *v,
+                                const hla_pattern_desc *pat, int32_t tile_m, int32_t tile_n,
+                                void *out, float *lse, int64_t B, int64_t heads, int64_t N,
+                                int64_t d, hla_dtype dtype, float scale, hla_stream_t stream);
+
+/*
  * The attention forward with the global relative position bias of the Hilbert
  * Window Transformer (Sec. 3.2: the Swin window bias enlarged to the whole
  * feature map, because Hilbert windows have irregular shapes; Eq. 1 counts such

@@ -28,7 +28,8 @@ from typing import Optional, Tuple
 import torch
 
 __all__ = ["HLAError", "lib", "hilbert_perm", "gather", "scatter", "block_mask_dims",
-           "build_block_mask", "BlockMask", "attn_fwd", "attn_fwd_perm", "attn_fwd_rpb", "attn_bwd",
+           "build_block_mask", "BlockMask", "attn_fwd", "attn_fwd_perm", "attn_fwd_hilbert",
+           "attn_fwd_rpb", "attn_bwd",
            "attn_bwd_perm",
            "qkv_proj", "out_proj",
            "PATTERN_IDS", "LIB_PATH", "EXPORTED"]
@@ -49,7 +50,8 @@ HLA_OK, HLA_ERR_INVALID_ARG, HLA_ERR_UNSUPPORTED, HLA_ERR_HIP = 0, 1, 2, 3
 HLA_F32, HLA_BF16 = 0, 1
 
 EXPORTED = ("hla_hilbert_perm", "hla_gather", "hla_scatter", "hla_block_mask_dims",
-            "hla_build_block_mask", "hla_build_path_and_mask", "hla_attn_fwd", "hla_attn_fwd_perm", "hla_attn_fwd_rpb",
+            "hla_build_block_mask", "hla_build_path_and_mask", "hla_attn_fwd", "hla_attn_fwd_perm",
+            "hla_attn_fwd_hilbert", "hla_attn_fwd_rpb",
             "hla_attn_bwd", "hla_attn_bwd_perm", "hla_attn_bwd_noalloc",
             "hla_qkv_proj", "hla_out_proj", "hla_qkv_proj_perm", "hla_out_proj_perm",
             "hla_last_error", "hla_version")
@@ -107,6 +109,8 @@ def lib() -> ctypes.CDLL:
                              i64, i64, i64, i64, ctypes.c_int, f32, vp],
             "hla_attn_fwd_perm": [vp, vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp,
                                   i64, i64, i64, i64, ctypes.c_int, f32, vp],
+            "hla_attn_fwd_hilbert": [vp, vp, vp, ctypes.POINTER(PatternDesc), i32, i32, vp, vp,
+                                     i64, i64, i64, i64, ctypes.c_int, f32, vp],
             "hla_attn_fwd_rpb": [vp, vp, vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp,
                                  i64, i64, i64, i64, ctypes.c_int, f32, vp],
             "hla_attn_bwd": [vp, vp, vp, vp, vp, vp, ctypes.POINTER(BlockMaskStruct), vp, vp, vp,
@@ -363,6 +367,20 @@ def attn_fwd_perm(q, k, v, order, mask: BlockMask, scale: Optional[float] = None
     _check(lib().hla_attn_fwd_perm(_ptr(q), _ptr(k), _ptr(v), _ptr(order), ctypes.byref(mask.struct),
                                    _ptr(out), _ptr(lse), B, Hh, N, d, _dtype_code(q), scale,
                                    _stream(q)))
+    return out, lse
+
+
+def attn_fwd_hilbert(q, k, v, pattern, tile_m: int, tile_n: int, scale: Optional[float] = None,
+                     out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                     with_lse: bool = True):
+    """attn_fwd_perm with the Hilbert order and the tile lists computed inside the
+    kernel (hla_attn_fwd_hilbert): q, k, v in grid order, a Hilbert pattern on a
+    2^k x 2^k grid. Returns (out, lse or None), in grid order."""
+    B, Hh, N, d, scale, out, lse = _attn_fwd_args(q, k, v, scale, out, lse, with_lse)
+    desc = _pattern_desc(pattern)
+    _check(lib().hla_attn_fwd_hilbert(_ptr(q), _ptr(k), _ptr(v), ctypes.byref(desc), int(tile_m),
+                                      int(tile_n), _ptr(out), _ptr(lse), B, Hh, N, d, _dtype_code(q),
+                                      scale, _stream(q)))
     return out, lse
 
 

@@ -71,12 +71,17 @@
 // tiles: neighbouring tiles share key/value tiles (a window is two query tiles;
 // a band overlaps its neighbour almost entirely), and the reuse stays in one
 // XCD's L2.
+#include <algorithm>
+#include <cstdlib>
 #include <type_traits>
 
 #include "attn_common.h"
+#include "hilbert_common.h"
+#include "tiles_common.h"
 
 namespace hla {
 namespace {
+
 
 constexpr int BN = 64;
 constexpr float kRescaleSlack = 8.f;  // log2 units the softmax reference may lag the max
@@ -97,6 +102,10 @@ __device__ __forceinline__ float xhalf_sum(float x) { return x + __shfl_xor(x, 3
 
 // RPB: table entries a staged bias window may hold (per buffer).
 constexpr int kWinCap = 1024;
+
+// HIL: list entries whose curve blocks are tabulated in LDS by the prologue
+// (later entries, in rows with longer lists, walk the curve per tile).
+constexpr int kBlkTab = 256;
 
 // Bounding box {r_min, r_max, c_min, c_max} of the 64 lanes' grid cells (r, c <
 // 2^15), in every lane: both coordinates' min and max at once, as packed 16-bit
@@ -160,6 +169,7 @@ template <int D, int NW, int MODE>
 // the RPB mode's windows leave room for two workgroups per CU)
 __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) : (NW == 4 ? 3 : 2))
     attn_fwd_bf16(AttnArgs a) {
+  constexpr bool HIL = MODE == ATTN_HILBERT;
   constexpr bool GATHER = MODE == ATTN_GATHER;
   constexpr bool RPB = MODE == ATTN_RPB;
   constexpr bool IDX = GATHER || RPB;
@@ -188,7 +198,15 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
   constexpr int WINB = WINP + 4 * 16;
   constexpr int QBOX = WINB + 4 * BN * 4;
   constexpr int WIN = QBOX + NW * 16;
-  constexpr int LDSB = RPB ? WIN + 2 * kWinCap * 4 : IDX ? IDXK + 4 * BN * 4 : kStages * STAGE;
+  // HIL: the curve blocks of the first kBlkTab list entries, after the ring: the
+  // grid row of the block's origin cell (a multiple of 8) ORed with the state
+  // entering the block; then the row's runs (nf, ntot, t_lo, f_lo, f_hi).
+  constexpr int BLKT = kStages * STAGE;
+  constexpr int LDSB = RPB   ? WIN + 2 * kWinCap * 4
+                       : IDX ? IDXK + 4 * BN * 4
+                       : HIL ? BLKT + kBlkTab * 4 + 32
+                             : kStages * STAGE;
+  static_assert(!HIL || BN == 64, "a key tile must be one 8 x 8 block of the curve");
 
   __shared__ __attribute__((aligned(16))) char lds[LDSB];
   const int32_t *idx_q = reinterpret_cast<const int32_t *>(lds + IDXQ);
@@ -198,9 +216,12 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 31, half = lane >> 5;
 
+  // (HIL: a workgroup runs its query tile for a.hpw consecutive heads, the
+  // items, starting at head bh.)
   const int logical = xcd_remap(blockIdx.x, gridDim.x);
-  const int bh = logical / a.n_qtiles;
-  const int qt = logical - bh * a.n_qtiles;
+  const int grp = logical / a.n_qtiles;
+  const int qt = logical - grp * a.n_qtiles;
+  const int bh = HIL ? grp * a.hpw : grp;
   const int64_t slice = (int64_t)bh * a.N * D;
   const __bf16 *Q = static_cast<const __bf16 *>(a.q) + slice;
   const __bf16 *K = static_cast<const __bf16 *>(a.k) + slice;
@@ -215,10 +236,23 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
   const Region R = region_of<true>(P, qpos);
 
   // Tile lists, read through the scalar unit: the full tiles, then the partial.
-  const int nf = sload(a.n_full + qt), ntot = nf + sload(a.n_part + qt);
-  const int32_t *frow = a.full_idx + (int64_t)qt * a.n_ktiles;
-  const int32_t *prow = a.part_idx + (int64_t)qt * a.n_ktiles;
-  auto tile_of = [&](int i) { return i < nf ? sload(frow + i) : sload(prow + i - nf); };
+  // (HIL: set by the prologue.)
+  int nf = 0, ntot = 0, t_lo = 0, f_lo = 0, f_hi = -1;
+  if constexpr (!HIL) {
+    nf = sload(a.n_full + qt);
+    ntot = nf + sload(a.n_part + qt);
+  }
+  const int32_t *frow = HIL ? nullptr : a.full_idx + (int64_t)qt * a.n_ktiles;
+  const int32_t *prow = HIL ? nullptr : a.part_idx + (int64_t)qt * a.n_ktiles;
+  auto tile_of = [&](int i) {
+    if constexpr (HIL) {
+      if (i < nf) return f_lo + i;
+      const int j = i - nf, before = f_lo - t_lo;
+      return j < before ? t_lo + j : f_hi + 1 + (j - before);
+    } else {
+      return i < nf ? sload(frow + i) : sload(prow + i - nf);
+    }
+  };
 
   // Per-thread source offsets (elements, within a tile) of this thread's K and V
   // chunk copies: LDS slot p = (j*NW + wave)*64 + lane holds row p / CPR, chunk
@@ -246,9 +280,33 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
     kin[j] = (uint32_t)(krow[j] * D + kch[j]) * 2u;
     vin[j] = (uint32_t)(krow[j] * D + vch[j]) * 2u;
   }
-  auto issue_tile = [&](int i, int stage) {
+  // HIL: key tile t is the curve's block t, and a copy's tile row is its
+  // position in the block. Blocks entered in different states are transposes
+  // and mirrors of one another, so each copy's byte offset from the block's
+  // origin row is hA0 (state 0) or hA1 (transposed), with the K chunk in its low
+  // bits, XORed with a uniform constant when the block is mirrored (both cell
+  // coordinates XOR 7); the V chunk's offset differs from the K chunk's by the
+  // XOR hX. Lane l also holds the local cells of local position l in a block
+  // entered in state 0 (bits 0-5) and in a transposed one (bits 6-11), for the
+  // lookups of the prologue.
+  uint32_t hA0[CPW], hA1[CPW], hX[CPW];
+  int e_lane = 0;
+  if constexpr (HIL) {
+    const uint32_t c0 = hilbert_local_walk((uint32_t)lane, 0);
+    e_lane = (int)(c0 | hilbert_local_state(c0, 1) << 6);
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) {
+      const uint32_t e = (uint32_t)__shfl(e_lane, krow[j]), c0 = e & 63u, c1 = e >> 6;
+      const uint32_t kb = (uint32_t)kch[j] * 2u;
+      hA0[j] = ((c0 >> 3) << a.lg | (c0 & 7u)) * (uint32_t)(D * 2) + kb;
+      hA1[j] = ((c1 >> 3) << a.lg | (c1 & 7u)) * (uint32_t)(D * 2) + kb;
+      hX[j] = kb ^ ((uint32_t)vch[j] * 2u);
+    }
+  }
+  // (ioff: elements from this workgroup's first slice to the item's.)
+  auto issue_tile = [&](int i, int stage, int64_t ioff = 0) {
     char *base = lds + stage * STAGE;
-    const __bf16 *Kt = K, *Vt = V;
+    const __bf16 *Kt = K + ioff, *Vt = V + ioff;
     uint32_t ko[CPW], vo[CPW];
     if constexpr (GATHER) {
       const int32_t *rows = idx_k(i);
@@ -257,6 +315,25 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
         const uint32_t r = (uint32_t)rows[krow[j]] * (uint32_t)(D * 2);
         ko[j] = r + (uint32_t)kch[j] * 2u;
         vo[j] = r + (uint32_t)vch[j] * 2u;
+      }
+    } else if constexpr (HIL) {
+      // the block's origin row and entry state (uniform), into the slice base
+      uint32_t ent;
+      if (i < kBlkTab) {
+        ent = __builtin_amdgcn_readfirstlane(reinterpret_cast<const uint32_t *>(lds + BLKT)[i]);
+      } else {
+        uint32_t bx, by, bst;
+        hilbert_block((uint32_t)tile_of(i), a.lg, bx, by, bst);
+        ent = (by << a.lg | bx) | bst;
+      }
+      Kt += (int64_t)(ent & ~3u) * D;
+      Vt += (int64_t)(ent & ~3u) * D;
+      const uint32_t mirror = (ent & 2u) ? (7u << a.lg | 7u) * (uint32_t)(D * 2) : 0u;
+      const bool transposed = (ent & 1u) != 0;
+#pragma unroll
+      for (int j = 0; j < CPW; ++j) {
+        ko[j] = (transposed ? hA1[j] : hA0[j]) ^ mirror;
+        vo[j] = ko[j] ^ hX[j];
       }
     } else {
       const int k0 = tile_of(i) * BN;
@@ -335,7 +412,132 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
   // keeps every global load of the kernel a tracked ring copy: a Q operand
   // loaded straight into registers would make the compiler wait for all copies
   // in flight before its first use in the loop.
-  if constexpr (GATHER) {
+  // HIL: wave 0 classifies this row's candidate key tiles (the key positions
+  // any query of the tile may attend, per pattern) with the list builder's
+  // classifier, one tile per lane. For the 1-D patterns the non-empty tiles of a
+  // row are one run [t_lo, t_hi] and the full ones one run [f_lo, f_hi] inside
+  // it, so the lists are "f_lo .. f_hi, then t_lo .. f_lo - 1, then f_hi + 1 ..
+  // t_hi" (ascending within each, as the builder writes them); should a row
+  // ever not have that shape, every tile of [t_lo, t_hi] runs masked instead.
+  // It tabulates the curve blocks of the first list entries and hands the runs
+  // to the other waves through LDS. Meanwhile every wave finds the row of its
+  // own query (the output row).
+  // HIL: the query tile's curve blocks (uniform) and the row of a position of
+  // it in block c of the tile (c uniform; its local cell a cross-lane read).
+  constexpr int QBLK = BM / 64;
+  uint32_t bx[QBLK], by[QBLK], bst[QBLK];
+  // (a tile reaching past the sequence, N = 64 < BM: its positions past the
+  // end read the last row)
+  int cmax = 0;
+  if constexpr (HIL) {
+    const uint32_t b0 = (uint32_t)(qt * BM) >> 6;
+#pragma unroll
+    for (int c = 0; c < QBLK; ++c) hilbert_block(b0 + c, a.lg, bx[c], by[c], bst[c]);
+    cmax = ((a.N - 1) >> 6) - (int)b0;
+  }
+  auto row_in = [&](int c, int pos) {
+    const int cc = min(c, cmax);
+    uint32_t x = bx[0], y = by[0], st = bst[0];
+#pragma unroll
+    for (int k = 1; k < QBLK; ++k)
+      if (cc == k) {
+        x = bx[k];
+        y = by[k];
+        st = bst[k];
+      }
+    const uint32_t e = (uint32_t)__shfl(e_lane, min(pos, a.N - 1) & 63);
+    const uint32_t cell = ((e >> (6 * (st & 1u))) & 63u) ^ ((st & 2u) ? 63u : 0u);
+    return hilbert_block_row(x, y, cell, a.lg);
+  };
+  uint32_t my_row = 0;
+  uint32_t qoff[LQ];
+  if constexpr (HIL) {
+    uint32_t *blkt = reinterpret_cast<uint32_t *>(lds + BLKT);
+    int32_t *runs = reinterpret_cast<int32_t *>(lds + BLKT + kBlkTab * 4);
+    if (wave == 0) {
+      // candidate range (64-bit: window ends may pass 2^31 for parameters
+      // near 2^30; the group quotients fit 32 bits)
+      const int64_t i0 = (int64_t)qt * BM, i1 = min(i0 + BM - 1, (int64_t)P.N - 1);
+      const int64_t w = P.p0;
+      int64_t lo = 0, hi = P.N - 1;
+      if (P.kind == HLA_HILBERT_WINDOW || P.kind == HLA_HILBERT_SHIFTED_WINDOW) {
+        const uint32_t off = P.kind == HLA_HILBERT_WINDOW ? 0u : (uint32_t)(P.p0 - P.p1);
+        const uint32_t ga = ((uint32_t)i0 + off) / (uint32_t)w, gb = ((uint32_t)i1 + off) / (uint32_t)w;
+        lo = (int64_t)ga * w - off;
+        hi = (int64_t)gb * w + w - 1 - off;
+      } else if (P.kind == HLA_HILBERT_SLIDE) {
+        lo = i0 - w;
+        hi = i1 + w;
+      } else if (P.kind == HLA_HILBERT_NEIGHBORHOOD) {
+        lo = min(max(i0 - w / 2, (int64_t)0), (int64_t)P.N - w);
+        hi = min(max(i1 - w / 2, (int64_t)0), (int64_t)P.N - w) + w - 1;
+      }
+      const int c_lo = (int)(max(lo, (int64_t)0) / BN), c_hi = (int)(min(hi, (int64_t)P.N - 1) / BN);
+      int n_any = 0, n_full = 0, tl = 0x7fffffff, th = -1, fl = 0x7fffffff, fh = -1;
+      for (int c0 = c_lo; c0 <= c_hi; c0 += 64) {
+        const int kt = c0 + lane;
+        const int cls = kt <= c_hi ? tile_class<true>(P, BM, BN, qt, kt) : 0;
+        const uint64_t ba = __ballot(cls != 0), bf = __ballot(cls == 2);
+        if (ba) {
+          tl = min(tl, c0 + (int)__builtin_ctzll(ba));
+          th = c0 + 63 - (int)__builtin_clzll(ba);
+          n_any += __popcll(ba);
+        }
+        if (bf) {
+          fl = min(fl, c0 + (int)__builtin_ctzll(bf));
+          fh = c0 + 63 - (int)__builtin_clzll(bf);
+          n_full += __popcll(bf);
+        }
+      }
+      const bool one_run = n_any == th - tl + 1 && (n_full == 0 || n_full == fh - fl + 1);
+      if (n_any > 0) {
+        t_lo = tl;
+        ntot = one_run ? n_any : th - tl + 1;
+        if (one_run && n_full > 0) {
+          nf = n_full;
+          f_lo = fl;
+          f_hi = fh;
+        } else {
+          f_lo = tl;
+          f_hi = tl - 1;
+        }
+      }
+      nf = __builtin_amdgcn_readfirstlane(nf);
+      ntot = __builtin_amdgcn_readfirstlane(ntot);
+      t_lo = __builtin_amdgcn_readfirstlane(t_lo);
+      f_lo = __builtin_amdgcn_readfirstlane(f_lo);
+      f_hi = __builtin_amdgcn_readfirstlane(f_hi);
+      // the block table: origin row | entry state of each list entry's block
+      for (int e = lane; e < min(ntot, kBlkTab); e += 64) {
+        uint32_t x, y, st;
+        hilbert_block((uint32_t)tile_of(e), a.lg, x, y, st);
+        blkt[e] = (y << a.lg | x) | st;
+      }
+      if (lane == 0) {
+        runs[0] = nf;
+        runs[1] = ntot;
+        runs[2] = t_lo;
+        runs[3] = f_lo;
+        runs[4] = f_hi;
+      }
+    }
+    my_row = row_in(wave / 2, qpos);
+    // (a copy's tile row lies in block (j * NW + wave) / CPR: it is a whole
+    // multiple of 64 / CPR rows past the wave's first)
+#pragma unroll
+    for (int j = 0; j < LQ; ++j) {
+      const int p = (j * NW + wave) * 64 + lane;
+      const int r = p / CPR, cs = p % CPR;
+      qoff[j] = row_in((j * NW + wave) / CPR, qt * BM + r) * (uint32_t)(D * 2) +
+                (uint32_t)(cs ^ swz_q<D>(r)) * 16u;
+    }
+    wait_then_barrier<0>();
+    nf = __builtin_amdgcn_readfirstlane(runs[0]);
+    ntot = __builtin_amdgcn_readfirstlane(runs[1]);
+    t_lo = __builtin_amdgcn_readfirstlane(runs[2]);
+    f_lo = __builtin_amdgcn_readfirstlane(runs[3]);
+    f_hi = __builtin_amdgcn_readfirstlane(runs[4]);
+  } else if constexpr (GATHER) {
     // Row indices of the Q tile and of the first three key tiles, first.
     if (wave == 0) {
 #pragma unroll
@@ -347,24 +549,33 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
       if (i < ntot) issue_idx(i);
     wait_then_barrier<0>();
   }
-  {
-    char *base = lds + 2 * STAGE;
+  // The Q tile's copies (Qs: the item's slice) into ring stage stg.
+  // (HIL: from the slice base plus the copies' byte offsets qoff, found once.)
+  auto issue_q = [&](const __bf16 *Qs, int stg) {
+    char *base = lds + stg * STAGE;
 #pragma unroll
     for (int j = 0; j < LQ; ++j) {
-      const int p = (j * NW + wave) * 64 + lane;
-      const int r = p / CPR, cs = p % CPR;
-      const int64_t row = GATHER ? (int64_t)idx_q[r] : (int64_t)min(qt * BM + r, a.N - 1);
-      lds_dma16(Q + row * D + (cs ^ swz_q<D>(r)) * 8, lds_addr(base + (j * NW + wave) * 1024));
+      if constexpr (HIL) {
+        lds_dma16_at(Qs, qoff[j], lds_addr(base + (j * NW + wave) * 1024));
+      } else {
+        const int p = (j * NW + wave) * 64 + lane;
+        const int r = p / CPR, cs = p % CPR;
+        const int64_t row = GATHER ? (int64_t)idx_q[r] : (int64_t)min(qt * BM + r, a.N - 1);
+        lds_dma16(Qs + row * D + (cs ^ swz_q<D>(r)) * 8, lds_addr(base + (j * NW + wave) * 1024));
+      }
     }
-  }
-  if constexpr (RPB) {
-    if (ntot > 0) issue_idx(0);
-    if (ntot > 1) issue_idx(1);
-  }
-  if (ntot > 0) issue_tile(0, 0);
-  if (ntot > 1) issue_tile(1, 1);
-  if constexpr (RPB) {
-    if (ntot > 2) issue_idx(2);
+  };
+  if constexpr (!HIL) {
+    issue_q(Q, 2);
+    if constexpr (RPB) {
+      if (ntot > 0) issue_idx(0);
+      if (ntot > 1) issue_idx(1);
+    }
+    if (ntot > 0) issue_tile(0, 0);
+    if (ntot > 1) issue_tile(1, 1);
+    if constexpr (RPB) {
+      if (ntot > 2) issue_idx(2);
+    }
   }
   // RPB: this lane's query cell (rq, cq) and bias base C + off(q), loaded after
   // the copies; one wait the compiler sees then covers it and them. Then the
@@ -391,19 +602,21 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
     qr1 = __builtin_amdgcn_readfirstlane(box.y);
     qc0 = __builtin_amdgcn_readfirstlane(box.z);
     qc1 = __builtin_amdgcn_readfirstlane(box.w);
-  } else {
+  } else if constexpr (!HIL) {
     // Q and the first key tile are in; the second may still be in flight.
     if (ntot > 1) wait_then_barrier<LPT>();
     else wait_then_barrier<0>();
   }
+  // This lane's Q operand, from the Q tile in ring stage stg.
   bf16x8 qop[NCH];
-  {
+  auto load_q = [&](int stg) {
     const int r = wave * 32 + col;
 #pragma unroll
     for (int c = 0; c < NCH; ++c)
-      qop[c] = *reinterpret_cast<const bf16x8 *>(lds + 2 * STAGE + r * D * 2 +
+      qop[c] = *reinterpret_cast<const bf16x8 *>(lds + stg * STAGE + r * D * 2 +
                                                  (((half * NCH + c) ^ swz_q<D>(r)) * 16));
-  }
+  };
+  if constexpr (!HIL) load_q(2);
 
   // RPB: the bias window of list entry j, issued by one wave: the table entries
   // that this workgroup's queries and entry j's keys can address - the rectangle
@@ -448,33 +661,9 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
     wait_then_barrier<0>();
   }
 
-  // One key tile: wait for its copies, refill the ring, then S^T, (mask),
-  // online softmax and O^T += V^T P^T. MASKED is a compile-time flag, so full
-  // and partial tiles run separate loop bodies and the unmasked path carries no
-  // mask code at all.
-  int stage = 0;
-  auto step = [&](int it, auto masked) {
-    // Wait for this wave's copies of tile `it`; the copies of tile it + 1 (the
-    // only one issued after it) may stay in flight.
-    // RPB: after tile it's window come tile it + 1's copies and entry it + 2's
-    // indices.
-    if (RPB && it + 2 < ntot) wait_then_barrier<LPT + 1>();
-    else if (it + 1 < ntot) wait_then_barrier<LPT>();
-    else wait_then_barrier<0>();
-    // The stage refilled next was last read in iteration it - 1, which every
-    // wave has finished (it is behind the barrier above).
-    const int nstage = stage == 0 ? 2 : stage - 1;  // (it + 2) % 3
-    // (GATHER: the indices of entry it + 2 arrived with the wait above, those of
-    // it + 3 go out first.)
-    if constexpr (GATHER) {
-      if (it + 3 < ntot) issue_idx(it + 3);
-    }
-    if constexpr (!RPB) {
-      if (it + 2 < ntot) issue_tile(it + 2, nstage);
-    }
-    const char *st = lds + stage * STAGE;
-    stage = stage == 2 ? 0 : stage + 1;
-
+  // The math of one key tile staged at st (list entry it): S^T, (mask), online
+  // softmax and O^T += V^T P^T.
+  auto tile_math = [&](const char *st, int it, auto masked) {
     // S^T for the two 32-key blocks (independent accumulators interleaved), the
     // RPB bias and the mask: the tile's scores, this lane's 32 of them.
     auto scores = [&](f32x16 (&s)[2]) {
@@ -622,6 +811,36 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
         const bf16x8 vop = lds_read_tr16x2(st + vbase[db] + (16 * t) * D * 2, D * 2);
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[t], oacc[db], 0, 0, 0);
       }
+  };
+
+  // One key tile: wait for its copies, refill the ring, then S^T, (mask),
+  // online softmax and O^T += V^T P^T. MASKED is a compile-time flag, so full
+  // and partial tiles run separate loop bodies and the unmasked path carries no
+  // mask code at all.
+  int stage = 0;
+  auto step = [&](int it, auto masked) {
+    // Wait for this wave's copies of tile `it`; the copies of tile it + 1 (the
+    // only one issued after it) may stay in flight.
+    // RPB: after tile it's window come tile it + 1's copies and entry it + 2's
+    // indices.
+    if (RPB && it + 2 < ntot) wait_then_barrier<LPT + 1>();
+    else if (it + 1 < ntot) wait_then_barrier<LPT>();
+    else wait_then_barrier<0>();
+    // The stage refilled next was last read in iteration it - 1, which every
+    // wave has finished (it is behind the barrier above).
+    const int nstage = stage == 0 ? 2 : stage - 1;  // (it + 2) % 3
+    // (GATHER: the indices of entry it + 2 arrived with the wait above, those of
+    // it + 3 go out first.)
+    if constexpr (GATHER) {
+      if (it + 3 < ntot) issue_idx(it + 3);
+    }
+    if constexpr (!RPB) {
+      if (it + 2 < ntot) issue_tile(it + 2, nstage);
+    }
+    const char *st = lds + stage * STAGE;
+    stage = stage == 2 ? 0 : stage + 1;
+
+    tile_math(st, it, masked);
     // RPB: at the end of the step, entry it + 1's window (its indices arrived
     // before this step's barrier), then the ring refill (stage (it + 2) % 3 held
     // tile it - 1, which every wave finished before this step's barrier), then
@@ -632,52 +851,165 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
       if (it + 3 < ntot) issue_idx(it + 3);
     }
   };
-  for (int it = 0; it < nf; ++it) step(it, std::false_type{});
-  for (int it = nf; it < ntot; ++it) step(it, std::true_type{});
-
   // Epilogue: normalise and store the rows straight from the accumulators. Lane
   // (col, half) holds, per d block and 8-row group a, the four values
   // d = 8a + 4half + 0..3 of query col; one exchange with lane col ^ 32 per pair
   // of groups gives each lane eight consecutive values (16 bytes) to store.
-  const float l_tot = xhalf_sum(l_run);
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  // (queries past the end of the sequence, in a ragged last query tile, take part
-  // in the exchanges but store nothing)
-  const bool live = qpos < a.N;
-  const int64_t out_row = GATHER ? (int64_t)idx_q[wave * 32 + col] : (int64_t)qpos;
-  __bf16 *orow = static_cast<__bf16 *>(a.out) + slice + out_row * D;
-#pragma unroll
-  for (int db = 0; db < NDB; ++db)
-#pragma unroll
-    for (int pr = 0; pr < 2; ++pr) {
-      bf16x4 x0, x1;
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        x0[b] = (__bf16)(oacc[db][8 * pr + b] * inv);
-        x1[b] = (__bf16)(oacc[db][8 * pr + 4 + b] * inv);
+  // (sl: the item's slice, bhh: its head index)
+  auto store_rows = [&](int64_t sl, int bhh) {
+    const float l_tot = xhalf_sum(l_run);
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    // (queries past the end of the sequence, in a ragged last query tile, take part
+    // in the exchanges but store nothing)
+    const bool live = qpos < a.N;
+    const int64_t out_row = GATHER ? (int64_t)idx_q[wave * 32 + col] : HIL ? (int64_t)my_row : (int64_t)qpos;
+    __bf16 *orow = static_cast<__bf16 *>(a.out) + sl + out_row * D;
+  #pragma unroll
+    for (int db = 0; db < NDB; ++db)
+  #pragma unroll
+      for (int pr = 0; pr < 2; ++pr) {
+        bf16x4 x0, x1;
+  #pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          x0[b] = (__bf16)(oacc[db][8 * pr + b] * inv);
+          x1[b] = (__bf16)(oacc[db][8 * pr + 4 + b] * inv);
+        }
+        const uint2 u0 = __builtin_bit_cast(uint2, x0), u1 = __builtin_bit_cast(uint2, x1);
+        // half 0 keeps group 2pr and receives the partner's part of it; half 1
+        // keeps group 2pr + 1 and receives the partner's part of that.
+        const uint2 send = half ? u0 : u1;
+        uint2 recv;
+        recv.x = __shfl_xor(send.x, 32);
+        recv.y = __shfl_xor(send.y, 32);
+        const uint4 row = half ? uint4{recv.x, recv.y, u1.x, u1.y} : uint4{u0.x, u0.y, recv.x, recv.y};
+        if (live) *reinterpret_cast<uint4 *>(orow + db * 32 + 16 * pr + 8 * half) = row;
       }
-      const uint2 u0 = __builtin_bit_cast(uint2, x0), u1 = __builtin_bit_cast(uint2, x1);
-      // half 0 keeps group 2pr and receives the partner's part of it; half 1
-      // keeps group 2pr + 1 and receives the partner's part of that.
-      const uint2 send = half ? u0 : u1;
-      uint2 recv;
-      recv.x = __shfl_xor(send.x, 32);
-      recv.y = __shfl_xor(send.y, 32);
-      const uint4 row = half ? uint4{recv.x, recv.y, u1.x, u1.y} : uint4{u0.x, u0.y, recv.x, recv.y};
-      if (live) *reinterpret_cast<uint4 *>(orow + db * 32 + 16 * pr + 8 * half) = row;
+    if (a.lse && half == 0 && live) {
+      const float ln2 = 0.69314718055994530942f;
+      a.lse[(int64_t)bhh * a.N + out_row] =
+          l_tot > 0.f ? (m_run + __builtin_amdgcn_logf(l_tot)) * ln2 : -__builtin_inff();
     }
-  if (a.lse && half == 0 && live) {
-    const float ln2 = 0.69314718055994530942f;
-    a.lse[(int64_t)bh * a.N + out_row] =
-        l_tot > 0.f ? (m_run + __builtin_amdgcn_logf(l_tot)) * ln2 : -__builtin_inff();
+  };
+
+  if constexpr (HIL) {
+    // The items as one stream of ring copies: item h's Q tile, then its list's
+    // key tiles, then item h + 1's. Element e goes into stage e % 3 once every
+    // wave has read element e - 3, so the next item's Q tile and first key tile
+    // are copied during the current item's last two tiles, and the workgroup's
+    // classification, block table and rows serve every item. The previous
+    // item's rows are stored after the next item's first wait, so that wait
+    // never waits for stores.
+    const int nitems = min(a.hpw, a.BH - bh);
+    const int64_t ND = (int64_t)a.N * D;
+    if (ntot == 0) {
+      for (int h = 0; h < nitems; ++h) store_rows(slice + h * ND, bh + h);
+      return;
+    }
+    // Element e + 2 goes out when element e is read: in stage (s + 2) % 3 for
+    // the element read from stage s. Within an item that is its entry it + 2;
+    // the item's last two entries hand over to the next item's Q tile and its
+    // entry 0.
+    issue_q(Q, 0);
+    issue_tile(0, 1);
+    if (ntot > 1) issue_tile(1, 2);
+    else if (nitems > 1) issue_q(Q + ND, 2);
+    int h = 0, cstage = 0;  // item, stage of the element read next
+    int64_t ioff = 0;       // elements from the first item's slice to item h's
+    // List entry it of item h: wait for its copies (the one element issued
+    // after it may stay in flight: the item's next entry, or the next item's
+    // Q tile), refill the ring, the math.
+    auto hil_step = [&](int it, auto masked) {
+      const int nst = cstage == 0 ? 2 : cstage - 1;
+      if (it + 2 < ntot) {
+        if (h > 0 && it == 0) wait_then_barrier<63>();  // entry 0 arrived before the item began
+        else wait_then_barrier<LPT>();
+        issue_tile(it + 2, nst, ioff);
+      } else {
+        if (h > 0 && it == 0) wait_then_barrier<63>();
+        else if (it + 1 < ntot) wait_then_barrier<LPT>();
+        else if (h + 1 < nitems) wait_then_barrier<LQ>();
+        else wait_then_barrier<0>();
+        if (h + 1 < nitems) {
+          if (it + 2 == ntot) issue_q(Q + ioff + ND, nst);
+          else issue_tile(0, nst, ioff + ND);
+        }
+      }
+      const char *st = lds + cstage * STAGE;
+      cstage = cstage == 2 ? 0 : cstage + 1;
+      tile_math(st, it, masked);
+    };
+    for (h = 0; h < nitems; ++h, ioff += ND) {
+      // the item's Q tile and list entry 0 are in (at the first item the
+      // third element may still be in flight; later, nothing was issued after
+      // them); then the stage of the previous item's last entry takes the
+      // element after the item's entry 0
+      if (h == 0) {
+        if (ntot > 1) wait_then_barrier<LPT>();
+        else if (nitems > 1) wait_then_barrier<LQ>();
+        else wait_then_barrier<0>();
+      } else {
+        wait_then_barrier<0>();
+        const int nst = cstage == 0 ? 2 : cstage - 1;
+        if (ntot > 1) issue_tile(1, nst, ioff);
+        else if (h + 1 < nitems) issue_q(Q + ioff + ND, nst);
+      }
+      if (h > 0) {
+        store_rows(slice + ioff - ND, bh + h - 1);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) oacc[db] = f32x16{};
+        m_run = -__builtin_inff();
+        l_run = 0.f;
+        primed = false;
+      }
+      load_q(cstage);
+      cstage = cstage == 2 ? 0 : cstage + 1;
+      for (int it = 0; it < nf; ++it) hil_step(it, std::false_type{});
+      for (int it = nf; it < ntot; ++it) hil_step(it, std::true_type{});
+    }
+    store_rows(slice + (nitems - 1) * ND, bh + nitems - 1);
+  } else {
+    for (int it = 0; it < nf; ++it) step(it, std::false_type{});
+    for (int it = nf; it < ntot; ++it) step(it, std::true_type{});
+    store_rows(slice, bh);
   }
 }
 
+// Heads per workgroup of the one-launch path. A workgroup's set-up (the tile
+// classification, the block table and rows, the first copies' latency) is paid
+// once for all its heads, while long workgroups lengthen the tail of the grid:
+// aim at about kHeadsWork key tiles per workgroup (the row's key span in tiles
+// from the pattern), at most 8 heads, and keep at least two workgroups per CU.
+// HLA_HILBERT_HEADS_PER_WORKGROUP (1 .. 64) overrides it.
+constexpr int kHeadsWork = 40;
+int heads_per_workgroup(const AttnArgs &a, int BM) {
+  if (const char *env = std::getenv("HLA_HILBERT_HEADS_PER_WORKGROUP")) {
+    const int h = std::atoi(env);
+    if (h >= 1 && h <= 64) return h;
+  }
+  static int cus = 0;
+  if (!cus) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+      cus = 256;
+  }
+  const int64_t span = a.pat.kind == HLA_HILBERT_SLIDE ? 2 * (int64_t)a.pat.p0 + 1 : (int64_t)a.pat.p0;
+  const int64_t tiles = (std::min<int64_t>(span, a.N) + BM + BN - 1) / BN;
+  int h = (int)std::max<int64_t>(1, std::min<int64_t>(8, kHeadsWork / tiles));
+  h = std::min(h, a.BH);
+  while (h > 1 && (int64_t)((a.BH + h - 1) / h) * a.n_qtiles < 2 * (int64_t)cus) --h;
+  return h;
+}
+
 template <int D, int NW>
-hipError_t launch(const AttnArgs &a, hipStream_t s) {
-  const int64_t blocks = (int64_t)a.BH * a.n_qtiles;
+hipError_t launch(const AttnArgs &a_in, hipStream_t s) {
+  AttnArgs a = a_in;
+  a.hpw = a.mode == ATTN_HILBERT ? heads_per_workgroup(a, 32 * NW) : 1;
+  const int64_t blocks = (int64_t)((a.BH + a.hpw - 1) / a.hpw) * a.n_qtiles;
   if (a.mode == ATTN_GATHER)
     hipLaunchKernelGGL((attn_fwd_bf16<D, NW, ATTN_GATHER>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
+  else if (a.mode == ATTN_HILBERT)
+    hipLaunchKernelGGL((attn_fwd_bf16<D, NW, ATTN_HILBERT>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
   else if (a.mode == ATTN_RPB)
     hipLaunchKernelGGL((attn_fwd_bf16<D, NW, ATTN_RPB>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
   else

@@ -168,6 +168,58 @@ constexpr HilbertLut make_hilbert_lut() {
   return t;
 }
 
+// ---------------------------------------------------------------------------
+// Level-3 blocks: on a curve of side >= 8, the 64 positions 64b .. 64b + 63 are
+// one aligned 8 x 8 sub-square, whose cells the curve visits in the order of the
+// 3-level curve from the orientation state s entering the block. So the cell of
+// position p is the block's origin plus a local cell that depends only on
+// (p mod 64, s).
+// The local cell (lx | ly << 3) of local position p < 64 in a block entered in
+// state st = sw | fl << 1.
+constexpr uint32_t hilbert_local_walk(uint32_t p, uint32_t st) {
+  uint32_t sw = st & 1u, fl = st >> 1, x = 0, y = 0;
+  for (int l = 2; l >= 0; --l) {
+    const uint32_t q = (p >> (2 * l)) & 3u;
+    const uint32_t a = q >> 1, b = (q ^ a) & 1u, tt = ((a ^ b) & sw) ^ fl;
+    x |= (a ^ tt) << l;
+    y |= (b ^ tt) << l;
+    sw ^= turn_sw(q);
+    fl ^= turn_fl(q);
+  }
+  return x | y << 3;
+}
+
+// Entering a block in another state only transposes it (sw) and mirrors both
+// coordinates (fl): the local cell for state st from the one for state 0.
+constexpr uint32_t hilbert_local_state(uint32_t c0, uint32_t st) {
+  const uint32_t c = (st & 1u) ? ((c0 & 7u) << 3 | c0 >> 3) : c0;
+  return (st & 2u) ? c ^ 63u : c;
+}
+
+constexpr bool hilbert_local_states_agree() {
+  for (uint32_t p = 0; p < 64; ++p)
+    for (uint32_t st = 0; st < 4; ++st)
+      if (hilbert_local_state(hilbert_local_walk(p, 0), st) != hilbert_local_walk(p, st)) return false;
+  return true;
+}
+static_assert(hilbert_local_states_agree(), "block orientations are transposes and mirrors");
+
+// Block b of the 2^lg square (lg >= 3): the cell origin (x, y: bits 3 and up)
+// and the state entering the block.
+__device__ __forceinline__ void hilbert_block(uint32_t b, int lg, uint32_t &x, uint32_t &y,
+                                              uint32_t &st) {
+  uint32_t sw = 0, fl = 0;
+  x = y = 0;
+  d2xy_levels(b << 6, lg, 3, x, y, sw, fl);
+  st = sw | fl << 1;
+}
+
+// The grid row of a cell given its block origin and its local cell.
+__device__ __forceinline__ uint32_t hilbert_block_row(uint32_t bx, uint32_t by, uint32_t cell,
+                                                      int lg) {
+  return (by | (cell >> 3)) << lg | (bx | (cell & 7u));
+}
+
 // Block b of the job with the tables in LDS. A walk of nl levels starts at the
 // top of ceil(nl / 4) groups: the padding levels above the curve have digit 0
 // and coordinate bits 0, and each of them only toggles sw, so the walk starts

@@ -308,11 +308,13 @@ namespace {
 
 // Checks shared by the attention passes: the mask, sizes, dtype, scale and the
 // supported shapes. Pointers are checked by the callers.
+// (need_lists = false: the kernel classifies its own tiles, so the mask's arrays
+// are not read.)
 hla_status check_attn(const hla_block_mask *mask, int64_t B, int64_t heads, int64_t N,
-                      int64_t d, hla_dtype dtype, float scale) {
+                      int64_t d, hla_dtype dtype, float scale, bool need_lists = true) {
   hla_status st;
   if (!mask) return fail(HLA_ERR_INVALID_ARG, "mask is NULL");
-  if (!mask->n_full || !mask->full_idx || !mask->n_part || !mask->part_idx)
+  if (need_lists && (!mask->n_full || !mask->full_idx || !mask->n_part || !mask->part_idx))
     return fail(HLA_ERR_INVALID_ARG, "mask arrays are NULL (build the mask first)");
   if (B <= 0 || heads <= 0 || N <= 0 || d <= 0)
     return fail(HLA_ERR_INVALID_ARG, "sizes must be positive");
@@ -349,7 +351,8 @@ static hla_status attn_fwd(const void *q, const void *k, const void *v, const in
   if ((st = check_tensor_args(v, "v")) != HLA_OK) return st;
   if ((st = check_tensor_args(out, "out")) != HLA_OK) return st;
   if (lse && !aligned(lse, 4)) return fail(HLA_ERR_INVALID_ARG, "lse is not 4-byte aligned");
-  if ((st = check_attn(mask, B, heads, N, d, dtype, scale)) != HLA_OK) return st;
+  if ((st = check_attn(mask, B, heads, N, d, dtype, scale, mode != hla::ATTN_HILBERT)) != HLA_OK)
+    return st;
   const int64_t BH = B * heads;
   const int64_t bytes = BH * N * d * dtype_size(dtype);
   for (const void *in : {q, k, v})
@@ -377,6 +380,9 @@ static hla_status attn_fwd(const void *q, const void *k, const void *v, const in
   a.scale = scale;
   a.scale_log2 = (float)((double)scale * 1.4426950408889634074);
   a.pat = hla::make_pattern_args(mask->pat);
+  a.lg = 0;
+  a.hpw = 1;
+  while ((1 << a.lg) < mask->pat.W) ++a.lg;
   hipError_t e = dtype == HLA_BF16
                      ? hla::launch_attn_bf16(a, (int)d, mask->tile_m, mask->tile_n, (hipStream_t)stream)
                      : hla::launch_attn_f32(a, (int)d, mask->tile_m, mask->tile_n, (hipStream_t)stream);
@@ -401,6 +407,34 @@ hla_status hla_attn_fwd_perm(const void *q, const void *k, const void *v, const 
       return fail(HLA_ERR_INVALID_ARG, "order overlaps a tensor");
   return attn_fwd(q, k, v, order, nullptr, hla::ATTN_GATHER, mask, out, lse, B, heads, N, d,
                   dtype, scale, stream, "hla_attn_fwd_perm");
+}
+
+hla_status hla_attn_fwd_hilbert(const void *q, const void *k, const void *v,
+                                const hla_pattern_desc *pat, int32_t tile_m, int32_t tile_n,
+                                void *out, float *lse, int64_t B, int64_t heads, int64_t N,
+                                int64_t d, hla_dtype dtype, float scale, hla_stream_t stream) {
+  hla_status st;
+  if (!pat) return fail(HLA_ERR_INVALID_ARG, "pat is NULL");
+  if ((st = check_pattern(pat)) != HLA_OK) return st;
+  if (pat->pattern != HLA_HILBERT_WINDOW && pat->pattern != HLA_HILBERT_SLIDE &&
+      pat->pattern != HLA_HILBERT_NEIGHBORHOOD && pat->pattern != HLA_HILBERT_SHIFTED_WINDOW)
+    return fail(HLA_ERR_UNSUPPORTED, "hla_attn_fwd_hilbert takes the Hilbert patterns (got %d)",
+                (int)pat->pattern);
+  if (pat->H != pat->W || pat->W < 8 || (pat->W & (pat->W - 1)) != 0)
+    return fail(HLA_ERR_UNSUPPORTED, "hla_attn_fwd_hilbert needs a 2^k x 2^k grid with side >= 8 "
+                "(got %d x %d)", pat->H, pat->W);
+  if (dtype != HLA_BF16) return fail(HLA_ERR_UNSUPPORTED, "hla_attn_fwd_hilbert takes bf16 only");
+  if ((st = check_tiles(tile_m, tile_n)) != HLA_OK) return st;
+  hla_block_mask m;
+  std::memset(&m, 0, sizeof(m));
+  m.N = pat->H * pat->W;
+  m.tile_m = tile_m;
+  m.tile_n = tile_n;
+  m.n_qtiles = (m.N + tile_m - 1) / tile_m;
+  m.n_ktiles = (m.N + tile_n - 1) / tile_n;
+  m.pat = *pat;
+  return attn_fwd(q, k, v, nullptr, nullptr, hla::ATTN_HILBERT, &m, out, lse, B, heads, N, d,
+                  dtype, scale, stream, "hla_attn_fwd_hilbert");
 }
 
 hla_status hla_attn_fwd_rpb(const void *q, const void *k, const void *v, const int32_t *order,

@@ -94,8 +94,11 @@ hipError_t launch_path_and_mask(int32_t side, int32_t *order, int32_t *rank,
 
 // Forward modes: plain (tensors in sequence order), gather (tensors in grid
 // order, sequence position i is row order[i]), rpb (tensors in sequence order,
-// plus the global relative position bias looked up from the grid cells order[i]).
-enum AttnMode { ATTN_PLAIN = 0, ATTN_GATHER = 1, ATTN_RPB = 2 };
+// plus the global relative position bias looked up from the grid cells order[i]),
+// hilbert (as gather, with the rows taken from the Hilbert curve of the 2^lg
+// square and the tile lists classified inside the kernel: no order array, no
+// lists).
+enum AttnMode { ATTN_PLAIN = 0, ATTN_GATHER = 1, ATTN_RPB = 2, ATTN_HILBERT = 3 };
 
 struct AttnArgs {
   const void *q, *k, *v;
@@ -108,6 +111,8 @@ struct AttnArgs {
   int32_t BH, heads, N, n_qtiles, n_ktiles;
   float scale, scale_log2;  // scale, scale * log2(e)
   PatternArgs pat;
+  int32_t lg;               // hilbert: log2 of the grid side (N = 4^lg)
+  int32_t hpw;              // hilbert: heads per workgroup (else 1)
 };
 
 hipError_t launch_attn_bf16(const AttnArgs &a, int d, int tile_m, int tile_n,

@@ -174,6 +174,40 @@ def test_attn_fwd_perm_validation(L):
     assert call(vp(0x800000), m=fake_mask(tm=256, tn=64)) == hla.HLA_ERR_UNSUPPORTED
 
 
+def test_attn_fwd_hilbert_validation(L):
+    """The forward that computes its own Hilbert rows and tile lists takes only the
+    Hilbert patterns on 2^k x 2^k grids, in bf16; every call here is invalid or
+    unsupported, so nothing is launched."""
+    vp = ctypes.c_void_p
+    q, k, v, o = vp(0x100000), vp(0x200000), vp(0x300000), vp(0x400000)
+
+    def call(kind="hilbert_slide", H=64, W=64, p0=128, p1=0, tm=128, tn=64, N=None, d=64,
+             dt=hla.HLA_BF16, out=o):
+        pat = hla.PatternDesc(hla.PATTERN_IDS[kind], H, W, p0, p1)
+        n = H * W if N is None else N
+        return L.hla_attn_fwd_hilbert(q, k, v, ctypes.byref(pat), tm, tn, out, None, 2, 4, n, d,
+                                      dt, 0.125, None)
+
+    def err():
+        return L.hla_last_error().decode()
+
+    assert L.hla_attn_fwd_hilbert(q, k, v, None, 128, 64, o, None, 2, 4, 4096, 64, hla.HLA_BF16,
+                                  0.125, None) == hla.HLA_ERR_INVALID_ARG
+    assert call(kind="rowmajor_window", p0=16, p1=16) == hla.HLA_ERR_UNSUPPORTED and "Hilbert patterns" in err()
+    assert call(kind="rowmajor_slide", p0=4, p1=4) == hla.HLA_ERR_UNSUPPORTED
+    assert call(H=64, W=32) == hla.HLA_ERR_UNSUPPORTED and "2^k" in err()
+    assert call(H=96, W=96) == hla.HLA_ERR_UNSUPPORTED
+    assert call(H=2, W=2, p0=1) == hla.HLA_ERR_UNSUPPORTED
+    assert call(H=4, W=4, p0=4) == hla.HLA_ERR_UNSUPPORTED and ">= 8" in err()
+    assert call(dt=hla.HLA_F32) == hla.HLA_ERR_UNSUPPORTED and "bf16" in err()
+    assert call(N=2048) == hla.HLA_ERR_INVALID_ARG and "built for" in err()
+    assert call(d=48) == hla.HLA_ERR_UNSUPPORTED
+    assert call(tm=64, tn=128) == hla.HLA_ERR_UNSUPPORTED
+    assert call(tm=100) == hla.HLA_ERR_UNSUPPORTED
+    assert call(out=vp(0x100000 + 4096)) == hla.HLA_ERR_INVALID_ARG
+    assert call(kind="hilbert_window", p0=0) == hla.HLA_ERR_INVALID_ARG
+
+
 def test_attn_fwd_rpb_validation(L):
     """Every call here is invalid, so nothing is launched."""
     vp = ctypes.c_void_p

@@ -435,7 +435,8 @@ class LayerPipeline:
 
 
 ATTN_SOURCES = ("paper_2511_05832_amd/csrc/attn_bf16.hip", "paper_2511_05832_amd/csrc/attn_common.h",
-                "paper_2511_05832_amd/csrc/hla_internal.h")
+                "paper_2511_05832_amd/csrc/hla_internal.h", "paper_2511_05832_amd/csrc/hilbert_common.h",
+                "paper_2511_05832_amd/csrc/tiles_common.h")
 PERM_SOURCES = ("paper_2511_05832_amd/csrc/permute.hip", "paper_2511_05832_amd/csrc/hla_internal.h")
 PROJ_SOURCES = ("paper_2511_05832_amd/csrc/proj.hip", "paper_2511_05832_amd/csrc/attn_common.h",
                 "paper_2511_05832_amd/csrc/hla_internal.h")

@@ -250,7 +250,7 @@ hla_status hla_attn_fwd_perm(const void *q, const void *k, const void *v,
  * hla_hilbert_perm -> hla_build_block_mask -> hla_attn_fwd_perm bit for bit.
  * A workgroup serves one query tile for up to 8 consecutive (batch, head)
  * slices, chosen by the library from the pattern's key span and the grid size;
- * the environment variable HLA_HILBERT_HEADS_PER_WORKGROUP (1 .. 64) sets that
+ * the environment variable HLA_ATTN_HEADS_PER_WORKGROUP (1 .. 64) sets that
  * number instead (read at every call; the results do not depend on it).
  * Errors: HLA_ERR_UNSUPPORTED for other patterns, grids or dtypes (use
  * hla_attn_fwd_perm with a precomputed order and mask); otherwise as

@@ -170,6 +170,8 @@ template <int D, int NW, int MODE>
 __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) : (NW == 4 ? 3 : 2))
     attn_fwd_bf16(AttnArgs a) {
   constexpr bool HIL = MODE == ATTN_HILBERT;
+  // one query tile for several heads per workgroup (see the end of the kernel)
+  constexpr bool STREAM = HIL;
   constexpr bool GATHER = MODE == ATTN_GATHER;
   constexpr bool RPB = MODE == ATTN_RPB;
   constexpr bool IDX = GATHER || RPB;
@@ -216,12 +218,18 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 31, half = lane >> 5;
 
-  // (HIL: a workgroup runs its query tile for a.hpw consecutive heads, the
-  // items, starting at head bh.)
+  // (STREAM: a workgroup runs its query tile for one of a.hgroups near-equal
+  // groups of consecutive heads, the items, starting at head bh. The query
+  // tile varies fastest, as in the other modes, so each XCD's contiguous share
+  // of the grid reads the keys of few heads.)
   const int logical = xcd_remap(blockIdx.x, gridDim.x);
   const int grp = logical / a.n_qtiles;
   const int qt = logical - grp * a.n_qtiles;
-  const int bh = HIL ? grp * a.hpw : grp;
+  int bh = grp, nitems = 1;
+  if constexpr (STREAM) {
+    bh = (int)((int64_t)grp * a.BH / a.hgroups);
+    nitems = (int)((int64_t)(grp + 1) * a.BH / a.hgroups) - bh;
+  }
   const int64_t slice = (int64_t)bh * a.N * D;
   const __bf16 *Q = static_cast<const __bf16 *>(a.q) + slice;
   const __bf16 *K = static_cast<const __bf16 *>(a.k) + slice;
@@ -338,8 +346,8 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
     } else {
       const int k0 = tile_of(i) * BN;
       if (k0 + BN <= a.N) {
-        Kt = K + (int64_t)k0 * D;
-        Vt = V + (int64_t)k0 * D;
+        Kt += (int64_t)k0 * D;
+        Vt += (int64_t)k0 * D;
 #pragma unroll
         for (int j = 0; j < CPW; ++j) {
           ko[j] = kin[j];
@@ -565,7 +573,7 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
       }
     }
   };
-  if constexpr (!HIL) {
+  if constexpr (!STREAM) {
     issue_q(Q, 2);
     if constexpr (RPB) {
       if (ntot > 0) issue_idx(0);
@@ -602,7 +610,7 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
     qr1 = __builtin_amdgcn_readfirstlane(box.y);
     qc0 = __builtin_amdgcn_readfirstlane(box.z);
     qc1 = __builtin_amdgcn_readfirstlane(box.w);
-  } else if constexpr (!HIL) {
+  } else if constexpr (!STREAM) {
     // Q and the first key tile are in; the second may still be in flight.
     if (ntot > 1) wait_then_barrier<LPT>();
     else wait_then_barrier<0>();
@@ -616,7 +624,7 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
       qop[c] = *reinterpret_cast<const bf16x8 *>(lds + stg * STAGE + r * D * 2 +
                                                  (((half * NCH + c) ^ swz_q<D>(r)) * 16));
   };
-  if constexpr (!HIL) load_q(2);
+  if constexpr (!STREAM) load_q(2);
 
   // RPB: the bias window of list entry j, issued by one wave: the table entries
   // that this workgroup's queries and entry j's keys can address - the rectangle
@@ -891,15 +899,14 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
     }
   };
 
-  if constexpr (HIL) {
+  if constexpr (STREAM) {
     // The items as one stream of ring copies: item h's Q tile, then its list's
     // key tiles, then item h + 1's. Element e goes into stage e % 3 once every
     // wave has read element e - 3, so the next item's Q tile and first key tile
     // are copied during the current item's last two tiles, and the workgroup's
-    // classification, block table and rows serve every item. The previous
-    // item's rows are stored after the next item's first wait, so that wait
-    // never waits for stores.
-    const int nitems = min(a.hpw, a.BH - bh);
+    // tile list (HIL: its classification, block table and rows) serves every
+    // item. The previous item's rows are stored after the next item's first
+    // wait, so that wait never waits for stores.
     const int64_t ND = (int64_t)a.N * D;
     if (ntot == 0) {
       for (int h = 0; h < nitems; ++h) store_rows(slice + h * ND, bh + h);
@@ -974,15 +981,19 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
   }
 }
 
-// Heads per workgroup of the one-launch path. A workgroup's set-up (the tile
+// Heads per workgroup of the one-launch mode. A workgroup's set-up (the tile
 // classification, the block table and rows, the first copies' latency) is paid
 // once for all its heads, while long workgroups lengthen the tail of the grid:
-// aim at about kHeadsWork key tiles per workgroup (the row's key span in tiles
-// from the pattern), at most 8 heads, and keep at least two workgroups per CU.
-// HLA_HILBERT_HEADS_PER_WORKGROUP (1 .. 64) overrides it.
-constexpr int kHeadsWork = 40;
+// aim at about kHeadsWork key tiles per workgroup (the row's key span in tiles,
+// from the pattern), at most 8 heads, preferring a count that divides B * heads
+// (equal groups: the grid's contiguous shares, one per XCD, then carry equal
+// work), and keep at least two workgroups per CU. HLA_ATTN_HEADS_PER_WORKGROUP
+// (1 .. 64) overrides it. (The plain mode, whose set-up is only its list reads
+// and first copies, gained at most 7% from several heads per workgroup and lost
+// at some counts; it keeps one.)
+constexpr int kHeadsWork = 48;
 int heads_per_workgroup(const AttnArgs &a, int BM) {
-  if (const char *env = std::getenv("HLA_HILBERT_HEADS_PER_WORKGROUP")) {
+  if (const char *env = std::getenv("HLA_ATTN_HEADS_PER_WORKGROUP")) {
     const int h = std::atoi(env);
     if (h >= 1 && h <= 64) return h;
   }
@@ -993,19 +1004,27 @@ int heads_per_workgroup(const AttnArgs &a, int BM) {
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
       cus = 256;
   }
+  // key positions a query may reach: the window, band or neighbourhood
   const int64_t span = a.pat.kind == HLA_HILBERT_SLIDE ? 2 * (int64_t)a.pat.p0 + 1 : (int64_t)a.pat.p0;
   const int64_t tiles = (std::min<int64_t>(span, a.N) + BM + BN - 1) / BN;
   int h = (int)std::max<int64_t>(1, std::min<int64_t>(8, kHeadsWork / tiles));
   h = std::min(h, a.BH);
   while (h > 1 && (int64_t)((a.BH + h - 1) / h) * a.n_qtiles < 2 * (int64_t)cus) --h;
+  for (int d = h; 2 * d > h; --d)
+    if (a.BH % d == 0) return d;
   return h;
 }
 
 template <int D, int NW>
 hipError_t launch(const AttnArgs &a_in, hipStream_t s) {
   AttnArgs a = a_in;
-  a.hpw = a.mode == ATTN_HILBERT ? heads_per_workgroup(a, 32 * NW) : 1;
-  const int64_t blocks = (int64_t)((a.BH + a.hpw - 1) / a.hpw) * a.n_qtiles;
+  if (a.mode == ATTN_HILBERT) {
+    const int h = heads_per_workgroup(a, 32 * NW);
+    a.hgroups = (a.BH + h - 1) / h;  // groups of ceil or floor of BH / hgroups heads
+  } else {
+    a.hgroups = a.BH;
+  }
+  const int64_t blocks = (int64_t)a.hgroups * a.n_qtiles;
   if (a.mode == ATTN_GATHER)
     hipLaunchKernelGGL((attn_fwd_bf16<D, NW, ATTN_GATHER>), dim3((uint32_t)blocks), dim3(64 * NW), 0, s, a);
   else if (a.mode == ATTN_HILBERT)

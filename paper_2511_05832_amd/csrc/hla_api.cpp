@@ -381,7 +381,7 @@ static hla_status attn_fwd(const void *q, const void *k, const void *v, const in
   a.scale_log2 = (float)((double)scale * 1.4426950408889634074);
   a.pat = hla::make_pattern_args(mask->pat);
   a.lg = 0;
-  a.hpw = 1;
+  a.hgroups = (int32_t)BH;
   while ((1 << a.lg) < mask->pat.W) ++a.lg;
   hipError_t e = dtype == HLA_BF16
                      ? hla::launch_attn_bf16(a, (int)d, mask->tile_m, mask->tile_n, (hipStream_t)stream)

@@ -112,7 +112,7 @@ struct AttnArgs {
   float scale, scale_log2;  // scale, scale * log2(e)
   PatternArgs pat;
   int32_t lg;               // hilbert: log2 of the grid side (N = 4^lg)
-  int32_t hpw;              // hilbert: heads per workgroup (else 1)
+  int32_t hgroups;          // hilbert: groups the B * heads slices are split into (else BH)
 };
 
 hipError_t launch_attn_bf16(const AttnArgs &a, int d, int tile_m, int tile_n,

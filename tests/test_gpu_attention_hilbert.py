@@ -102,12 +102,12 @@ def test_full_size_workloads(name):
     (Pat("hilbert_neighborhood", 8, 8, 25), 128, 64),
 ], ids=lambda x: str(x) if isinstance(x, Pat) else None)
 def test_heads_per_workgroup(monkeypatch, hpw, pat, tile_m, d):
-    monkeypatch.setenv("HLA_HILBERT_HEADS_PER_WORKGROUP", str(hpw))
+    monkeypatch.setenv("HLA_ATTN_HEADS_PER_WORKGROUP", str(hpw))
     both(pat, tile_m, 2, 3, d, seed=hpw * 31 + tile_m + d)
 
 
 def test_heads_per_workgroup_without_lse(monkeypatch):
-    monkeypatch.setenv("HLA_HILBERT_HEADS_PER_WORKGROUP", "4")
+    monkeypatch.setenv("HLA_ATTN_HEADS_PER_WORKGROUP", "4")
     pat = Pat("hilbert_slide", 32, 32, 64)
     q, k, v = (t.to(DEV) for t in W.attn_inputs(2, 3, pat.N, 64, "bf16", 5))
     out_a, _ = hla.attn_fwd_hilbert(q, k, v, pat, 128, 64, 0.125)

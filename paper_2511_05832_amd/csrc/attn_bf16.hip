@@ -791,11 +791,16 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
       const bool grow = mt > m_run + kRescaleSlack;
       if (__ballot(grow)) {
         const float m_new = grow ? mt : m_run;
-        // 1 where unchanged; a row with no allowed key yet has nothing to rescale
-        const float alpha = m_new == -__builtin_inff() ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
-        l_run *= alpha;
+        // A row whose reference is still -inf has seen no allowed key: its O
+        // and l are exactly 0. So when no row of the wave has a finite
+        // reference (a row's first tile), the rescale is skipped.
+        if (__ballot(m_run != -__builtin_inff())) {
+          // 1 where unchanged; a row with no allowed key yet has nothing to rescale
+          const float alpha = m_new == -__builtin_inff() ? 1.f : __builtin_amdgcn_exp2f(m_run - m_new);
+          l_run *= alpha;
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
+          for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
+        }
         m_run = m_new;
       }
       ln = weights(s, m_run == -__builtin_inff() ? 0.f : m_run, l_run);

@@ -116,6 +116,18 @@ def test_heads_per_workgroup_without_lse(monkeypatch):
     assert lse_b is None and torch.equal(out_a, out_b)
 
 
+# rows listing more key tiles than the kernel's block table holds (256): the
+# entries past it walk the curve per tile
+@pytest.mark.parametrize("pat,tile_m,d", [(Pat("hilbert_slide", 256, 256, 20000), 128, 32),
+                                          (Pat("hilbert_window", 256, 256, 32768), 64, 32),
+                                          (Pat("hilbert_neighborhood", 256, 256, 40000), 128, 64),
+                                          (Pat("hilbert_shifted_window", 256, 256, 24576, 5000), 128, 32),
+                                          (Pat("hilbert_slide", 512, 512, 9000), 128, 32)],
+                         ids=lambda x: str(x) if isinstance(x, Pat) else None)
+def test_rows_longer_than_the_block_table(pat, tile_m, d):
+    both(pat, tile_m, 1, 1, d, seed=zlib.crc32(repr(pat).encode()) % 1000)
+
+
 def test_layer_attention_shape():
     """The layer's attention: 64x64 grid, band +-64, B=16, 6 heads of 32, 64x64 tiles."""
     both(Pat("hilbert_slide", 64, 64, 64), 64, 16, 6, 32, seed=4, scale=32 ** -0.5)

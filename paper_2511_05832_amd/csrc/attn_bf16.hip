@@ -539,7 +539,12 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
       qoff[j] = row_in((j * NW + wave) / CPR, qt * BM + r) * (uint32_t)(D * 2) +
                 (uint32_t)(cs ^ swz_q<D>(r)) * 16u;
     }
-    wait_then_barrier<0>();
+    // The first item's Q tile into stage 0 now (the first element of the copy
+    // stream below), while wave 0 classifies; the barrier publishes wave 0's
+    // LDS writes and leaves the copies in flight.
+#pragma unroll
+    for (int j = 0; j < LQ; ++j) lds_dma16_at(Q, qoff[j], lds_addr(lds + (j * NW + wave) * 1024));
+    wait_then_barrier<63>();
     nf = __builtin_amdgcn_readfirstlane(runs[0]);
     ntot = __builtin_amdgcn_readfirstlane(runs[1]);
     t_lo = __builtin_amdgcn_readfirstlane(runs[2]);
@@ -914,6 +919,7 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
     // wait, so that wait never waits for stores.
     const int64_t ND = (int64_t)a.N * D;
     if (ntot == 0) {
+      wait_vmem_all();  // the unused Q copies land before the workgroup ends
       for (int h = 0; h < nitems; ++h) store_rows(slice + h * ND, bh + h);
       return;
     }
@@ -921,7 +927,7 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
     // the element read from stage s. Within an item that is its entry it + 2;
     // the item's last two entries hand over to the next item's Q tile and its
     // entry 0.
-    issue_q(Q, 0);
+    // (element 0, the first item's Q tile, went out in the prologue)
     issue_tile(0, 1);
     if (ntot > 1) issue_tile(1, 2);
     else if (nitems > 1) issue_q(Q + ND, 2);

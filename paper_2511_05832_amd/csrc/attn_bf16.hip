@@ -971,6 +971,16 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
         if (ntot > 1) issue_tile(1, nst, ioff);
         else if (h + 1 < nitems) issue_q(Q + ioff + ND, nst);
       }
+      // Waves of the workgroup that has more items left issue first: a CU's
+      // workgroups start together, and the arbiter would otherwise favour the
+      // older one, leaving the younger to finish alone.
+      {
+        const int left = (nitems - h) >> 1;
+        if (left >= 3) __builtin_amdgcn_s_setprio(3);
+        else if (left == 2) __builtin_amdgcn_s_setprio(2);
+        else if (left == 1) __builtin_amdgcn_s_setprio(1);
+        else __builtin_amdgcn_s_setprio(0);
+      }
       if (h > 0) {
         store_rows(slice + ioff - ND, bh + h - 1);
 #pragma unroll

@@ -106,6 +106,18 @@ def test_heads_per_workgroup(monkeypatch, hpw, pat, tile_m, d):
     both(pat, tile_m, 2, 3, d, seed=hpw * 31 + tile_m + d)
 
 
+@pytest.mark.parametrize("value", ["0", "65", "abc", ""])
+def test_heads_per_workgroup_override_out_of_range_is_ignored(monkeypatch, value):
+    pat = Pat("hilbert_window", 32, 32, 64)
+    q, k, v = (t.to(DEV) for t in W.attn_inputs(2, 3, pat.N, 64, "bf16", 9))
+    monkeypatch.delenv("HLA_ATTN_HEADS_PER_WORKGROUP", raising=False)
+    out_a, lse_a = hla.attn_fwd_hilbert(q, k, v, pat, 128, 64, 0.125)
+    monkeypatch.setenv("HLA_ATTN_HEADS_PER_WORKGROUP", value)
+    out_b, lse_b = hla.attn_fwd_hilbert(q, k, v, pat, 128, 64, 0.125)
+    torch.cuda.synchronize()
+    assert torch.equal(out_a, out_b) and torch.equal(lse_a, lse_b)
+
+
 def test_heads_per_workgroup_without_lse(monkeypatch):
     monkeypatch.setenv("HLA_ATTN_HEADS_PER_WORKGROUP", "4")
     pat = Pat("hilbert_slide", 32, 32, 64)

@@ -153,10 +153,10 @@ def perm_record(kernel_ms, nbytes, traffic=None):
 
 def single_ok(w) -> bool:
     """hla_attn_fwd_hilbert covers the workload: a 1-D Hilbert pattern on a 2^k x 2^k
-    grid (side >= 4), bf16."""
+    grid (side >= 8), bf16."""
     p = getattr(w, "pattern", None)
     return (p is not None and p.hilbert and getattr(w, "dtype", "bf16") == "bf16" and p.H == p.W
-            and p.W >= 4 and (p.W & (p.W - 1)) == 0)
+            and p.W >= 8 and (p.W & (p.W - 1)) == 0)
 
 
 class AttnPipeline:
@@ -339,14 +339,19 @@ class AttnPipeline:
 
 
 class LayerPipeline:
-    """The layer step. fused (the default): the QKV projection reads x through the
-    Hilbert order and the output projection writes y through it
-    (hla_qkv_proj_perm, hla_out_proj_perm); otherwise separate gather and scatter
-    passes around hla_qkv_proj and hla_out_proj."""
+    """The layer step. single: the projections work in grid order (hla_qkv_proj,
+    hla_out_proj) around the one-launch attention (hla_attn_fwd_hilbert, which
+    takes its rows from the curve and classifies its tiles itself) - three
+    launches, no index or list in memory. fused: the index and lists in one
+    launch, the QKV projection reading x through the Hilbert order and the output
+    projection writing y through it (hla_qkv_proj_perm, hla_out_proj_perm), the
+    attention in sequence order. Otherwise separate gather and scatter passes
+    around hla_qkv_proj and hla_out_proj."""
 
-    def __init__(self, w: W.LayerWorkload, hla, fused: bool = True):
+    def __init__(self, w: W.LayerWorkload, hla, fused: bool = True, single: bool = False):
         self.w, self.hla = w, hla
-        self.fused = fused
+        self.single = single and single_ok(w)
+        self.fused = fused and not self.single
         self.hilbert = True
         B, N, C, Hh, d = w.B, w.N, w.C, w.heads, w.d
         x, wq, wp = W.layer_inputs(w)
@@ -365,10 +370,22 @@ class LayerPipeline:
         self.order = torch.empty(N, dtype=torch.int32, device="cuda")
         self.rank = torch.empty(N, dtype=torch.int32, device="cuda")
         self.mask = hla.BlockMask(w.pattern, w.tile_m, w.tile_n, totals=False)
+        if self.single:
+            # the step computes its own; these serve the FLOP count
+            self.mask.build_with_path(self.order, self.rank)
         self.timer = Timer()
 
     def step(self, i):
         hla, w, s, T = self.hla, self.w, self.sets[i % self.nsets], self.timer
+        if self.single:
+            with T.stage("qkv"):
+                hla.qkv_proj(s["x"], self.wq, w.heads, outs=(s["q"], s["k"], s["v"]))
+            with T.stage("attn"):
+                hla.attn_fwd_hilbert(s["q"], s["k"], s["v"], w.pattern, w.tile_m, w.tile_n, w.scale,
+                                     out=s["o"], with_lse=False)
+            with T.stage("proj"):
+                hla.out_proj(s["o"], self.wp, out=s["y"])
+            return
         with T.stage("path_mask"):
             self.mask.build_with_path(self.order, self.rank)
         if self.fused:
@@ -399,11 +416,17 @@ class LayerPipeline:
 
         def S(i):
             return self.sets[i % self.nsets]
+
+        def attn(i):
+            if self.single:
+                hla.attn_fwd_hilbert(S(i)["q"], S(i)["k"], S(i)["v"], w.pattern, w.tile_m, w.tile_n, w.scale,
+                                     out=S(i)["o"], with_lse=False)
+            else:
+                hla.attn_fwd(S(i)["q"], S(i)["k"], S(i)["v"], self.mask, w.scale, out=S(i)["o"], with_lse=False)
         calls = {
             "qkv": lambda i: hla.qkv_proj(S(i)["x"], self.wq, w.heads, outs=(S(i)["q"], S(i)["k"], S(i)["v"]),
                                           order=order),
-            "attn": lambda i: hla.attn_fwd(S(i)["q"], S(i)["k"], S(i)["v"], self.mask, w.scale,
-                                           out=S(i)["o"], with_lse=False),
+            "attn": attn,
             "proj": lambda i: hla.out_proj(S(i)["o"], self.wp, out=S(i)["y"], order=order),
             "gather": lambda i: hla.gather(S(i)["x"], self.order, out=S(i)["xh"]),
             "scatter": lambda i: hla.scatter(S(i)["yh"], self.order, out=S(i)["y"]),
@@ -473,7 +496,9 @@ def measured_traffic(workload_name, kernel="attn_fwd"):
 
 
 def make_pipeline(w, hla, fused=False, single=False):
-    return (LayerPipeline(w, hla) if isinstance(w, W.LayerWorkload)
+    """A layer workload gets its default step: one launch for the attention where
+    the pattern allows it, else the reordering fused into the projections."""
+    return (LayerPipeline(w, hla, single=True) if isinstance(w, W.LayerWorkload)
             else AttnPipeline(w, hla, fused, single))
 
 
@@ -767,24 +792,37 @@ def layer_config_record(w, hla, steps, warmup):
     rec["unfused_step"] = {"ms_per_step": ru["ms_per_step"], "ms_per_step_eager": ru["ms_per_step_eager"]}
     del un
     torch.cuda.empty_cache()
-    lp = LayerPipeline(w, hla, fused=True)
+    fused_res = None
+    if single_ok(w):
+        fp = LayerPipeline(w, hla, fused=True)
+        fr = summarize(fp, run_timed(fp, steps, warmup))
+        fused_res = {"ms_per_step": fr["ms_per_step"], "ms_per_step_eager": fr["ms_per_step_eager"],
+                     "attn_kernel_ms": fp.kernel_ms("attn", n)}
+        del fp
+        torch.cuda.empty_cache()
+    lp = LayerPipeline(w, hla, fused=True, single=single_ok(w))
     res = summarize(lp, run_timed(lp, steps, warmup))
     flops, tf, tp = lp.tile_flops()
     kernels = {}
-    for which, name in (("qkv", "qkv_proj_perm"), ("attn", "attn_fwd"), ("proj", "out_proj_perm")):
+    names = (("qkv", "qkv_proj"), ("attn", "attn_fwd_hilbert"), ("proj", "out_proj")) if lp.single else \
+        (("qkv", "qkv_proj_perm"), ("attn", "attn_fwd"), ("proj", "out_proj_perm"))
+    for which, name in names:
         ms = lp.kernel_ms(which, n)
         if which == "attn":
             nb, fl = lp.attn_bytes(), flops
         else:
             nb, fl = lp.proj_figures(which)
         kernels[which] = roofline_record(name, ms, nb, fl, "bf16")
-        kernels[which]["traffic"] = (measured_traffic(w.name, "attn_fwd") if which == "attn" else
-                                     profile_traffic(f"proj_stream_{'qkv' if which == 'qkv' else 'out'}_{w.name}",
-                                                     PROJ_SOURCES))
+        proj_name = f"proj_stream_{'qkv' if which == 'qkv' else 'out'}{'_plain' if lp.single else ''}_{w.name}"
+        kernels[which]["traffic"] = (measured_traffic(w.name, name) if which == "attn" else
+                                     profile_traffic(proj_name, PROJ_SOURCES))
     att = kernels["attn"]["kernel_ms_per_launch"]
     rec.update({
-        "step": "Hilbert index and tile lists (one launch), QKV projection with the gather fused in, "
-                "attention, output projection with the scatter fused in",
+        "step": ("QKV projection, attention with the Hilbert rows and tile lists computed in the kernel "
+                 "(hla_attn_fwd_hilbert), output projection: three launches, all in grid order"
+                 if lp.single else
+                 "Hilbert index and tile lists (one launch), QKV projection with the gather fused in, "
+                 "attention, output projection with the scatter fused in"),
         "ms_per_step": res["ms_per_step"], "ms_per_step_eager": res["ms_per_step_eager"],
         "value": flops / (res["ms_per_step"] * 1e-3) / 1e12, "unit": "TFLOP/s",
         "tiles": {"full": tf, "partial": tp}, "tile_flops": flops,
@@ -794,6 +832,8 @@ def layer_config_record(w, hla, steps, warmup):
         "roofline": max(kernels.values(), key=lambda r: r["kernel_ms_per_launch"]),
         "kernels": kernels, "stages_ms": res["stages_ms"],
     })
+    if fused_res is not None:
+        rec["fused_step"] = fused_res
     del lp
     torch.cuda.empty_cache()
     return rec
@@ -946,6 +986,8 @@ def main():
     res = summarize(pipe, timing)
     if isinstance(w, W.AttnWorkload):
         res["attn_kernel_ms"] = pipe.kernel_ms(max(args.steps, 20))
+    else:
+        res["attn_kernel_ms"] = pipe.kernel_ms("attn", max(args.steps, 20))
     print(f"[bench] {w.name} (composed): {json.dumps(res)}", file=sys.stderr, flush=True)
     bwd = None
     if isinstance(w, W.AttnWorkload) and not args.no_backward:
@@ -985,7 +1027,8 @@ def main():
     elif args.step in ("single", "fused") and res_fused:
         res = res_fused
     ms = res["ms_per_step"]
-    attn_kernel = ("attn_fwd_hilbert" if res is res_single else
+    attn_kernel = ("attn_fwd_hilbert" if res is res_single or getattr(pipe, "single", False) and
+                   isinstance(w, W.LayerWorkload) else
                    "attn_fwd_perm" if res is res_fused else "attn_fwd")
 
     compare = args.compare
@@ -1086,8 +1129,11 @@ def main():
         "config": {"workload": w.name, "description": w.description,
                    "B": w.B, "heads": w.heads, "tokens": w.N, "head_dim": w.d,
                    "tile": [w.tile_m, w.tile_n], "parallelism": "single-gpu"},
-        "step": ("Hilbert index and tile lists (one launch), QKV projection with the gather fused "
-                 "in, attention, output projection with the scatter fused in"
+        "step": (("QKV projection, attention with the Hilbert rows and tile lists computed in the "
+                  "kernel (hla_attn_fwd_hilbert), output projection: three launches, all in grid order"
+                  if getattr(pipe, "single", False) else
+                  "Hilbert index and tile lists (one launch), QKV projection with the gather fused "
+                  "in, attention, output projection with the scatter fused in")
                  if isinstance(w, W.LayerWorkload) else
                  STEP_TEXT[attn_kernel] if attn_kernel != "attn_fwd" else
                  "Hilbert index and tile lists (one launch), gather of q/k/v, attention, scatter of out"

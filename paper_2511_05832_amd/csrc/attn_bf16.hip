@@ -1004,16 +1004,19 @@ __global__ void __launch_bounds__(64 * NW, MODE == ATTN_RPB ? (NW == 4 ? 2 : 1) 
 
 // Heads per workgroup of the one-launch mode. A workgroup's set-up (the tile
 // classification, the block table and rows, the first copies' latency) is paid
-// once for all its heads, while long workgroups lengthen the tail of the grid:
-// aim at about kHeadsWork key tiles per workgroup (the row's key span in tiles,
-// from the pattern), at most 8 heads, preferring a count that divides B * heads
-// (equal groups: the grid's contiguous shares, one per XCD, then carry equal
-// work), and keep at least two workgroups per CU. HLA_ATTN_HEADS_PER_WORKGROUP
+// once for all its heads, while too few workgroups leave resident slots empty
+// and an extra partial round lengthens the tail. With `slots` = CUs x the
+// kernel's resident workgroups per CU, h* = B*heads*query tiles / slots heads
+// per workgroup is exactly one round: take the smallest count >= h* that
+// divides B*heads (equal groups; the grid's contiguous shares, one per XCD,
+// then carry equal work), within kHeadsWork key tiles of work per workgroup
+// (the row's key span in tiles, from the pattern) and 8 heads; else the
+// largest dividing count within that cap. HLA_ATTN_HEADS_PER_WORKGROUP
 // (1 .. 64) overrides it. (The plain mode, whose set-up is only its list reads
-// and first copies, gained at most 7% from several heads per workgroup and lost
-// at some counts; it keeps one.)
+// and first copies, gained at most 7% from several heads per workgroup and
+// lost at some counts; it keeps one.)
 constexpr int kHeadsWork = 48;
-int heads_per_workgroup(const AttnArgs &a, int BM) {
+int heads_per_workgroup(const AttnArgs &a, int BM, int per_cu) {
   if (const char *env = std::getenv("HLA_ATTN_HEADS_PER_WORKGROUP")) {
     const int h = std::atoi(env);
     if (h >= 1 && h <= 64) return h;
@@ -1032,19 +1035,31 @@ int heads_per_workgroup(const AttnArgs &a, int BM) {
   // key positions a query may reach: the window, band or neighbourhood
   const int64_t span = a.pat.kind == HLA_HILBERT_SLIDE ? 2 * (int64_t)a.pat.p0 + 1 : (int64_t)a.pat.p0;
   const int64_t tiles = (std::min<int64_t>(span, a.N) + BM + BN - 1) / BN;
-  int h = (int)std::max<int64_t>(1, std::min<int64_t>(8, kHeadsWork / tiles));
-  h = std::min(h, a.BH);
-  while (h > 1 && (int64_t)((a.BH + h - 1) / h) * a.n_qtiles < 2 * (int64_t)cus) --h;
-  for (int d = h; 2 * d > h; --d)
+  const int cap = (int)std::max<int64_t>(1, std::min<int64_t>(std::min<int64_t>(8, kHeadsWork / tiles), a.BH));
+  const int64_t slots = (int64_t)cus * std::max(per_cu, 1);
+  const int64_t items = (int64_t)a.BH * a.n_qtiles;
+  if (items <= slots) return 1;
+  for (int d = 1; d <= cap; ++d)  // smallest dividing count that fits one round
+    if (a.BH % d == 0 && (int64_t)(a.BH / d) * a.n_qtiles <= slots) return d;
+  for (int d = cap; d > 1; --d)   // else the largest dividing count within the cap
     if (a.BH % d == 0) return d;
-  return h;
+  return 1;
 }
 
 template <int D, int NW>
 hipError_t launch(const AttnArgs &a_in, hipStream_t s) {
   AttnArgs a = a_in;
   if (a.mode == ATTN_HILBERT) {
-    const int h = heads_per_workgroup(a, 32 * NW);
+    // resident workgroups per CU for this kernel, read once per instantiation
+    static int per_cu = 0;
+    if (!per_cu) {
+      int n = 0;
+      per_cu = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                   &n, reinterpret_cast<const void *>(&attn_fwd_bf16<D, NW, ATTN_HILBERT>), 64 * NW, 0) ==
+                           hipSuccess && n > 0
+                   ? n : 1;
+    }
+    const int h = heads_per_workgroup(a, 32 * NW, per_cu);
     a.hgroups = (a.BH + h - 1) / h;  // groups of ceil or floor of BH / hgroups heads
   } else {
     a.hgroups = a.BH;

@@ -52,6 +52,26 @@ def check_layer(w, pooled=False):
     return y
 
 
+def run_layer_one_launch(w, x, wq, wp):
+    """The layer in grid order: QKV projection, the one-launch attention (rows and
+    tile lists from the curve, in the kernel), output projection."""
+    xd, wqd, wpd = x.cuda(), wq.cuda(), wp.cuda()
+    q, k, v = hla.qkv_proj(xd, wqd, w.heads)
+    o, _ = hla.attn_fwd_hilbert(q, k, v, w.pattern, w.tile_m, w.tile_n, w.scale, with_lse=False)
+    y = hla.out_proj(o, wpd)
+    torch.cuda.synchronize()
+    return y.cpu()
+
+
+@pytest.mark.parametrize("name", ["hnt_layer_bf16_64x64_b16_6x32", "small"])
+def test_layer_one_launch_equals_the_reordered_layer(name):
+    """Same arithmetic on the same rows and tiles: bit for bit the layer with
+    separate gather and scatter (itself checked against the oracle above)."""
+    w = W.C5 if name != "small" else W.LayerWorkload("small", 16, 16, 3, 2, 32, 20, 64, 64, 11)
+    x, wq, wp = W.layer_inputs(w)
+    assert torch.equal(run_layer_one_launch(w, x, wq, wp), run_layer(w, x, wq, wp))
+
+
 def test_layer_full_size_every_row():
     """The whole 64 x 64 layer workload (16 x 4096 tokens x 192 features), every row."""
     check_layer(W.C5, pooled=True)

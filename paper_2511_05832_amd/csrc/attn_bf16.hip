@@ -1021,17 +1021,7 @@ int heads_per_workgroup(const AttnArgs &a, int BM, int per_cu) {
     const int h = std::atoi(env);
     if (h >= 1 && h <= 64) return h;
   }
-  // CU count of the current device, read once per device
-  static int cus_of[64] = {0};
-  int dev = 0, cus = 256;
-  if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64) {
-    if (!cus_of[dev]) {
-      int n = 0;
-      cus_of[dev] = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0
-                        ? n : 256;
-    }
-    cus = cus_of[dev];
-  }
+  const int cus = device_cu_count();
   // key positions a query may reach: the window, band or neighbourhood
   const int64_t span = a.pat.kind == HLA_HILBERT_SLIDE ? 2 * (int64_t)a.pat.p0 + 1 : (int64_t)a.pat.p0;
   const int64_t tiles = (std::min<int64_t>(span, a.N) + BM + BN - 1) / BN;

@@ -36,6 +36,8 @@
 // Register-resident weights. The A rows of S (dq: key rows; dkdv: query rows) are
 // fed permuted by row_perm, so the S and dP accumulators come out in the B-operand
 // layout of the next product, and P / dS go to bf16 operands in place.
+#include <algorithm>
+#include <cstdlib>
 #include <type_traits>
 
 #include "attn_common.h"
@@ -331,6 +333,15 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
 // The two query halves of a key block are summed through LDS at the end.
 constexpr int kStagesKv = 2;
 
+// Whether the dk/dv kernel's epilogue LDS (the query halves' exchange, then the
+// rows' staging) fits one ring stage of a BMQ-row query tile.
+template <int D, int BMQ>
+constexpr bool dkdv_streams() {
+  constexpr int stage = 2 * BMQ * D * 2 + BMQ * 8;
+  constexpr int xch = 2 * 2 * (D / 32) * 16 * 64 * 4, rows = 4 * 32 * (D + 8) * 2;
+  return (xch > rows ? xch : rows) <= stage;
+}
+
 template <int D, int BMQ, bool GATHER>
 __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   constexpr int NT = 256;
@@ -357,6 +368,11 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   static_assert(CPW >= 1 && BMQ * CPR % NT == 0, "tile copies must split evenly");
   static_assert(SL <= 64, "stats copies exceed a wave");
   static_assert(4 * SL * 4 == BMQ * 8, "the waves' stats copies cover the tile's rows");
+  // Several heads per workgroup when the epilogue's LDS fits one ring stage (it
+  // then uses the stage the item's last tile left while the other one receives
+  // the next item's first tile); the fused reordering keeps one.
+  constexpr bool STREAMS = !GATHER && dkdv_streams<D, BMQ>();
+  static_assert(!STREAMS || EPI <= STAGE, "the epilogue must fit one stage");
 
   __shared__ __attribute__((aligned(16))) char lds[LDSB];
   const int32_t *idx_k = reinterpret_cast<const int32_t *>(lds + KIDX);
@@ -367,11 +383,22 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   const int col = lane & 31, half = lane >> 5;
   const int kb = wave & 1, qh = wave >> 1;
 
+  // The workgroup runs its key tile for a group of consecutive heads (the
+  // items; one without STREAMS), the key tile fastest in the grid as in the
+  // other kernels.
   const int logical = xcd_remap(blockIdx.x, gridDim.x);
-  const int bh = logical / a.n_ktiles;
-  const int kt = logical - bh * a.n_ktiles;
+  const int grp = logical / a.n_ktiles;
+  const int kt = logical - grp * a.n_ktiles;
+  int bh = grp, nitems = 1;
+  if constexpr (STREAMS) {
+    // groups of q + 1 heads first, then of q (q = BH / hgroups, r = BH % hgroups)
+    const int q = a.BH / a.hgroups, r = a.BH - q * a.hgroups;
+    bh = grp * q + min(grp, r);
+    nitems = q + (grp < r ? 1 : 0);
+  }
   const int k0 = kt * BN;
-  const int64_t slice = (int64_t)bh * a.N * D;
+  const int64_t ND = (int64_t)a.N * D;  // elements per head
+  const int64_t slice = (int64_t)bh * ND;
   const __bf16 *Q = static_cast<const __bf16 *>(a.q) + slice;
   const __bf16 *K = static_cast<const __bf16 *>(a.k) + slice;
   const __bf16 *V = static_cast<const __bf16 *>(a.v) + slice;
@@ -398,11 +425,13 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
     offr[j] = r;
     offc[j] = (cs ^ swz<D>(r)) * 8;
   }
-  // Copies of the query tile of list entry i: Q, dout and the rows' stats
-  // (GATHER: row r of the tile is the row its index slot names).
-  auto issue_tile = [&](int i, int stage) {
+  // Copies of the query tile of list entry i of item h: Q, dout and the rows'
+  // stats (GATHER: row r of the tile is the row its index slot names).
+  auto issue_tile = [&](int i, int stage, int h) {
     char *base = lds + stage * STAGE;
     const int qt = tile_of(i);
+    const __bf16 *Qh = Q + h * ND, *Gh = G + h * ND;
+    const float *Sh = S + 2 * (int64_t)h * a.N;
     int64_t roff[CPW];
     if constexpr (GATHER) {
       const int32_t *rows = idx_q(i);
@@ -414,16 +443,16 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
     }
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
-      lds_dma16(Q + roff[j], lds_addr(base + (j * 4 + wave) * 1024));
+      lds_dma16(Qh + roff[j], lds_addr(base + (j * 4 + wave) * 1024));
 #pragma unroll
     for (int j = 0; j < CPW; ++j)
-      lds_dma16(G + roff[j], lds_addr(base + QT + (j * 4 + wave) * 1024));
+      lds_dma16(Gh + roff[j], lds_addr(base + QT + (j * 4 + wave) * 1024));
     // stats value f of the tile = component f / BMQ of row f % BMQ, so that the
     // stage holds lse log2e of every row, then -delta of every row
     if (lane < SL) {
       const int f = wave * SL + lane, r = f % BMQ;
       const int64_t row = GATHER ? (int64_t)idx_q(i)[r] : (int64_t)min(qt * BMQ + r, a.N - 1);
-      lds_dma4(S + 2 * row + f / BMQ, lds_addr(base + SOFF + wave * SL * 4));
+      lds_dma4(Sh + 2 * row + f / BMQ, lds_addr(base + SOFF + wave * SL * 4));
     }
   };
   // GATHER: the row indices of list entry i (first wave, one per lane) into its
@@ -465,31 +494,44 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
       if (i < ntot) issue_idx(i);
     wait_then_barrier<0>();
   }
-  if (ntot > 0) issue_tile(0, 0);
-  // The wave's own k and v rows, loaded after the first copy so that both
-  // latencies overlap; one wait the compiler can see then covers both, so it
-  // inserts no wait of its own inside the loop.
+  if (ntot > 0) issue_tile(0, 0, 0);
+  // The wave's own k and v rows of item h (the first item's loaded after the
+  // first copy so that both latencies overlap; one wait the compiler can see
+  // then covers both, so it inserts no wait of its own inside the loop).
   // (a key row past the end of the sequence reads row N - 1 and stores nothing)
   const int64_t krow = GATHER ? (int64_t)idx_k[kb * 32 + col] : (int64_t)min(kpos, a.N - 1);
   bf16x8 kop[NCH], vop[NCH];
+  // (byte offset within a head: below 2^31, as N * d <= 2^30)
+  const uint32_t kvoff = (uint32_t)(krow * D + half * (D / 2)) * 2u;
+  auto load_kv = [&](int h) {
+    const char *Kh = reinterpret_cast<const char *>(K + h * ND) + kvoff;
+    const char *Vh = reinterpret_cast<const char *>(V + h * ND) + kvoff;
 #pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    kop[c] = *reinterpret_cast<const bf16x8 *>(K + krow * D + half * (D / 2) + 8 * c);
-    vop[c] = *reinterpret_cast<const bf16x8 *>(V + krow * D + half * (D / 2) + 8 * c);
-  }
+    for (int c = 0; c < NCH; ++c) {
+      kop[c] = *reinterpret_cast<const bf16x8 *>(Kh + 16 * c);
+      vop[c] = *reinterpret_cast<const bf16x8 *>(Vh + 16 * c);
+    }
+  };
+  load_kv(0);
   wait_vmem_all();
 
-  // One query tile; full and partial tiles run separate loop bodies (as in the
-  // dq kernel).
+  // One query tile, list entry it of item h; full and partial tiles run
+  // separate loop bodies (as in the dq kernel). The items' tiles are one
+  // stream through the two-stage ring: each step copies the next tile (the
+  // item's next entry, or the next item's entry 0) into the other stage.
+  int h = 0, cur = 0;  // item, stage of the tile read next
   auto step = [&](int it, auto masked) __attribute__((always_inline)) {
-    const int stage = it % kStagesKv;
+    const int stage = cur;
+    cur ^= 1;
     wait_then_barrier<0>();
-    // (GATHER: entry it + 1's indices arrived with the wait above; entry it + 2's
-    // go out first, into slot (it + 2) % 4, last read for entry it - 2.)
+    // (GATHER, one item: entry it + 1's indices arrived with the wait above;
+    // entry it + 2's go out first, into slot (it + 2) % 4, last read for entry
+    // it - 2.)
     if constexpr (GATHER) {
       if (it + 2 < ntot) issue_idx(it + 2);
     }
-    if (it + 1 < ntot) issue_tile(it + 1, (it + 1) % kStagesKv);
+    if (it + 1 < ntot) issue_tile(it + 1, cur, h);
+    else if (h + 1 < nitems) issue_tile(0, cur, h + 1);
     const char *st = lds + stage * STAGE;
     const int qt = tile_of(it);
 
@@ -549,52 +591,76 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
         dk[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qto, dsop[t], dk[db], 0, 0, 0);
       }
   };
-  int it = 0;
-  for (; it < nf; ++it) step(it, std::false_type{});
-  for (; it < ntot; ++it) step(it, std::true_type{});
+  for (h = 0; h < nitems; ++h) {
+    // (a wait the compiler sees, at every item: it covers the k and v rows
+    // loaded during the previous item's epilogue - and that item's first tile
+    // and stores - so the compiler adds no wait of its own in the tile loop)
+    wait_vmem_all();
+    int it = 0;
+    for (; it < nf; ++it) step(it, std::false_type{});
+    for (; it < ntot; ++it) step(it, std::true_type{});
+    // the next item's k and v rows, in flight during this item's epilogue (the
+    // products no longer read this item's)
+    if (h + 1 < nitems) load_kv(h + 1);
 
-  // Sum the two query halves: half 1 hands its dk to half 0, half 0 hands its dv
-  // to half 1; then half 0 writes dk and half 1 writes dv.
-  wait_then_barrier<0>();
-  float *xch = reinterpret_cast<float *>(lds);
-  auto xidx = [&](int which, int db, int v) {
-    return (((kb * 2 + which) * NDB + db) * 16 + v) * 64 + lane;
-  };
-  // (qh is wave-uniform: one branch around whole loops, not one per element)
-  const int give = qh == 1 ? 0 : 1, keep = 1 - give;
-  if (qh == 1) {
+    // Sum the two query halves: half 1 hands its dk to half 0, half 0 hands its
+    // dv to half 1; then half 0 writes dk and half 1 writes dv. Through the
+    // stage the item's last tile used (the other one may be receiving the next
+    // item's first tile), with barriers that wait for LDS only.
+    char *ep = STREAMS && nitems > 1 ? lds + (cur ^ 1) * STAGE : lds;
+    // (the lane index passed through an empty asm: the epilogue's addresses are
+    // then computed here, per item, instead of being kept in registers across
+    // the loop, where they would be spilled and their reloads would wait for
+    // the copies in flight)
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+    const int lcol = ln & 31, lhalf = ln >> 5;
+    wait_then_barrier<63>();
+    float *xch = reinterpret_cast<float *>(ep);
+    auto xidx = [&](int which, int db, int v) {
+      return (((kb * 2 + which) * NDB + db) * 16 + v) * 64 + ln;
+    };
+    // (qh is wave-uniform: one branch around whole loops, not one per element)
+    const int give = qh == 1 ? 0 : 1, keep = 1 - give;
+    if (qh == 1) {
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
+      for (int db = 0; db < NDB; ++db)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) xch[xidx(give, db, v)] = dk[db][v];
-  } else {
+        for (int v = 0; v < 16; ++v) xch[xidx(give, db, v)] = dk[db][v];
+    } else {
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
+      for (int db = 0; db < NDB; ++db)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) xch[xidx(give, db, v)] = dv[db][v];
+        for (int v = 0; v < 16; ++v) xch[xidx(give, db, v)] = dv[db][v];
+    }
+    wait_then_barrier<63>();
+    f32x16 res[NDB];
+    if (qh == 0) {
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) res[db][v] = dk[db][v] + xch[xidx(keep, db, v)];
+    } else {
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) res[db][v] = dv[db][v] + xch[xidx(keep, db, v)];
+    }
+    wait_then_barrier<63>();
+    __bf16 *Os = reinterpret_cast<__bf16 *>(ep) + wave * 32 * (D + 8);
+    stage_rows<D>(res, qh == 0 ? a.scale : 1.f, Os, lcol, lhalf);
+    wait_then_barrier<63>();
+    __bf16 *dst = static_cast<__bf16 *>(qh == 0 ? a.dk : a.dv) + slice + h * ND;
+    if constexpr (GATHER)
+      write_rows<D>(Os, dst, ln, a.N - (k0 + kb * 32), idx_k + kb * 32);
+    else
+      write_rows<D>(Os, dst + (int64_t)(k0 + kb * 32) * D, ln, a.N - (k0 + kb * 32));
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      dk[db] = f32x16{};
+      dv[db] = f32x16{};
+    }
   }
-  __syncthreads();
-  f32x16 res[NDB];
-  if (qh == 0) {
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) res[db][v] = dk[db][v] + xch[xidx(keep, db, v)];
-  } else {
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) res[db][v] = dv[db][v] + xch[xidx(keep, db, v)];
-  }
-  __syncthreads();
-  __bf16 *Os = reinterpret_cast<__bf16 *>(lds) + wave * 32 * (D + 8);
-  stage_rows<D>(res, qh == 0 ? a.scale : 1.f, Os, col, half);
-  __syncthreads();
-  __bf16 *dst = static_cast<__bf16 *>(qh == 0 ? a.dk : a.dv) + slice;
-  if constexpr (GATHER)
-    write_rows<D>(Os, dst, lane, a.N - (k0 + kb * 32), idx_k + kb * 32);
-  else
-    write_rows<D>(Os, dst + (int64_t)(k0 + kb * 32) * D, lane, a.N - (k0 + kb * 32));
 }
 
 template <int D, int NW>
@@ -607,9 +673,52 @@ hipError_t launch_dq(const AttnBwdArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Heads per dk/dv workgroup (the 1-D patterns; the others keep one). A
+// workgroup's set-up - its k and v rows and the first query tile's latency - is
+// paid once for all its heads, while too few workgroups leave resident slots
+// empty. With `slots` = CUs x resident workgroups per CU: the smallest count
+// dividing B*heads that puts every workgroup in one round, within
+// kHeadsWorkBwd query tiles of work per workgroup (a key's query span from the
+// pattern) and 8 heads; else the largest dividing count within that cap.
+// HLA_ATTN_BWD_HEADS_PER_WORKGROUP (1 .. 64) overrides it.
+constexpr int kHeadsWorkBwd = 72;
+int dkdv_heads_per_workgroup(const AttnBwdArgs &a, int BMQ, int per_cu) {
+  if (const char *env = std::getenv("HLA_ATTN_BWD_HEADS_PER_WORKGROUP")) {
+    const int h = std::atoi(env);
+    if (h >= 1 && h <= 64) return h;
+  }
+  if (!pattern_is_1d(a.pat.kind)) return 1;
+  const int64_t span = a.pat.kind == HLA_HILBERT_SLIDE ? 2 * (int64_t)a.pat.p0 + 1 : (int64_t)a.pat.p0;
+  const int64_t tiles = (std::min<int64_t>(span, a.N) + BN + BMQ - 1) / BMQ;
+  const int cap = (int)std::max<int64_t>(1, std::min<int64_t>(std::min<int64_t>(8, kHeadsWorkBwd / tiles), a.BH));
+  const int64_t slots = (int64_t)device_cu_count() * std::max(per_cu, 1);
+  const int64_t items = (int64_t)a.BH * a.n_ktiles;
+  if (items <= slots) return 1;
+  for (int d = 1; d <= cap; ++d)
+    if (a.BH % d == 0 && (int64_t)(a.BH / d) * a.n_ktiles <= slots) return d;
+  for (int d = cap; d > 1; --d)
+    if (a.BH % d == 0) return d;
+  return 1;
+}
+
 template <int D, int BMQ>
-hipError_t launch_dkdv(const AttnBwdArgs &a, hipStream_t s) {
-  const int64_t blocks = (int64_t)a.BH * a.n_ktiles;
+hipError_t launch_dkdv(const AttnBwdArgs &a_in, hipStream_t s) {
+  AttnBwdArgs a = a_in;
+  a.hgroups = a.BH;
+  if (!a.order && dkdv_streams<D, BMQ>()) {
+    // resident workgroups per CU for this kernel, read once per instantiation
+    static int per_cu = 0;
+    if (!per_cu) {
+      int n = 0;
+      per_cu = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                   &n, reinterpret_cast<const void *>(&attn_bwd_dkdv_bf16<D, BMQ, false>), 256, 0) ==
+                           hipSuccess && n > 0
+                   ? n : 1;
+    }
+    const int h = dkdv_heads_per_workgroup(a, BMQ, per_cu);
+    a.hgroups = (a.BH + h - 1) / h;  // groups of ceil or floor of BH / hgroups heads
+  }
+  const int64_t blocks = (int64_t)a.hgroups * a.n_ktiles;
   if (a.order)
     hipLaunchKernelGGL((attn_bwd_dkdv_bf16<D, BMQ, true>), dim3((uint32_t)blocks), dim3(256), 0, s, a);
   else

@@ -542,6 +542,7 @@ static hla_status attn_bwd(const void *q, const void *k, const void *v, const vo
   a.scale = scale;
   a.scale_log2 = (float)((double)scale * 1.4426950408889634074);
   a.pat = hla::make_pattern_args(mask->pat);
+  a.hgroups = (int32_t)BH;
   hipError_t e =
       dtype == HLA_BF16
           ? hla::launch_attn_bwd_bf16(a, (int)d, mask->tile_m, mask->tile_n, (hipStream_t)stream)

@@ -47,6 +47,20 @@ inline bool pattern_is_1d(int32_t kind) {
          kind == HLA_HILBERT_NEIGHBORHOOD || kind == HLA_HILBERT_SHIFTED_WINDOW;
 }
 
+// Compute units of the current device, read once per device (256 if the query
+// fails).
+inline int device_cu_count() {
+  static int cus_of[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cus_of[dev]) {
+    int n = 0;
+    cus_of[dev] =
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0 ? n : 256;
+  }
+  return cus_of[dev];
+}
+
 inline PatternArgs make_pattern_args(const hla_pattern_desc &p) {
   PatternArgs a;
   a.kind = p.pattern;
@@ -133,6 +147,9 @@ struct AttnBwdArgs {
   int32_t BH, N, n_qtiles, n_ktiles;
   float scale, scale_log2;
   PatternArgs pat;
+  // The heads split into hgroups near-equal groups of consecutive heads, one
+  // group per workgroup and tile (set by each kernel's launcher; BH: one head)
+  int32_t hgroups;
 };
 
 

@@ -281,3 +281,39 @@ def test_growing_scores(pat, tm, dtype, growth):
         err = max_abs(np64(a), r)
         print(f"{pat} {dtype} {name}: err {err:.3e} (scale {gs:.3f})")
         assert err <= TOL_GRAD[dtype] * gs, (name, err, gs)
+
+
+# Several heads per dk/dv workgroup (the launcher picks more than one only when
+# one head per workgroup would overfill the GPU; the override forces it): head
+# counts that do and do not divide B*heads, 1-D and 2-D patterns, the shapes
+# whose epilogue fits one ring stage (128-row query tiles) and one that keeps one
+# head (64-row tiles). The gradients must equal the one-head launch bit for bit.
+@pytest.mark.parametrize("hpw", [2, 3, 5])
+@pytest.mark.parametrize("pat", [Pat("hilbert_window", 32, 32, 64), Pat("hilbert_slide", 32, 32, 100),
+                                 Pat("hilbert_neighborhood", 16, 16, 49),
+                                 Pat("rowmajor_slide", 32, 32, 3, 3)], ids=repr)
+@pytest.mark.parametrize("d,tm", [(64, 128), (32, 128), (64, 64)], ids=str)
+def test_heads_per_workgroup(monkeypatch, hpw, pat, d, tm):
+    q, k, v = W.attn_inputs(2, 3, pat.N, d, "bf16", seed=700 + hpw + d)
+    g = dout_like(q, 800 + tm)
+    scale = d ** -0.5
+    gather = pat.kind.startswith("hilbert")
+    monkeypatch.setenv("HLA_ATTN_BWD_HEADS_PER_WORKGROUP", "1")
+    ref = run_hip(pat, q, k, v, g, tm, 64, scale, gather)
+    monkeypatch.setenv("HLA_ATTN_BWD_HEADS_PER_WORKGROUP", str(hpw))
+    got = run_hip(pat, q, k, v, g, tm, 64, scale, gather)
+    for name, a, b in zip(("dq", "dk", "dv"), got, ref):
+        assert torch.equal(a, b), f"{name} differs with {hpw} heads per workgroup"
+
+
+@pytest.mark.parametrize("value", ["0", "65", "x"])
+def test_heads_per_workgroup_override_out_of_range_is_ignored(monkeypatch, value):
+    pat = Pat("hilbert_window", 32, 32, 64)
+    q, k, v = W.attn_inputs(2, 3, pat.N, 64, "bf16", seed=9)
+    g = dout_like(q, 10)
+    monkeypatch.delenv("HLA_ATTN_BWD_HEADS_PER_WORKGROUP", raising=False)
+    ref = run_hip(pat, q, k, v, g, 128, 64, 0.125)
+    monkeypatch.setenv("HLA_ATTN_BWD_HEADS_PER_WORKGROUP", value)
+    got = run_hip(pat, q, k, v, g, 128, 64, 0.125)
+    for a, b in zip(got, ref):
+        assert torch.equal(a, b)

@@ -370,8 +370,8 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   static_assert(4 * SL * 4 == BMQ * 8, "the waves' stats copies cover the tile's rows");
   // Several heads per workgroup when the epilogue's LDS fits one ring stage (it
   // then uses the stage the item's last tile left while the other one receives
-  // the next item's first tile); the fused reordering keeps one.
-  constexpr bool STREAMS = !GATHER && dkdv_streams<D, BMQ>();
+  // the next item's first tile).
+  constexpr bool STREAMS = dkdv_streams<D, BMQ>();
   static_assert(!STREAMS || EPI <= STAGE, "the epilogue must fit one stage");
 
   __shared__ __attribute__((aligned(16))) char lds[LDSB];
@@ -385,7 +385,7 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
 
   // The workgroup runs its key tile for a group of consecutive heads (the
   // items; one without STREAMS), the key tile fastest in the grid as in the
-  // other kernels.
+  // other kernels. (GATHER: every head has the same rows and lists.)
   const int logical = xcd_remap(blockIdx.x, gridDim.x);
   const int grp = logical / a.n_ktiles;
   const int kt = logical - grp * a.n_ktiles;
@@ -426,15 +426,15 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
     offc[j] = (cs ^ swz<D>(r)) * 8;
   }
   // Copies of the query tile of list entry i of item h: Q, dout and the rows'
-  // stats (GATHER: row r of the tile is the row its index slot names).
-  auto issue_tile = [&](int i, int stage, int h) {
+  // stats (GATHER: row r of the tile is the row index slot `slot` names).
+  auto issue_tile = [&](int i, int stage, int h, int slot) {
     char *base = lds + stage * STAGE;
     const int qt = tile_of(i);
     const __bf16 *Qh = Q + h * ND, *Gh = G + h * ND;
     const float *Sh = S + 2 * (int64_t)h * a.N;
     int64_t roff[CPW];
     if constexpr (GATHER) {
-      const int32_t *rows = idx_q(i);
+      const int32_t *rows = idx_q(slot);
 #pragma unroll
       for (int j = 0; j < CPW; ++j) roff[j] = (int64_t)rows[offr[j]] * D + offc[j];
     } else {
@@ -451,19 +451,30 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
     // stage holds lse log2e of every row, then -delta of every row
     if (lane < SL) {
       const int f = wave * SL + lane, r = f % BMQ;
-      const int64_t row = GATHER ? (int64_t)idx_q(i)[r] : (int64_t)min(qt * BMQ + r, a.N - 1);
+      const int64_t row = GATHER ? (int64_t)idx_q(slot)[r] : (int64_t)min(qt * BMQ + r, a.N - 1);
       lds_dma4(Sh + 2 * row + f / BMQ, lds_addr(base + SOFF + wave * SL * 4));
     }
   };
-  // GATHER: the row indices of list entry i (first wave, one per lane) into its
-  // slot; positions past the end of the sequence read entry N - 1.
-  auto issue_idx = [&](int i) {
+  // GATHER: the row indices of list entry i (first wave, one per lane) into
+  // index slot `slot`; positions past the end of the sequence read entry N - 1.
+  auto issue_idx = [&](int i, int slot) {
     if (wave == 0) {
 #pragma unroll
       for (int c = 0; c < BMQ / 64; ++c)
         lds_dma4(a.order + min(tile_of(i) * BMQ + 64 * c + lane, a.N - 1),
-                 lds_addr(lds + QIDX + (i & 3) * BMQ * 4 + 256 * c));
+                 lds_addr(lds + QIDX + (slot & 3) * BMQ * 4 + 256 * c));
     }
+  };
+  // Element k of the stream after entry it of item h (the items' lists one after
+  // the other): its item hh and entry ii; false past the last item.
+  auto elem = [&](int h, int it, int k, int &hh, int &ii) {
+    hh = h;
+    ii = it + k;
+    while (ii >= ntot) {
+      ii -= ntot;
+      ++hh;
+    }
+    return hh < nitems;
   };
 
   int raddr[QB][NCH];
@@ -485,16 +496,21 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   }
   const float sl2 = a.scale_log2;
 
+  // (GATHER: the element counter e of the stream picks the index slot, e % 4)
   if constexpr (GATHER) {
-    // Row indices of the key tile and of the first two query tiles, first.
+    // Row indices of the key tile and of the stream's first two query tiles,
+    // first.
     if (wave == 0)
       lds_dma4(a.order + min(k0 + lane, a.N - 1), lds_addr(lds + KIDX));
+    if (ntot > 0) {
+      int hh, ii;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-      if (i < ntot) issue_idx(i);
+      for (int k = 0; k < 2; ++k)
+        if (elem(0, 0, k, hh, ii)) issue_idx(ii, k);
+    }
     wait_then_barrier<0>();
   }
-  if (ntot > 0) issue_tile(0, 0, 0);
+  if (ntot > 0) issue_tile(0, 0, 0, 0);
   // The wave's own k and v rows of item h (the first item's loaded after the
   // first copy so that both latencies overlap; one wait the compiler can see
   // then covers both, so it inserts no wait of its own inside the loop).
@@ -519,19 +535,19 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
   // separate loop bodies (as in the dq kernel). The items' tiles are one
   // stream through the two-stage ring: each step copies the next tile (the
   // item's next entry, or the next item's entry 0) into the other stage.
-  int h = 0, cur = 0;  // item, stage of the tile read next
+  int h = 0, cur = 0, e = 0;  // item, stage of the tile read next, its element
   auto step = [&](int it, auto masked) __attribute__((always_inline)) {
     const int stage = cur;
     cur ^= 1;
     wait_then_barrier<0>();
-    // (GATHER, one item: entry it + 1's indices arrived with the wait above;
-    // entry it + 2's go out first, into slot (it + 2) % 4, last read for entry
-    // it - 2.)
+    // (GATHER: element e + 1's indices arrived with the wait above; element
+    // e + 2's go out first, into slot (e + 2) % 4, last read for element e - 2.)
+    int hh, ii;
     if constexpr (GATHER) {
-      if (it + 2 < ntot) issue_idx(it + 2);
+      if (elem(h, it, 2, hh, ii)) issue_idx(ii, e + 2);
     }
-    if (it + 1 < ntot) issue_tile(it + 1, cur, h);
-    else if (h + 1 < nitems) issue_tile(0, cur, h + 1);
+    if (elem(h, it, 1, hh, ii)) issue_tile(ii, cur, hh, e + 1);
+    ++e;
     const char *st = lds + stage * STAGE;
     const int qt = tile_of(it);
 
@@ -705,17 +721,17 @@ template <int D, int BMQ>
 hipError_t launch_dkdv(const AttnBwdArgs &a_in, hipStream_t s) {
   AttnBwdArgs a = a_in;
   a.hgroups = a.BH;
-  if (!a.order && dkdv_streams<D, BMQ>()) {
-    // resident workgroups per CU for this kernel, read once per instantiation
-    static int per_cu = 0;
-    if (!per_cu) {
+  if (dkdv_streams<D, BMQ>()) {
+    // resident workgroups per CU for each kernel, read once per instantiation
+    static int per_cu[2] = {0, 0};
+    const int g = a.order ? 1 : 0;
+    if (!per_cu[g]) {
       int n = 0;
-      per_cu = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                   &n, reinterpret_cast<const void *>(&attn_bwd_dkdv_bf16<D, BMQ, false>), 256, 0) ==
-                           hipSuccess && n > 0
-                   ? n : 1;
+      const void *f = a.order ? reinterpret_cast<const void *>(&attn_bwd_dkdv_bf16<D, BMQ, true>)
+                              : reinterpret_cast<const void *>(&attn_bwd_dkdv_bf16<D, BMQ, false>);
+      per_cu[g] = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, f, 256, 0) == hipSuccess && n > 0 ? n : 1;
     }
-    const int h = dkdv_heads_per_workgroup(a, BMQ, per_cu);
+    const int h = dkdv_heads_per_workgroup(a, BMQ, per_cu[g]);
     a.hgroups = (a.BH + h - 1) / h;  // groups of ceil or floor of BH / hgroups heads
   }
   const int64_t blocks = (int64_t)a.hgroups * a.n_ktiles;

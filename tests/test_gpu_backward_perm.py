@@ -103,3 +103,23 @@ def test_rejects_wrong_order_length():
     mask = hla.build_block_mask(pat, 64, 64, columns=True)
     with pytest.raises(hla.HLAError):
         hla.attn_bwd_perm(q, q, q, q, q, lse, torch.arange(pat.N - 1, dtype=torch.int32, device=DEV), mask)
+
+
+# Several heads per dk/dv workgroup in both launches (the override applies to
+# the fused and the plain kernel): head counts that do and do not divide
+# B*heads, ragged and whole tilings, Hilbert and random orders. The fused launch
+# must still equal gather -> attn_bwd -> scatter bit for bit, and the plain one
+# the one-head launch.
+@pytest.mark.parametrize("hpw", [2, 3, 5])
+@pytest.mark.parametrize("pat,d,tm,order_kind", [
+    (Pat("hilbert_window", 32, 32, 64), 64, 128, "hilbert"),
+    (Pat("hilbert_slide", 32, 32, 300), 32, 128, "hilbert"),
+    (Pat("rowmajor_slide", 20, 30, 3, 4), 64, 128, "random"),
+], ids=str)
+def test_heads_per_workgroup(monkeypatch, hpw, pat, d, tm, order_kind):
+    monkeypatch.setenv("HLA_ATTN_BWD_HEADS_PER_WORKGROUP", "1")
+    _, _, ref, _ = run(pat, 2, 3, d, "bf16", tm, 40 + hpw, order_kind)
+    monkeypatch.setenv("HLA_ATTN_BWD_HEADS_PER_WORKGROUP", str(hpw))
+    _, _, got, _ = run(pat, 2, 3, d, "bf16", tm, 40 + hpw, order_kind)
+    for name, a, b in zip(("dq", "dk", "dv"), got, ref):
+        assert torch.equal(a, b), f"{name} differs with {hpw} heads per workgroup"

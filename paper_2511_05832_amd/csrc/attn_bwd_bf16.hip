@@ -111,7 +111,7 @@ __device__ __forceinline__ void write_rows(const __bf16 *Os, __bf16 *dst, int la
 constexpr int kStagesDq = 3;
 
 template <int D, int NW, bool GATHER>
-__global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
+__global__ void __launch_bounds__(64 * NW, 3) attn_bwd_dq_bf16(AttnBwdArgs a) {
   constexpr int BM = 32 * NW;
   constexpr int NT = 64 * NW;
   constexpr int CPR = D / 8;
@@ -276,34 +276,33 @@ __global__ void __launch_bounds__(64 * NW, 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
     const char *st = lds + stage * STAGE;
     const int kt = tile_of(it);
 
-    f32x16 s[2] = {f32x16{}, f32x16{}}, dp[2] = {f32x16{}, f32x16{}};
+    // the tile's two 32-key blocks one after the other (half the score
+    // registers of both at once)
 #pragma unroll
-    for (int c = 0; c < NCH; ++c)
+    for (int kb = 0; kb < 2; ++kb) {
+      f32x16 s[1] = {f32x16{}}, dp = f32x16{};
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+      for (int c = 0; c < NCH; ++c) {
         const bf16x8 kop = *reinterpret_cast<const bf16x8 *>(st + raddr[kb][c]);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[c], s[kb], 0, 0, 0);
+        s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[c], s[0], 0, 0, 0);
         const bf16x8 vop = *reinterpret_cast<const bf16x8 *>(st + TILE + raddr[kb][c]);
-        dp[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, gop[c], dp[kb], 0, 0, 0);
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, gop[c], dp, 0, 0, 0);
       }
-    if constexpr (decltype(masked)::value) mask_blocks<2>(s, R, P, kt * BN + 8 * half);
-
-    bf16x8 dsop[4];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      if constexpr (decltype(masked)::value) mask_blocks<1>(s, R, P, kt * BN + 32 * kb + 8 * half);
+      bf16x8 dsop[2];
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(s[kb][v] * sl2 - lse2);
-        dsop[kb * 2 + (v >> 3)][v & 7] = (__bf16)(p * (dp[kb][v] - delta));
+        const float p = __builtin_amdgcn_exp2f(s[0][v] * sl2 - lse2);
+        dsop[v >> 3][v & 7] = (__bf16)(p * (dp[v] - delta));
       }
-
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        const bf16x8 kto = lds_read_tr16x2(st + tbase[db] + (16 * t) * D * 2, D * 2);
-        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kto, dsop[t], acc[db], 0, 0, 0);
-      }
+        for (int db = 0; db < NDB; ++db) {
+          const bf16x8 kto = lds_read_tr16x2(st + tbase[db] + (16 * (2 * kb + t)) * D * 2, D * 2);
+          acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kto, dsop[t], acc[db], 0, 0, 0);
+        }
+    }
   };
   int it = 0;
   for (; it < nf; ++it) step(it, std::false_type{});

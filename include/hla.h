@@ -306,6 +306,11 @@ hla_status hla_attn_fwd_rpb(const void *q, const void *k, const void *v,
  * fixed summation order (no atomics).
  * bf16: products on bf16 matrix cores with P and dS rounded to bf16 as
  * operands, fp32 accumulation, gradients rounded to bf16. f32: fp32 throughout.
+ * With bf16 and tile_m == 128 a dk/dv workgroup may run its key tile for up
+ * to 8 consecutive heads in turn (chosen from the GPU's size and the pattern;
+ * the environment variable HLA_ATTN_BWD_HEADS_PER_WORKGROUP (1 .. 64) sets
+ * that count, read at every call); the results do not depend on it. The same
+ * holds for hla_attn_bwd_perm and hla_attn_bwd_noalloc.
  * Supported: d in {32, 64}; tile_m in {64, 128}; tile_n == 64;
  * otherwise UNSUPPORTED.
  */

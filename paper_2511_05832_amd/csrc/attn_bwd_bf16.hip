@@ -465,10 +465,12 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
     }
   };
   // Element k of the stream after entry it of item h (the items' lists one after
-  // the other): its item hh and entry ii; false past the last item.
+  // the other): its item hh and entry ii; false past the last item (and for an
+  // empty list).
   auto elem = [&](int h, int it, int k, int &hh, int &ii) {
     hh = h;
     ii = it + k;
+    if (ntot <= 0) return false;
     while (ii >= ntot) {
       ii -= ntot;
       ++hh;

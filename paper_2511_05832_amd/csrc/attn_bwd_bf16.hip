@@ -90,8 +90,10 @@ template <int D>
 __device__ __forceinline__ void write_rows(const __bf16 *Os, __bf16 *dst, int lane, int nrows,
                                            const int32_t *rows = nullptr) {
   constexpr int OS = D + 8, CPR = D / 8;
+  static_assert(32 * CPR % 64 == 0, "the rows' chunks split evenly over the lanes");
 #pragma unroll
-  for (int i = lane; i < 32 * CPR; i += 64) {
+  for (int k = 0; k < 32 * CPR / 64; ++k) {
+    const int i = lane + 64 * k;
     const int r = i / CPR, c = i % CPR;
     if (r < nrows) {
       const int64_t row = rows ? (int64_t)rows[r] : (int64_t)r;
@@ -111,7 +113,7 @@ __device__ __forceinline__ void write_rows(const __bf16 *Os, __bf16 *dst, int la
 constexpr int kStagesDq = 3;
 
 template <int D, int NW, bool GATHER>
-__global__ void __launch_bounds__(64 * NW, 3) attn_bwd_dq_bf16(AttnBwdArgs a) {
+__global__ void __launch_bounds__(64 * NW, NW == 4 ? 3 : 2) attn_bwd_dq_bf16(AttnBwdArgs a) {
   constexpr int BM = 32 * NW;
   constexpr int NT = 64 * NW;
   constexpr int CPR = D / 8;
@@ -505,7 +507,6 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dkdv_bf16(AttnBwdArgs a) {
       lds_dma4(a.order + min(k0 + lane, a.N - 1), lds_addr(lds + KIDX));
     if (ntot > 0) {
       int hh, ii;
-#pragma unroll
       for (int k = 0; k < 2; ++k)
         if (elem(0, 0, k, hh, ii)) issue_idx(ii, k);
     }

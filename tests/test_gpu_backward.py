@@ -285,10 +285,11 @@ def test_growing_scores(pat, tm, dtype, growth):
 
 # Several heads per dk/dv workgroup (the launcher picks more than one only when
 # one head per workgroup would overfill the GPU; the override forces it): head
-# counts that do and do not divide B*heads, 1-D and 2-D patterns, the shapes
-# whose epilogue fits one ring stage (128-row query tiles) and one that keeps one
-# head (64-row tiles). The gradients must equal the one-head launch bit for bit.
-@pytest.mark.parametrize("hpw", [2, 3, 5])
+# counts that do and do not divide B*heads and one above it (every head in one
+# workgroup), 1-D and 2-D patterns, the shapes whose epilogue fits one ring stage
+# (128-row query tiles) and one that keeps one head (64-row tiles). The
+# gradients must equal the one-head launch bit for bit.
+@pytest.mark.parametrize("hpw", [2, 3, 5, 8])
 @pytest.mark.parametrize("pat", [Pat("hilbert_window", 32, 32, 64), Pat("hilbert_slide", 32, 32, 100),
                                  Pat("hilbert_neighborhood", 16, 16, 49),
                                  Pat("rowmajor_slide", 32, 32, 3, 3)], ids=repr)

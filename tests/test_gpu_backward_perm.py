@@ -107,10 +107,10 @@ def test_rejects_wrong_order_length():
 
 # Several heads per dk/dv workgroup in both launches (the override applies to
 # the fused and the plain kernel): head counts that do and do not divide
-# B*heads, ragged and whole tilings, Hilbert and random orders. The fused launch
+# B*heads and one above it, ragged and whole tilings, Hilbert and random orders. The fused launch
 # must still equal gather -> attn_bwd -> scatter bit for bit, and the plain one
 # the one-head launch.
-@pytest.mark.parametrize("hpw", [2, 3, 5])
+@pytest.mark.parametrize("hpw", [2, 3, 5, 8])
 @pytest.mark.parametrize("pat,d,tm,order_kind", [
     (Pat("hilbert_window", 32, 32, 64), 64, 128, "hilbert"),
     (Pat("hilbert_slide", 32, 32, 300), 32, 128, "hilbert"),
